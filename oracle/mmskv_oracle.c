@@ -1,0 +1,592 @@
+/*
+ * mmskv_oracle.c -- plain, slow fp64 CPU oracle for MM-ShiftKV prefill-stage
+ * KV scoring and selection.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no code, header, table or constant generator
+ * with the HIP library: every step is written out here from the paper
+ * (MM-ShiftKV, arxiv 2607.22586) and from the published definitions of the
+ * counter-based generator, in plain loops, double precision, one row at a
+ * time, with no blocking, fusion or reordering beyond what the definitions
+ * state.
+ *
+ * Readings of the paper that this file adopts (each is a choice where the
+ * paper is silent or ambiguous):
+ *   - Statistics are taken in query space over the W given window queries of
+ *     each (batch, query head), per feature dimension (Sec. 3.2.1 Eq. 4 takes
+ *     element-wise mean/std; Appendix A.4 Eq. 15 states the proxy law in
+ *     query space).  std uses divisor (W - ddof), ddof = 0 by default.
+ *   - Sampling uses a diagonal Gaussian, x = mu + (gamma*sigma)*z, i.e. gamma
+ *     multiplies the standard deviation (Sec. 3.2.1 Eq. 5, diag((gamma sigma)^2)).
+ *   - Noise z is independent per (batch, layer, query head, proxy, dim).
+ *   - Optional rotary embedding uses caller tables (rotate-half pairing j,
+ *     j+d/2) for one synthetic future position (Sec. 3.2.1, last paragraph).
+ *   - Proxies are rounded fp64 -> fp32 -> bf16 (round to nearest even);
+ *     scoring keys are rounded fp32 -> bf16 the same way; the logits are then
+ *     computed in fp64 on those bf16 values (mixed-precision inference,
+ *     Sec. 4.1 "Implementation and Hyperparameters").
+ *   - Softmax over all T prompt keys, scale 1/sqrt(head_dim) (Sec. 3.2.2 Eq. 7).
+ *   - Groups are contiguous proxy blocks I_g = {g*P/G .. (g+1)*P/G - 1}
+ *     (Sec. 3.2.2 Eq. 8 leaves the partition open).
+ *   - GQA: the masses of the query heads that share a KV head are summed
+ *     inside each group before the tau-set is formed (Appendix B; Sec. 4.1).
+ *   - tau-set: keys ordered by (group mass desc, index asc); the shortest
+ *     prefix whose running sum is >= tau * (sum of all keys in that same
+ *     order) (Sec. 3.2.2 Eq. 9 uses >=).
+ *   - Anchor: the mean over the GQA group of the softmax of each query head's
+ *     last window query (Sec. 3.2.3 Eq. 11), so the anchor never exceeds one
+ *     vote step.  Score = vote + lambda*anchor in fp64.
+ *   - Selection: if T <= C keep all; else keep token T-1 plus the top C-1 of
+ *     [0, T-1) by (score desc, index asc); output in ascending index order
+ *     (Sec. 3.2.3; Appendix B; Algorithm 1).
+ *
+ * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (see build.py).
+ * The -ffp-contract=off flag keeps every a*b+c as two rounded operations,
+ * which the counter-based normal generator below relies on.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------ */
+/* Counter-based generator: Philox4x32-10 (Salmon, Moraes, Dror, Shaw,       */
+/* "Parallel random numbers: as easy as 1, 2, 3", SC 2011).                  */
+/* One round maps counter (c0,c1,c2,c3) with key (k0,k1) to                  */
+/*   (hi(M1*c2) ^ c1 ^ k0, lo(M1*c2), hi(M0*c0) ^ c3 ^ k1, lo(M0*c0)),       */
+/* M0 = 0xD2511F53, M1 = 0xCD9E8D57; the key is bumped by the Weyl constants */
+/* (0x9E3779B9, 0xBB67AE85) between rounds; ten rounds.                      */
+/* ------------------------------------------------------------------------ */
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        uint64_t prod0 = (uint64_t)0xD2511F53u * (uint64_t)c0;
+        uint64_t prod1 = (uint64_t)0xCD9E8D57u * (uint64_t)c2;
+        uint32_t hi0 = (uint32_t)(prod0 >> 32), lo0 = (uint32_t)prod0;
+        uint32_t hi1 = (uint32_t)(prod1 >> 32), lo1 = (uint32_t)prod1;
+        uint32_t n0 = hi1 ^ c1 ^ k0;
+        uint32_t n1 = lo1;
+        uint32_t n2 = hi0 ^ c3 ^ k1;
+        uint32_t n3 = lo0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* A 32-bit word x -> uniform (2*(x>>9) + 1) * 2^-24, exactly representable,
+ * strictly inside (0, 1). */
+double oracle_uniform(uint32_t x)
+{
+    return (double)(2u * (x >> 9) + 1u) * (1.0 / 16777216.0);
+}
+
+/* Natural logarithm for u in (0,1), written from the series
+ *   ln m = 2 * sum_k s^(2k+1) / (2k+1),  s = (m-1)/(m+1),
+ * after splitting u = m * 2^e with m in [sqrt(1/2), sqrt(2)).  Twelve terms
+ * (|s| <= 0.1716 makes the next term < 1e-20).  Horner form, plain mul/add. */
+double oracle_ln(double u)
+{
+    int e;
+    double f = frexp(u, &e);               /* u = f * 2^e, f in [0.5, 1) */
+    double m = f;
+    if (f < 0.70710678118654752440) {      /* sqrt(1/2) */
+        m = 2.0 * f;
+        e = e - 1;
+    }
+    double s = (m - 1.0) / (m + 1.0);
+    double s2 = s * s;
+    double poly = 1.0 / 23.0;
+    for (int k = 10; k >= 0; --k) {
+        poly = poly * s2;
+        poly = poly + 1.0 / (double)(2 * k + 1);
+    }
+    double ln_m = 2.0 * s;
+    ln_m = ln_m * poly;
+    double ln2 = 0.69314718055994530942;   /* nearest double to ln 2 */
+    double eln2 = (double)e * ln2;
+    return eln2 + ln_m;
+}
+
+/* sin and cos of 2*pi*u for u in (0,1): the quarter-turn q nearest to 4u is
+ * removed exactly, the remainder f in [-1/8, 1/8] is scaled by 2*pi, and the
+ * Taylor series (sin to phi^21, cos to phi^20, coefficients by repeated
+ * division) are evaluated in Horner form; the quarter turns are then
+ * restored by the usual quadrant identities. */
+void oracle_sincos_2pi(double u, double *sin_out, double *cos_out)
+{
+    double four_u = 4.0 * u;
+    int q = (int)floor(four_u + 0.5);
+    double f = u - (double)q * 0.25;
+    double two_pi = 6.28318530717958647692;
+    double phi = f * two_pi;
+    double p2 = phi * phi;
+
+    double cs[11], cc[11];
+    cs[0] = 1.0;
+    cc[0] = 1.0;
+    for (int k = 1; k <= 10; ++k) {
+        cs[k] = -cs[k - 1] / (double)((2 * k) * (2 * k + 1));
+        cc[k] = -cc[k - 1] / (double)((2 * k - 1) * (2 * k));
+    }
+    double ps = cs[10], pc = cc[10];
+    for (int k = 9; k >= 0; --k) {
+        ps = ps * p2;
+        ps = ps + cs[k];
+        pc = pc * p2;
+        pc = pc + cc[k];
+    }
+    double sp = phi * ps;
+    double cp = pc;
+    switch (q & 3) {
+    case 0: *sin_out = sp;  *cos_out = cp;  break;
+    case 1: *sin_out = cp;  *cos_out = -sp; break;
+    case 2: *sin_out = -sp; *cos_out = -cp; break;
+    default: *sin_out = -cp; *cos_out = sp; break;
+    }
+}
+
+/* Standard normals for dims 4*jq .. 4*jq+3 of proxy i of query head h,
+ * batch b, layer l: Philox counter (jq, i, h, (b<<16)|l), key = seed split in
+ * two 32-bit halves; uniforms (u0,u1) and (u2,u3) each give one Box-Muller
+ * pair (Box & Muller 1958): r = sqrt(-2 ln u_a), z = (r cos 2pi u_b,
+ * r sin 2pi u_b). */
+void oracle_normal4(uint64_t seed, int b, int layer, int h, int i, int jq, double z[4])
+{
+    uint32_t ctr[4] = {(uint32_t)jq, (uint32_t)i, (uint32_t)h,
+                       ((uint32_t)b << 16) | ((uint32_t)layer & 0xFFFFu)};
+    uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+    uint32_t x[4];
+    oracle_philox4x32_10(ctr, key, x);
+    for (int pair = 0; pair < 2; ++pair) {
+        double ua = oracle_uniform(x[2 * pair]);
+        double ub = oracle_uniform(x[2 * pair + 1]);
+        double r = sqrt(-2.0 * oracle_ln(ua));
+        double sn, cs;
+        oracle_sincos_2pi(ub, &sn, &cs);
+        z[2 * pair] = r * cs;
+        z[2 * pair + 1] = r * sn;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* bf16 helpers (round to nearest even; NaN is not expected in inputs).      */
+/* ------------------------------------------------------------------------ */
+uint16_t oracle_f32_to_bf16(float x)
+{
+    uint32_t bits;
+    memcpy(&bits, &x, 4);
+    uint32_t lsb = (bits >> 16) & 1u;
+    bits = bits + 0x7FFFu + lsb;
+    return (uint16_t)(bits >> 16);
+}
+
+double oracle_bf16_to_f64(uint16_t h)
+{
+    uint32_t bits = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &bits, 4);
+    return (double)f;
+}
+
+/* dtype codes: 0 = fp32, 1 = bf16 (raw 16-bit patterns). */
+static double load_elem(const void *base, int dtype, int64_t off)
+{
+    if (dtype == 0)
+        return (double)((const float *)base)[off];
+    return oracle_bf16_to_f64(((const uint16_t *)base)[off]);
+}
+
+/* Scoring value of a key element: fp32 keys are first rounded to bf16. */
+static double load_key_bf16(const void *base, int dtype, int64_t off)
+{
+    if (dtype == 0)
+        return oracle_bf16_to_f64(oracle_f32_to_bf16(((const float *)base)[off]));
+    return oracle_bf16_to_f64(((const uint16_t *)base)[off]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Step 1 -- proxies (Sec. 3.2.1 Eqs. 4-5, Appendix A.4 Eq. 15).             */
+/* ------------------------------------------------------------------------ */
+/*
+ * q_win      [B, Hq, W, d] contiguous, dtype 0/1
+ * rope_cos_f / rope_sin_f: [d/2] fp32 tables for the proxies' future
+ *            position, or NULL (no rotary embedding)
+ * rope_cos_l / rope_sin_l: [d/2] fp32 tables for the last query's position
+ *            (used for the anchor query), or NULL
+ * proxies    [B, Hq, P, d] bf16 out;  q_last [B, Hq, d] bf16 out
+ * stats      [B, Hq, 2, d] fp64 out (mu, sigma), may be NULL
+ * returns 0, or -1 on invalid arguments
+ */
+int oracle_build_proxies(int B, int Hq, int W, int d, int P, double gamma, int ddof,
+                         uint64_t seed, int layer, const void *q_win, int dtype,
+                         const float *rope_cos_f, const float *rope_sin_f,
+                         const float *rope_cos_l, const float *rope_sin_l,
+                         uint16_t *proxies, uint16_t *q_last, double *stats)
+{
+    if (B < 1 || Hq < 1 || W < 1 || d < 4 || (d % 4) != 0 || P < 1 || W - ddof < 1 ||
+        ddof < 0 || layer < 0 || layer > 0xFFFF || B > 0xFFFF)
+        return -1;
+    int use_rope = (rope_cos_f != NULL && rope_sin_f != NULL);
+    int use_rope_last = (rope_cos_l != NULL && rope_sin_l != NULL);
+    int half = d / 2;
+
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int h = 0; h < Hq; ++h) {
+            double *mu = (double *)malloc(sizeof(double) * (size_t)d);
+            double *sg = (double *)malloc(sizeof(double) * (size_t)d);
+            double *x = (double *)malloc(sizeof(double) * (size_t)d);
+            int64_t qbase = ((int64_t)b * Hq + h) * (int64_t)W * d;
+            /* mean and std over the window, per dimension, summed in order */
+            for (int j = 0; j < d; ++j) {
+                double acc = 0.0;
+                for (int w = 0; w < W; ++w)
+                    acc = acc + load_elem(q_win, dtype, qbase + (int64_t)w * d + j);
+                double m = acc / (double)W;
+                double sq = 0.0;
+                for (int w = 0; w < W; ++w) {
+                    double diff = load_elem(q_win, dtype, qbase + (int64_t)w * d + j) - m;
+                    double dd = diff * diff;
+                    sq = sq + dd;
+                }
+                double var = sq / (double)(W - ddof);
+                mu[j] = m;
+                sg[j] = sqrt(var);
+            }
+            if (stats) {
+                double *st = stats + ((int64_t)b * Hq + h) * 2 * d;
+                for (int j = 0; j < d; ++j) {
+                    st[j] = mu[j];
+                    st[d + j] = sg[j];
+                }
+            }
+            /* proxies */
+            for (int i = 0; i < P; ++i) {
+                for (int jq = 0; jq < d / 4; ++jq) {
+                    double z[4];
+                    oracle_normal4(seed, b, layer, h, i, jq, z);
+                    for (int e = 0; e < 4; ++e) {
+                        int j = 4 * jq + e;
+                        double gs = gamma * sg[j];
+                        double t = gs * z[e];
+                        x[j] = mu[j] + t;
+                    }
+                }
+                uint16_t *out = proxies + (((int64_t)b * Hq + h) * P + i) * d;
+                if (use_rope) {
+                    for (int j = 0; j < half; ++j) {
+                        double c = (double)rope_cos_f[j], s = (double)rope_sin_f[j];
+                        double a0 = x[j] * c, a1 = x[j + half] * s;
+                        double b0 = x[j + half] * c, b1 = x[j] * s;
+                        double lo = a0 - a1, hi = b0 + b1;
+                        out[j] = oracle_f32_to_bf16((float)lo);
+                        out[j + half] = oracle_f32_to_bf16((float)hi);
+                    }
+                } else {
+                    for (int j = 0; j < d; ++j)
+                        out[j] = oracle_f32_to_bf16((float)x[j]);
+                }
+            }
+            /* anchor query: the last window query of this head */
+            {
+                for (int j = 0; j < d; ++j)
+                    x[j] = load_elem(q_win, dtype, qbase + (int64_t)(W - 1) * d + j);
+                uint16_t *out = q_last + ((int64_t)b * Hq + h) * d;
+                if (use_rope_last) {
+                    for (int j = 0; j < half; ++j) {
+                        double c = (double)rope_cos_l[j], s = (double)rope_sin_l[j];
+                        double a0 = x[j] * c, a1 = x[j + half] * s;
+                        double b0 = x[j + half] * c, b1 = x[j] * s;
+                        double lo = a0 - a1, hi = b0 + b1;
+                        out[j] = oracle_f32_to_bf16((float)lo);
+                        out[j + half] = oracle_f32_to_bf16((float)hi);
+                    }
+                } else {
+                    for (int j = 0; j < d; ++j)
+                        out[j] = oracle_f32_to_bf16((float)x[j]);
+                }
+            }
+            free(mu);
+            free(sg);
+            free(x);
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Step 2 -- proxy attention and masses (Sec. 3.2.2 Eqs. 7-8; Sec. 3.2.3     */
+/* Eq. 11 for the anchor; Appendix B for the GQA aggregation).               */
+/* ------------------------------------------------------------------------ */
+
+/* softmax over t of q . k_t / sqrt(d) for one bf16 query row; writes p[T]. */
+static void softmax_row(const uint16_t *q, const void *k, int kdtype, int64_t kbase, int T,
+                        int d, double *logit, double *p)
+{
+    double sqrt_d = sqrt((double)d);
+    double mx = -INFINITY;
+    for (int t = 0; t < T; ++t) {
+        double dot = 0.0;
+        for (int j = 0; j < d; ++j) {
+            double prod = oracle_bf16_to_f64(q[j]) * load_key_bf16(k, kdtype, kbase + (int64_t)t * d + j);
+            dot = dot + prod;
+        }
+        logit[t] = dot / sqrt_d;
+        if (logit[t] > mx)
+            mx = logit[t];
+    }
+    double sum = 0.0;
+    for (int t = 0; t < T; ++t)
+        sum = sum + exp(logit[t] - mx);
+    double lse = mx + log(sum);
+    for (int t = 0; t < T; ++t)
+        p[t] = exp(logit[t] - lse);
+}
+
+/*
+ * proxies  [B, Hq, P, d] bf16;  q_last [B, Hq, d] bf16
+ * k        [B, Hkv, T, d] contiguous, dtype 0 (fp32, rounded to bf16) / 1
+ * group_mass [B, Hkv, G, T] fp64 out (may be NULL)
+ * mass       [B, Hkv, T] fp64 out;  anchor [B, Hkv, T] fp64 out
+ */
+int oracle_score(int B, int Hq, int Hkv, int T, int d, int P, int G,
+                 const uint16_t *proxies, const uint16_t *q_last, const void *k, int kdtype,
+                 double *group_mass, double *mass, double *anchor)
+{
+    if (B < 1 || Hq < 1 || Hkv < 1 || (Hq % Hkv) != 0 || T < 1 || d < 1 || P < 1 || G < 1 ||
+        (P % G) != 0)
+        return -1;
+    int Gh = Hq / Hkv;
+    int g = P / G;
+    double *gm = group_mass;
+    double *gm_own = NULL;
+    if (!gm) {
+        gm_own = (double *)malloc(sizeof(double) * (size_t)B * Hkv * G * T);
+        gm = gm_own;
+    }
+
+    /* one task per (b, kv head, group): the group's rows are summed in a
+     * fixed order (head, then proxy), independent of the thread count */
+#pragma omp parallel for collapse(3) schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) {
+        for (int c = 0; c < Hkv; ++c) {
+            for (int gi = 0; gi < G; ++gi) {
+                double *logit = (double *)malloc(sizeof(double) * (size_t)T);
+                double *p = (double *)malloc(sizeof(double) * (size_t)T);
+                double *acc = gm + (((int64_t)b * Hkv + c) * G + gi) * T;
+                for (int t = 0; t < T; ++t)
+                    acc[t] = 0.0;
+                int64_t kbase = ((int64_t)b * Hkv + c) * (int64_t)T * d;
+                for (int hl = 0; hl < Gh; ++hl) {
+                    int h = c * Gh + hl;
+                    for (int i = gi * g; i < (gi + 1) * g; ++i) {
+                        const uint16_t *q = proxies + (((int64_t)b * Hq + h) * P + i) * d;
+                        softmax_row(q, k, kdtype, kbase, T, d, logit, p);
+                        for (int t = 0; t < T; ++t)
+                            acc[t] = acc[t] + p[t];
+                    }
+                }
+                free(logit);
+                free(p);
+            }
+        }
+    }
+
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int c = 0; c < Hkv; ++c) {
+            double *logit = (double *)malloc(sizeof(double) * (size_t)T);
+            double *p = (double *)malloc(sizeof(double) * (size_t)T);
+            int64_t kbase = ((int64_t)b * Hkv + c) * (int64_t)T * d;
+            double *ms = mass + ((int64_t)b * Hkv + c) * T;
+            double *an = anchor + ((int64_t)b * Hkv + c) * T;
+            for (int t = 0; t < T; ++t) {
+                double s = 0.0;
+                for (int gi = 0; gi < G; ++gi)
+                    s = s + gm[(((int64_t)b * Hkv + c) * G + gi) * T + t];
+                ms[t] = s;
+                an[t] = 0.0;
+            }
+            for (int hl = 0; hl < Gh; ++hl) {
+                int h = c * Gh + hl;
+                const uint16_t *q = q_last + ((int64_t)b * Hq + h) * d;
+                softmax_row(q, k, kdtype, kbase, T, d, logit, p);
+                for (int t = 0; t < T; ++t)
+                    an[t] = an[t] + p[t];
+            }
+            for (int t = 0; t < T; ++t)
+                an[t] = an[t] / (double)Gh;
+            free(logit);
+            free(p);
+        }
+    }
+    free(gm_own);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Step 3 -- tau-sets, votes, anchor score, budgeted top-k, temporal order   */
+/* (Sec. 3.2.2 Eqs. 9-10; Sec. 3.2.3 Eq. 11; Appendix B; Algorithm 1).       */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    double v;
+    int t;
+} keyed;
+
+/* order: value descending, then index ascending */
+static int cmp_desc(const void *a, const void *b)
+{
+    const keyed *x = (const keyed *)a, *y = (const keyed *)b;
+    if (x->v > y->v) return -1;
+    if (x->v < y->v) return 1;
+    return (x->t > y->t) - (x->t < y->t);
+}
+
+static int cmp_int(const void *a, const void *b)
+{
+    int x = *(const int *)a, y = *(const int *)b;
+    return (x > y) - (x < y);
+}
+
+/*
+ * mode 0 = VOTE (paper): score = vote + lambda * anchor
+ * mode 1 = MASS: score = total mass
+ * group_mass [B, Hkv, G, T] (needed for VOTE), mass/anchor [B, Hkv, T] fp64
+ * idx [B, Hkv, c_max] int32 out (ascending, -1 padded), counts [B, Hkv] out
+ * votes [B, Hkv, T] int32 out or NULL; score [B, Hkv, T] fp64 out or NULL
+ * cut_mass [B, Hkv, G] fp64 out or NULL: the mass of the last key that enters
+ *   each tau-set; cut_size [B, Hkv, G] int32 out or NULL: the tau-set sizes
+ */
+int oracle_select(int B, int Hkv, int T, int G, int mode, double tau, double lambda,
+                  int keep_last, int budget, int c_max, const double *group_mass,
+                  const double *mass, const double *anchor, int32_t *idx, int32_t *counts,
+                  int32_t *votes, double *score, double *cut_mass, int32_t *cut_size)
+{
+    if (B < 1 || Hkv < 1 || T < 1 || G < 1 || budget < 1 || c_max < budget ||
+        !(tau > 0.0 && tau <= 1.0) || !(lambda >= 0.0) || (mode != 0 && mode != 1))
+        return -1;
+
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) {
+        for (int c = 0; c < Hkv; ++c) {
+            int64_t hc = (int64_t)b * Hkv + c;
+            keyed *kv = (keyed *)malloc(sizeof(keyed) * (size_t)T);
+            int *vote = (int *)malloc(sizeof(int) * (size_t)T);
+            double *S = (double *)malloc(sizeof(double) * (size_t)T);
+            int *sel = (int *)malloc(sizeof(int) * (size_t)(T + 1));
+            for (int t = 0; t < T; ++t)
+                vote[t] = 0;
+            if (mode == 0) {
+                for (int gi = 0; gi < G; ++gi) {
+                    const double *a = group_mass + (hc * G + gi) * T;
+                    for (int t = 0; t < T; ++t) {
+                        kv[t].v = a[t];
+                        kv[t].t = t;
+                    }
+                    qsort(kv, (size_t)T, sizeof(keyed), cmp_desc);
+                    double total = 0.0;
+                    for (int r = 0; r < T; ++r)
+                        total = total + kv[r].v;
+                    double target = tau * total;
+                    double run = 0.0;
+                    int n = 0;
+                    while (n < T) {
+                        run = run + kv[n].v;
+                        n = n + 1;
+                        if (run >= target)
+                            break;
+                    }
+                    for (int r = 0; r < n; ++r)
+                        vote[kv[r].t] += 1;
+                    if (cut_mass) cut_mass[hc * G + gi] = kv[n - 1].v;
+                    if (cut_size) cut_size[hc * G + gi] = n;
+                }
+                for (int t = 0; t < T; ++t)
+                    S[t] = (double)vote[t] + lambda * anchor[hc * T + t];
+            } else {
+                for (int t = 0; t < T; ++t)
+                    S[t] = mass[hc * T + t];
+            }
+            if (votes)
+                for (int t = 0; t < T; ++t)
+                    votes[hc * T + t] = vote[t];
+            if (score)
+                for (int t = 0; t < T; ++t)
+                    score[hc * T + t] = S[t];
+
+            int nsel = 0;
+            if (T <= budget) {
+                for (int t = 0; t < T; ++t)
+                    sel[nsel++] = t;
+            } else {
+                int pool = keep_last ? T - 1 : T;
+                int want = keep_last ? budget - 1 : budget;
+                for (int t = 0; t < pool; ++t) {
+                    kv[t].v = S[t];
+                    kv[t].t = t;
+                }
+                qsort(kv, (size_t)pool, sizeof(keyed), cmp_desc);
+                for (int r = 0; r < want; ++r)
+                    sel[nsel++] = kv[r].t;
+                if (keep_last)
+                    sel[nsel++] = T - 1;
+                qsort(sel, (size_t)nsel, sizeof(int), cmp_int);
+            }
+            for (int j = 0; j < c_max; ++j)
+                idx[hc * c_max + j] = (j < nsel) ? sel[j] : -1;
+            counts[hc] = nsel;
+            free(kv);
+            free(vote);
+            free(S);
+            free(sel);
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Step 4 -- gather the retained rows into the compacted cache (Appendix B:  */
+/* restore temporal order, insert through the standard cache update).        */
+/* src [B, H, T, row_bytes], idx [B, H, c_max], counts [B, H];               */
+/* dst [B, H, c_max, row_bytes]; padding rows are zero-filled.               */
+/* ------------------------------------------------------------------------ */
+int oracle_gather(int B, int H, int T, int64_t row_bytes, int c_max, const void *src,
+                  const int32_t *idx, const int32_t *counts, void *dst)
+{
+    if (B < 1 || H < 1 || T < 1 || row_bytes < 1 || c_max < 1)
+        return -1;
+    for (int64_t bh = 0; bh < (int64_t)B * H; ++bh) {
+        for (int j = 0; j < c_max; ++j) {
+            unsigned char *o = (unsigned char *)dst + (bh * c_max + j) * row_bytes;
+            if (j < counts[bh]) {
+                int t = idx[bh * c_max + j];
+                if (t < 0 || t >= T)
+                    return -1;
+                memcpy(o, (const unsigned char *)src + (bh * T + t) * row_bytes, (size_t)row_bytes);
+            } else {
+                memset(o, 0, (size_t)row_bytes);
+            }
+        }
+    }
+    return 0;
+}
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
