@@ -1,0 +1,188 @@
+"""Throughput of MM-ShiftKV prefill-stage KV selection on one MI355X.
+
+A step is the whole hot path for every layer of one batch of synthetic
+inputs: proxies -> row log-sum-exp pass -> mass pass -> tau-sets / votes /
+top-k -> K/V gather, through the C ABI, inputs resident in HBM.  Default
+workload: 28 layers, batch 4, 28 query / 4 KV heads, d=128, T=16384 prompt
+keys (16128 visual + 256 text), W=64 window queries, budget 256 per KV
+head, the paper's method settings (P=512, G=32, gamma=10, tau=0.95,
+lambda=1, vote mode).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Prints one JSON line: keys scored+selected per second (B*L*T / step time),
+the roofline of the dominant kernel (algorithmic MFMA flops per launch /
+launch time, events on the launch stream) and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, cfg, layer_inputs, heads=1):
+    """The fp64 CPU oracle on `heads` (batch row, KV head) pairs of layer 0."""
+    import oracle
+    from paper_2607_22586_amd import workloads as wl
+    oracle.build()
+    Gh = w.Gh
+    t0 = time.perf_counter()
+    for i in range(heads):
+        b, c = i % w.B, (i // w.B) % w.Hkv
+        q1 = wl.to_numpy_bits(layer_inputs["q_win"][b:b + 1, c * Gh:(c + 1) * Gh].contiguous())
+        k1 = wl.to_numpy_bits(layer_inputs["k"][b:b + 1, c:c + 1].contiguous())
+        v1 = wl.to_numpy_bits(layer_inputs["v"][b:b + 1, c:c + 1].contiguous())
+        prox, ql, _ = oracle.build_proxies(q1, cfg.P, cfg.gamma, cfg.seed, 0, b0=b, h0=c * Gh)
+        gm, mass, an = oracle.score(prox, ql, k1, 1, cfg.G)
+        sel = oracle.select(gm, mass, an, w.budget, cfg.tau, cfg.lam, mode=cfg.mode)
+        oracle.gather(k1, sel.idx, sel.counts)
+        oracle.gather(v1, sel.idx, sel.counts)
+    dt = time.perf_counter() - t0
+    keys = heads / w.Hkv * w.T          # one KV head covers 1/Hkv of a sequence-layer's keys
+    return {"value": keys / dt, "unit": "prompt keys/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d (batch row, KV head) pair(s) of layer 0, T=%d, all steps; %.1f s"
+                      % (heads, w.T, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="qwen7b_16k_b4")
+    ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
+    ap.add_argument("--mode", choices=["vote", "mass"], default="vote")
+    ap.add_argument("--cpu-heads", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the selection path is independent per (layer, KV head) and "
+              "needs no collectives; --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_22586_amd as mm
+    from paper_2607_22586_amd import binding as bd
+    from paper_2607_22586_amd import workloads as wl
+
+    if not os.path.exists(bd.LIB_PATH):
+        from paper_2607_22586_amd import build
+        build.build()
+    bd.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.WORKLOADS[args.workload]
+    L = args.layers or w.L
+    B, Hq, Hkv, T, W, d = w.B, w.Hq, w.Hkv, w.T, w.W, w.d
+    mode = bd.MMSKV_VOTE if args.mode == "vote" else bd.MMSKV_MASS
+    cfgs = [bd.SelectionConfig(seed=w.wid, layer=l, mode=mode) for l in range(L)]
+    cfg = cfgs[0]
+
+    log("generating %d layers of %s on the device" % (L, w.name))
+    layers = [wl.make_layer(w, l, device=dev) for l in range(L)]
+    torch.cuda.synchronize()
+    log("inputs ready: %.2f GiB" % (sum(x["k"].numel() * 2 * x["k"].element_size() for x in layers) / 2**30))
+
+    # preallocated outputs and workspaces (reused by every layer)
+    prox = torch.empty((B, Hq, cfg.P, d), dtype=torch.bfloat16, device=dev)
+    qlast = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    sc = bd.ScoreOut(torch.empty((B, Hkv, cfg.G, T), dtype=torch.float32, device=dev) if mode == 0 else None,
+                     torch.empty((B, Hkv, T), dtype=torch.float32, device=dev),
+                     torch.empty((B, Hkv, T), dtype=torch.float32, device=dev))
+    ws_score = torch.empty(bd.score_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(bd.select_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev)
+    sel = bd.Selected(torch.empty((B, Hkv, w.budget), dtype=torch.int32, device=dev),
+                      torch.empty((B, Hkv), dtype=torch.int32, device=dev), None)
+    kv_out = [(torch.empty((B, Hkv, w.budget, d), dtype=layers[0]["k"].dtype, device=dev),
+               torch.empty((B, Hkv, w.budget, d), dtype=layers[0]["k"].dtype, device=dev)) for _ in range(L)]
+    stream = torch.cuda.current_stream(dev)
+
+    def step(events=None):
+        for l in range(L):
+            x = layers[l]
+            c = cfgs[l]
+            bd.build_proxies(x["q_win"], c, T, Hkv, out=(prox, qlast))
+            if events is not None:
+                events[l][0].record(stream)
+            bd.score_lse(prox, qlast, x["k"], c, ws_score, W)
+            if events is not None:
+                events[l][1].record(stream)
+            bd.score_mass(prox, qlast, x["k"], c, ws_score, W, out=sc)
+            if events is not None:
+                events[l][2].record(stream)
+            bd.select_topk(sc, c, w.budget, w.budget, None, Hq, W, out=sel, workspace=ws_sel)
+            bd.gather_kv(x["k"], x["v"], sel, out=kv_out[l])
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log("warmup step %d done" % (i + 1))
+
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(L)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for s in range(args.steps):
+        step(ev[s])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / args.steps
+    lse_ms = sum(ev[s][l][0].elapsed_time(ev[s][l][1]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
+    mass_ms = sum(ev[s][l][1].elapsed_time(ev[s][l][2]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
+    log("timed %d steps: %.3f ms/step, score_lse %.1f us, score_mass %.1f us per layer"
+        % (args.steps, ms_step, lse_ms * 1e3, mass_ms * 1e3))
+
+    # algorithmic MFMA work of one scoring launch: 2*Gh*P*d flops per prompt
+    # key per KV head (one proxy-by-key contraction), times B*Hkv*T keys
+    flops = 2.0 * w.Gh * cfg.P * d * B * Hkv * T
+    dom = "score_mass" if mass_ms >= lse_ms else "score_lse"
+    dom_ms = max(mass_ms, lse_ms)
+    achieved = flops / (dom_ms * 1e-3) / 1e12
+    keys_per_s = B * L * T / (ms_step * 1e-3)
+    out = {
+        "metric": "prompt keys scored+selected/sec",
+        "value": keys_per_s,
+        "unit": "keys/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "us_per_layer": ms_step * 1e3 / L,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "batch": B, "T": T, "Hq": Hq, "Hkv": Hkv, "d": d, "W": W,
+                   "budget": w.budget, "P": cfg.P, "G": cfg.G, "gamma": cfg.gamma, "tau": cfg.tau,
+                   "lambda": cfg.lam, "mode": args.mode},
+        "stages_us_per_layer": {"score_lse": lse_ms * 1e3, "score_mass": mass_ms * 1e3},
+        "roofline": {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on %d head(s)" % args.cpu_heads)
+        x0 = {k: (v.cpu() if torch.is_tensor(v) else v) for k, v in layers[0].items()}
+        out["cpu_baseline"] = cpu_baseline(w, cfg, x0, args.cpu_heads)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

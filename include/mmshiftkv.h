@@ -1,0 +1,194 @@
+/*
+ * mmshiftkv.h -- C ABI of the MI355X (gfx950) library for MM-ShiftKV
+ * prefill-stage KV scoring and selection (arxiv 2607.22586).
+ *
+ * Per layer, for every (batch row, KV head), the library
+ *   1. builds variance-expanded query proxies from the observation-window
+ *      queries                                (Sec. 3.2.1 Eqs. 4-5),
+ *   2. computes each proxy's softmax over all prompt keys and sums the
+ *      attention mass per proxy group across the query heads of the GQA
+ *      group, plus the last-query anchor       (Sec. 3.2.2 Eqs. 7-8,
+ *                                               Sec. 3.2.3 Eq. 11, Appendix B),
+ *   3. forms the tau-sets and votes, ranks keys by vote + lambda*anchor and
+ *      keeps the most recent key plus the top C-1 (Sec. 3.2.2 Eqs. 9-10,
+ *                                               Sec. 3.2.3, Algorithm 1),
+ *   4. gathers the retained K/V rows, in temporal order, into a compacted
+ *      cache                                   (Appendix B).
+ *
+ * Conventions (all entry points):
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The
+ *     library never allocates, frees or synchronises; scratch memory comes
+ *     from the caller, sized by the *_workspace() queries.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Calls only enqueue
+ *     work on it and return; results are valid once the stream reaches them.
+ *   - Arguments are validated on the host before anything is launched; an
+ *     invalid call returns a negative mmskv_status and enqueues nothing.
+ *     MMSKV_EHIP reports a launch error from the HIP runtime.
+ *   - bf16 tensors are passed as uint16_t bit patterns.
+ *   - Inputs containing NaN or Inf give unspecified (but memory-safe) results.
+ *   - Calls are thread-safe; the library holds no mutable global state.
+ */
+#ifndef MMSHIFTKV_H
+#define MMSHIFTKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MMSKV_OK = 0,
+    MMSKV_EINVAL = -1,       /* invalid argument: shape, pointer, parameter */
+    MMSKV_EUNSUPPORTED = -2, /* valid per the paper but not built: see each call */
+    MMSKV_EWORKSPACE = -3,   /* workspace pointer NULL or smaller than required */
+    MMSKV_EHIP = -4          /* the HIP runtime reported a launch error */
+} mmskv_status;
+
+typedef enum { MMSKV_F32 = 0, MMSKV_BF16 = 1 } mmskv_dtype;
+
+typedef enum {
+    MMSKV_VOTE = 0, /* the paper's rule: tau-set votes + lambda * anchor */
+    MMSKV_MASS = 1  /* total proxy mass (votes and anchor not used) */
+} mmskv_mode;
+
+/* Problem sizes of one layer.
+ *   B    batch rows (<= 65535)        Hq   query heads
+ *   Hkv  KV heads (Hq % Hkv == 0; the Gh = Hq/Hkv query heads h with
+ *        h / Gh == c share KV head c)
+ *   T    prompt keys per KV head (>= 1)
+ *   W    window queries per query head (>= 1)
+ *   d    head dimension: 64 or 128 (others -> MMSKV_EUNSUPPORTED) */
+typedef struct {
+    int32_t B, Hq, Hkv, T, W, d;
+} mmskv_shape;
+
+/* Element strides of a 4-D tensor [batch, head, token, d]; d is contiguous
+ * and every row must start on a 16-byte boundary. */
+typedef struct {
+    int64_t sb, sh, st;
+} mmskv_strides;
+
+/* Method parameters (paper defaults: P=512, G=32, gamma=10, tau=0.95,
+ * lambda=1; Sec. 4.1 and Appendix B).
+ *   P         proxies per query head (the paper's N); P % G == 0 and the
+ *             group size P/G must be a multiple of 16
+ *   G         proxy groups, 1..255 (groups are contiguous proxy blocks)
+ *   gamma     >= 0; multiplies the window std (x = mu + gamma*sigma*z)
+ *   tau       in (0, 1]: tau-set mass fraction
+ *   lambda    >= 0: anchor weight
+ *   std_ddof  0 (population std) or 1; W - std_ddof >= 1
+ *   layer     0..65535 and seed: fields of the Philox4x32-10 counter / key
+ *   mode      mmskv_mode
+ *   keep_last 1: token T-1 is always kept and the rest of the budget is
+ *             filled from [0, T-1); 0: plain top-C over [0, T) */
+typedef struct {
+    int32_t P, G;
+    double gamma, tau, lambda;
+    int32_t std_ddof, layer;
+    uint64_t seed;
+    int32_t mode, keep_last;
+} mmskv_params;
+
+/* Step 1 -- query proxies (Sec. 3.2.1 Eqs. 4-5; Appendix A.4 Eq. 15).
+ * Per (b, query head h) and dimension j: mu, sigma over the W window queries
+ * (fp64, summed in window order, divisor W - std_ddof).  Proxy i of head h:
+ *   x_j = mu_j + (gamma * sigma_j) * z_j,
+ * z from Philox4x32-10 (counter (j/4, i, h, (b<<16)|layer), key = seed) and
+ * Box-Muller on series-evaluated ln/sin/cos in fp64, each product and sum
+ * rounded separately; optional rotate-half rotary embedding (pairs j, j+d/2)
+ * from the caller's cos/sin tables; then fp64 -> fp32 -> bf16, both round to
+ * nearest even.  q_last[b,h] is window query W-1 (rotated by the *_l tables
+ * when given), rounded the same way; it is the anchor query of Eq. 11.
+ *   q_win     [B, Hq, W, d] q_dtype, strides q_strides (elements)
+ *   rope_*_f  [d/2] fp32 cos/sin at the proxies' future position, or both NULL
+ *   rope_*_l  [d/2] fp32 cos/sin at the last query's position, or both NULL
+ *   proxies   [B, Hq, P, d] bf16 out, contiguous
+ *   q_last    [B, Hq, d] bf16 out, contiguous
+ *   stats     [B, Hq, 2, d] fp64 out (mu then sigma) or NULL */
+int mmshiftkv_build_proxies(const mmskv_shape *shape, const mmskv_params *params,
+                            const void *q_win, int32_t q_dtype, const mmskv_strides *q_strides,
+                            const float *rope_cos_f, const float *rope_sin_f,
+                            const float *rope_cos_l, const float *rope_sin_l,
+                            uint16_t *proxies, uint16_t *q_last, double *stats, void *stream);
+
+/* Step 2 -- proxy attention and masses (Sec. 3.2.2 Eqs. 7-8; Sec. 3.2.3
+ * Eq. 11; Appendix B GQA aggregation).  For KV head c of batch row b, every
+ * proxy row of the Gh query heads that share c gets its softmax over all T
+ * keys (scale 1/sqrt(d); bf16 operands, fp32 accumulation; fp32 keys are
+ * rounded to bf16 for scoring).  Outputs, fp32, contiguous:
+ *   group_mass [B, Hkv, G, T]  sum over the group's proxies and heads
+ *                              (may be NULL in MMSKV_MASS mode)
+ *   mass       [B, Hkv, T]     sum over all groups
+ *   anchor     [B, Hkv, T]     mean over the Gh heads of softmax(q_last)
+ * The logit matrix never reaches memory: the call runs a row log-sum-exp
+ * pass and a mass pass over the keys.  Workspace: mmshiftkv_score_workspace
+ * bytes (256-byte aligned pointer). */
+size_t mmshiftkv_score_workspace(const mmskv_shape *shape, const mmskv_params *params);
+int mmshiftkv_score(const mmskv_shape *shape, const mmskv_params *params,
+                    const uint16_t *proxies, const uint16_t *q_last,
+                    const void *k, int32_t k_dtype, const mmskv_strides *k_strides,
+                    float *group_mass, float *mass, float *anchor,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
+/* The two passes of mmshiftkv_score as separate calls (same arguments and
+ * workspace), for callers that schedule or time them separately:
+ * mmshiftkv_score_lse writes each row's log-sum-exp into the workspace;
+ * mmshiftkv_score_mass then reads it and writes the outputs. */
+int mmshiftkv_score_lse(const mmskv_shape *shape, const mmskv_params *params,
+                        const uint16_t *proxies, const uint16_t *q_last,
+                        const void *k, int32_t k_dtype, const mmskv_strides *k_strides,
+                        void *workspace, size_t workspace_bytes, void *stream);
+int mmshiftkv_score_mass(const mmskv_shape *shape, const mmskv_params *params,
+                         const uint16_t *proxies, const uint16_t *q_last,
+                         const void *k, int32_t k_dtype, const mmskv_strides *k_strides,
+                         float *group_mass, float *mass, float *anchor,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Step 3 -- tau-sets, votes and budgeted selection (Sec. 3.2.2 Eqs. 9-10;
+ * Sec. 3.2.3 Eq. 11; Algorithm 1).
+ * VOTE: for each group, S_g = keys taken in (mass desc, index asc) order up to
+ * the first prefix whose mass reaches tau * the group total (masses summed in
+ * 2^-k fixed point, so the cut is deterministic); vote(t) = #groups with t in
+ * S_g; score = vote + lambda * anchor in fp64.  MASS: score = mass.
+ * Selection per (b, c) with budget C (budgets[b*Hkv+c] when `budgets` is a
+ * device array, else `budget`): if T <= C all keys; else token T-1 plus the
+ * C-1 best of [0, T-1) by (score desc, index asc) (keep_last = 1), or the C
+ * best of [0, T) (keep_last = 0).
+ *   idx    [B, Hkv, c_max] int32 out: ascending token indices, -1 padded
+ *   counts [B, Hkv] int32 out: min(C, T)
+ *   votes  [B, Hkv, T] uint8 out or NULL (VOTE mode only)
+ * Requires c_max >= min(C, T) for every head (checked on the host for the
+ * scalar budget; per-head budgets above c_max are clamped to c_max).
+ * Workspace: mmshiftkv_select_workspace bytes. */
+size_t mmshiftkv_select_workspace(const mmskv_shape *shape, const mmskv_params *params);
+int mmshiftkv_select_topk(const mmskv_shape *shape, const mmskv_params *params,
+                          const float *group_mass, const float *mass, const float *anchor,
+                          const int32_t *budgets, int32_t budget, int32_t c_max,
+                          int32_t *idx, int32_t *counts, uint8_t *votes,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* Step 4 -- compacted cache (Appendix B: retained tokens in temporal order,
+ * inserted through the standard cache update).  For j < counts[b,c]:
+ *   k_out[b,c,j,:] = k[b,c,idx[b,c,j],:], v_out likewise (byte copies);
+ * rows j >= counts[b,c] are zero-filled.
+ *   k, v          [B, Hkv, T, d] dtype, strides k_strides / v_strides
+ *   k_out, v_out  [B, Hkv, c_max, d] dtype, contiguous
+ * idx entries outside [0, T) are not read (their row is zero-filled). */
+int mmshiftkv_gather_kv(const mmskv_shape *shape, const void *k, const void *v, int32_t dtype,
+                        const mmskv_strides *k_strides, const mmskv_strides *v_strides,
+                        const int32_t *idx, const int32_t *counts, int32_t c_max,
+                        void *k_out, void *v_out, void *stream);
+
+/* Human-readable text for an mmskv_status value (static storage). */
+const char *mmshiftkv_status_string(int status);
+
+/* Library version: major*10000 + minor*100 + patch. */
+int mmshiftkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MMSHIFTKV_H */

@@ -64,6 +64,9 @@ def _load():
     lib.oracle_build_proxies.argtypes = [i32, i32, i32, i32, i32, f64, i32, u64, i32, P, i32,
                                          P, P, P, P, P, P, P]
     lib.oracle_build_proxies.restype = i32
+    lib.oracle_build_proxies_at.argtypes = [i32, i32, i32, i32, i32, f64, i32, u64, i32, i32, i32, P,
+                                            i32, P, P, P, P, P, P, P]
+    lib.oracle_build_proxies_at.restype = i32
     lib.oracle_score.argtypes = [i32, i32, i32, i32, i32, i32, i32, P, P, P, i32, P, P, P]
     lib.oracle_score.restype = i32
     lib.oracle_select.argtypes = [i32, i32, i32, i32, i32, f64, f64, i32, i32, i32, P, P, P,
@@ -140,12 +143,13 @@ def _dtype_code(a: np.ndarray) -> int:
 
 
 def build_proxies(q_win: np.ndarray, P: int, gamma: float, seed: int, layer: int = 0, ddof: int = 0,
-                  rope_f=None, rope_l=None):
+                  rope_f=None, rope_l=None, b0: int = 0, h0: int = 0):
     """Sec. 3.2.1: window statistics (Eq. 4), variance-expanded samples (Eq. 5).
 
     q_win: [B, Hq, W, d] float32 or bf16 bits.  rope_f / rope_l: optional
     (cos, sin) float32 tables of length d/2 for the proxies' future position
-    and for the last query's own position.
+    and for the last query's own position.  b0 / h0: global batch row and
+    query head of q_win[0, 0] when q_win is a slice of a larger problem.
     Returns (proxies [B,Hq,P,d] u16, q_last [B,Hq,d] u16, stats [B,Hq,2,d] f64).
     """
     q = np.ascontiguousarray(q_win)
@@ -160,9 +164,10 @@ def build_proxies(q_win: np.ndarray, P: int, gamma: float, seed: int, layer: int
         else:
             tabs += [np.ascontiguousarray(rp[0], dtype=np.float32),
                      np.ascontiguousarray(rp[1], dtype=np.float32)]
-    rc = _load().oracle_build_proxies(B, Hq, W, d, P, float(gamma), int(ddof), int(seed), int(layer),
-                                      _ptr(q), _dtype_code(q), *[_ptr(t) for t in tabs],
-                                      _ptr(prox), _ptr(qlast), _ptr(stats))
+    rc = _load().oracle_build_proxies_at(B, Hq, W, d, P, float(gamma), int(ddof), int(seed), int(layer),
+                                         int(b0), int(h0), _ptr(q), _dtype_code(q),
+                                         *[_ptr(t) for t in tabs],
+                                         _ptr(prox), _ptr(qlast), _ptr(stats))
     if rc != 0:
         raise ValueError("oracle_build_proxies rejected its arguments")
     return prox, qlast, stats

@@ -228,14 +228,17 @@ static double load_key_bf16(const void *base, int dtype, int64_t off)
  * stats      [B, Hq, 2, d] fp64 out (mu, sigma), may be NULL
  * returns 0, or -1 on invalid arguments
  */
-int oracle_build_proxies(int B, int Hq, int W, int d, int P, double gamma, int ddof,
-                         uint64_t seed, int layer, const void *q_win, int dtype,
-                         const float *rope_cos_f, const float *rope_sin_f,
-                         const float *rope_cos_l, const float *rope_sin_l,
-                         uint16_t *proxies, uint16_t *q_last, double *stats)
+/* b0 / h0: global batch row and query head of the first row/head of q_win,
+ * so that a slice of a larger problem draws the same noise (the generator
+ * counter uses the global indices). */
+int oracle_build_proxies_at(int B, int Hq, int W, int d, int P, double gamma, int ddof,
+                            uint64_t seed, int layer, int b0, int h0, const void *q_win, int dtype,
+                            const float *rope_cos_f, const float *rope_sin_f,
+                            const float *rope_cos_l, const float *rope_sin_l,
+                            uint16_t *proxies, uint16_t *q_last, double *stats)
 {
     if (B < 1 || Hq < 1 || W < 1 || d < 4 || (d % 4) != 0 || P < 1 || W - ddof < 1 ||
-        ddof < 0 || layer < 0 || layer > 0xFFFF || B > 0xFFFF)
+        ddof < 0 || layer < 0 || layer > 0xFFFF || b0 < 0 || h0 < 0 || B + b0 > 0xFFFF)
         return -1;
     int use_rope = (rope_cos_f != NULL && rope_sin_f != NULL);
     int use_rope_last = (rope_cos_l != NULL && rope_sin_l != NULL);
@@ -275,7 +278,7 @@ int oracle_build_proxies(int B, int Hq, int W, int d, int P, double gamma, int d
             for (int i = 0; i < P; ++i) {
                 for (int jq = 0; jq < d / 4; ++jq) {
                     double z[4];
-                    oracle_normal4(seed, b, layer, h, i, jq, z);
+                    oracle_normal4(seed, b0 + b, layer, h0 + h, i, jq, z);
                     for (int e = 0; e < 4; ++e) {
                         int j = 4 * jq + e;
                         double gs = gamma * sg[j];
@@ -323,6 +326,17 @@ int oracle_build_proxies(int B, int Hq, int W, int d, int P, double gamma, int d
         }
     }
     return 0;
+}
+
+int oracle_build_proxies(int B, int Hq, int W, int d, int P, double gamma, int ddof,
+                         uint64_t seed, int layer, const void *q_win, int dtype,
+                         const float *rope_cos_f, const float *rope_sin_f,
+                         const float *rope_cos_l, const float *rope_sin_l,
+                         uint16_t *proxies, uint16_t *q_last, double *stats)
+{
+    return oracle_build_proxies_at(B, Hq, W, d, P, gamma, ddof, seed, layer, 0, 0, q_win, dtype,
+                                   rope_cos_f, rope_sin_f, rope_cos_l, rope_sin_l, proxies, q_last,
+                                   stats);
 }
 
 /* ------------------------------------------------------------------------ */

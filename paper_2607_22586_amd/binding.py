@@ -1,0 +1,336 @@
+"""ctypes binding of libmmshiftkv (C ABI in include/mmshiftkv.h).
+
+Argument marshalling only: every step runs in the library's HIP kernels on
+the GPU.  Tensors are torch tensors on a ROCm device; the library enqueues on
+the current torch stream of that device.  If the shared library is missing
+or cannot be loaded, every call raises -- there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmmshiftkv.so")
+
+MMSKV_OK, MMSKV_EINVAL, MMSKV_EUNSUPPORTED, MMSKV_EWORKSPACE, MMSKV_EHIP = 0, -1, -2, -3, -4
+MMSKV_F32, MMSKV_BF16 = 0, 1
+MMSKV_VOTE, MMSKV_MASS = 0, 1
+
+EXPORTED = ("mmshiftkv_build_proxies", "mmshiftkv_score_workspace", "mmshiftkv_score",
+            "mmshiftkv_score_lse", "mmshiftkv_score_mass", "mmshiftkv_select_workspace",
+            "mmshiftkv_select_topk", "mmshiftkv_gather_kv", "mmshiftkv_status_string",
+            "mmshiftkv_version")
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32),
+                ("T", ctypes.c_int32), ("W", ctypes.c_int32), ("d", ctypes.c_int32)]
+
+
+class Strides(ctypes.Structure):
+    _fields_ = [("sb", ctypes.c_int64), ("sh", ctypes.c_int64), ("st", ctypes.c_int64)]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("P", ctypes.c_int32), ("G", ctypes.c_int32), ("gamma", ctypes.c_double),
+                ("tau", ctypes.c_double), ("lambda_", ctypes.c_double),
+                ("std_ddof", ctypes.c_int32), ("layer", ctypes.c_int32),
+                ("seed", ctypes.c_uint64), ("mode", ctypes.c_int32), ("keep_last", ctypes.c_int32)]
+
+
+class MMShiftKVError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__("%s failed: %s (%d)" % (fn, status_string(status), status))
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str | None = None):
+    """Load libmmshiftkv.so (raises if it is missing: there is no fallback)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError("libmmshiftkv.so is not built (%s); run __graft_entry__.build() or "
+                           "python -m paper_2607_22586_amd.build" % p)
+    lib = ctypes.CDLL(p)
+    V, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    PS, PP, PT = ctypes.POINTER(Shape), ctypes.POINTER(Params), ctypes.POINTER(Strides)
+    lib.mmshiftkv_build_proxies.argtypes = [PS, PP, V, I32, PT, V, V, V, V, V, V, V, V]
+    lib.mmshiftkv_score_workspace.argtypes = [PS, PP]
+    lib.mmshiftkv_score_workspace.restype = SZ
+    lib.mmshiftkv_score.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V, SZ, V]
+    lib.mmshiftkv_score_lse.argtypes = [PS, PP, V, V, V, I32, PT, V, SZ, V]
+    lib.mmshiftkv_score_mass.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V, SZ, V]
+    lib.mmshiftkv_select_workspace.argtypes = [PS, PP]
+    lib.mmshiftkv_select_workspace.restype = SZ
+    lib.mmshiftkv_select_topk.argtypes = [PS, PP, V, V, V, V, I32, I32, V, V, V, V, SZ, V]
+    lib.mmshiftkv_gather_kv.argtypes = [PS, V, V, I32, PT, PT, V, V, I32, V, V, V]
+    lib.mmshiftkv_status_string.argtypes = [ctypes.c_int]
+    lib.mmshiftkv_status_string.restype = ctypes.c_char_p
+    lib.mmshiftkv_version.restype = ctypes.c_int
+    for name in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_score_lse",
+                 "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_gather_kv"):
+        getattr(lib, name).restype = ctypes.c_int
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().mmshiftkv_status_string(int(status)).decode()
+
+
+def _check(fn: str, rc: int):
+    if rc != MMSKV_OK:
+        raise MMShiftKVError(fn, rc)
+
+
+@dataclass
+class SelectionConfig:
+    """Method parameters; defaults are the paper's (Sec. 4.1, Appendix B)."""
+    P: int = 512
+    G: int = 32
+    gamma: float = 10.0
+    tau: float = 0.95
+    lam: float = 1.0
+    std_ddof: int = 0
+    layer: int = 0
+    seed: int = 0
+    mode: int = MMSKV_VOTE
+    keep_last: bool = True
+
+    def c_params(self) -> Params:
+        return Params(int(self.P), int(self.G), float(self.gamma), float(self.tau), float(self.lam),
+                      int(self.std_ddof), int(self.layer), int(self.seed) & 0xFFFFFFFFFFFFFFFF,
+                      int(self.mode), int(bool(self.keep_last)))
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return MMSKV_F32
+    if t.dtype == torch.bfloat16:
+        return MMSKV_BF16
+    raise TypeError("expected float32 or bfloat16, got %s" % t.dtype)
+
+
+def _dev(t: torch.Tensor) -> torch.device:
+    if not t.is_cuda:
+        raise ValueError("libmmshiftkv takes device tensors (got a %s tensor)" % t.device)
+    return t.device
+
+
+def _strides4(t: torch.Tensor) -> Strides:
+    if t.dim() != 4 or t.stride(3) != 1:
+        raise ValueError("expected a [batch, head, token, d] tensor with contiguous d")
+    return Strides(t.stride(0), t.stride(1), t.stride(2))
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _shape(B, Hq, Hkv, T, W, d) -> Shape:
+    return Shape(int(B), int(Hq), int(Hkv), int(T), int(W), int(d))
+
+
+# ----------------------------------------------------------------------------
+# the four calls (plus the split score passes and workspace queries)
+# ----------------------------------------------------------------------------
+def build_proxies(q_win: torch.Tensor, cfg: SelectionConfig, T: int, Hkv: int, rope_f=None,
+                  rope_l=None, with_stats: bool = False, out=None):
+    """mmshiftkv_build_proxies: returns (proxies [B,Hq,P,d] bf16, q_last [B,Hq,d] bf16[, stats]).
+    `out` may hold preallocated (proxies, q_last) tensors."""
+    dev = _dev(q_win)
+    B, Hq, W, d = q_win.shape
+    shape = _shape(B, Hq, Hkv, T, W, d)
+    prm = cfg.c_params()
+    if out is None:
+        proxies = torch.empty((B, Hq, cfg.P, d), dtype=torch.bfloat16, device=dev)
+        q_last = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    else:
+        proxies, q_last = out
+        if (proxies.dtype != torch.bfloat16 or q_last.dtype != torch.bfloat16 or not proxies.is_contiguous()
+                or not q_last.is_contiguous() or tuple(proxies.shape) != (B, Hq, cfg.P, d)
+                or tuple(q_last.shape) != (B, Hq, d)):
+            raise ValueError("preallocated proxies/q_last do not match")
+    stats = torch.empty((B, Hq, 2, d), dtype=torch.float64, device=dev) if with_stats else None
+    tabs = []
+    for rp in (rope_f, rope_l):
+        if rp is None:
+            tabs += [None, None]
+        else:
+            tabs += [rp[0].to(device=dev, dtype=torch.float32).contiguous(),
+                     rp[1].to(device=dev, dtype=torch.float32).contiguous()]
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_build_proxies(
+            ctypes.byref(shape), ctypes.byref(prm), _p(q_win), _dtype_code(q_win),
+            ctypes.byref(_strides4(q_win)), *[_p(t) for t in tabs], _p(proxies), _p(q_last),
+            _p(stats), _stream(dev))
+    _check("mmshiftkv_build_proxies", rc)
+    return (proxies, q_last, stats) if with_stats else (proxies, q_last)
+
+
+def score_workspace(B, Hq, Hkv, T, W, d, cfg: SelectionConfig) -> int:
+    return int(load_library().mmshiftkv_score_workspace(ctypes.byref(_shape(B, Hq, Hkv, T, W, d)),
+                                                         ctypes.byref(cfg.c_params())))
+
+
+def select_workspace(B, Hq, Hkv, T, W, d, cfg: SelectionConfig) -> int:
+    return int(load_library().mmshiftkv_select_workspace(ctypes.byref(_shape(B, Hq, Hkv, T, W, d)),
+                                                          ctypes.byref(cfg.c_params())))
+
+
+def _ws(nbytes: int, dev) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=dev)
+
+
+@dataclass
+class ScoreOut:
+    group_mass: torch.Tensor | None    # [B, Hkv, G, T] fp32
+    mass: torch.Tensor                 # [B, Hkv, T] fp32
+    anchor: torch.Tensor               # [B, Hkv, T] fp32
+
+
+def _score_call(which: str, proxies, q_last, k, cfg, W, out: ScoreOut | None, workspace):
+    dev = _dev(k)
+    B, Hkv, T, d = k.shape
+    Hq = proxies.shape[1]
+    if proxies.dtype != torch.bfloat16 or q_last.dtype != torch.bfloat16:
+        raise TypeError("proxies and q_last are bf16")
+    if not (proxies.is_contiguous() and q_last.is_contiguous()):
+        raise ValueError("proxies and q_last must be contiguous")
+    if tuple(proxies.shape) != (B, Hq, cfg.P, d) or tuple(q_last.shape) != (B, Hq, d):
+        raise ValueError("proxies/q_last shapes do not match k")
+    shape = _shape(B, Hq, Hkv, T, W, d)
+    prm = cfg.c_params()
+    lib = load_library()
+    need = int(lib.mmshiftkv_score_workspace(ctypes.byref(shape), ctypes.byref(prm)))
+    ws = workspace if workspace is not None else _ws(need, dev)
+    strides = _strides4(k)
+    with torch.cuda.device(dev):
+        if which == "lse":
+            rc = lib.mmshiftkv_score_lse(ctypes.byref(shape), ctypes.byref(prm), _p(proxies), _p(q_last),
+                                         _p(k), _dtype_code(k), ctypes.byref(strides), _p(ws),
+                                         ws.numel() * ws.element_size(), _stream(dev))
+            _check("mmshiftkv_score_lse", rc)
+            return ws
+        if out is None:
+            gm = (torch.empty((B, Hkv, cfg.G, T), dtype=torch.float32, device=dev)
+                  if cfg.mode == MMSKV_VOTE else None)
+            out = ScoreOut(gm, torch.empty((B, Hkv, T), dtype=torch.float32, device=dev),
+                           torch.empty((B, Hkv, T), dtype=torch.float32, device=dev))
+        fn = lib.mmshiftkv_score if which == "full" else lib.mmshiftkv_score_mass
+        rc = fn(ctypes.byref(shape), ctypes.byref(prm), _p(proxies), _p(q_last), _p(k), _dtype_code(k),
+                ctypes.byref(strides), _p(out.group_mass), _p(out.mass), _p(out.anchor), _p(ws),
+                ws.numel() * ws.element_size(), _stream(dev))
+    _check("mmshiftkv_score" if which == "full" else "mmshiftkv_score_mass", rc)
+    return out
+
+
+def score(proxies, q_last, k, cfg: SelectionConfig, W: int = 1, out: ScoreOut | None = None,
+          workspace: torch.Tensor | None = None) -> ScoreOut:
+    """mmshiftkv_score: group masses, total mass and anchor for every (b, KV head)."""
+    return _score_call("full", proxies, q_last, k, cfg, W, out, workspace)
+
+
+def score_lse(proxies, q_last, k, cfg: SelectionConfig, workspace: torch.Tensor, W: int = 1):
+    """mmshiftkv_score_lse: the row log-sum-exp pass (result kept in `workspace`)."""
+    return _score_call("lse", proxies, q_last, k, cfg, W, None, workspace)
+
+
+def score_mass(proxies, q_last, k, cfg: SelectionConfig, workspace: torch.Tensor, W: int = 1,
+               out: ScoreOut | None = None) -> ScoreOut:
+    """mmshiftkv_score_mass: the mass pass, after score_lse on the same workspace."""
+    return _score_call("mass", proxies, q_last, k, cfg, W, out, workspace)
+
+
+@dataclass
+class Selected:
+    idx: torch.Tensor        # [B, Hkv, c_max] int32 ascending, -1 padded
+    counts: torch.Tensor     # [B, Hkv] int32
+    votes: torch.Tensor | None
+
+
+def select_topk(s: ScoreOut, cfg: SelectionConfig, budget: int, c_max: int | None = None,
+                budgets: torch.Tensor | None = None, Hq: int | None = None, W: int = 1,
+                want_votes: bool = False, out: Selected | None = None,
+                workspace: torch.Tensor | None = None) -> Selected:
+    """mmshiftkv_select_topk: tau-sets, votes, score and budgeted top-k."""
+    dev = _dev(s.mass)
+    B, Hkv, T = s.mass.shape
+    Hq = Hkv if Hq is None else Hq
+    c_max = int(budget if c_max is None else c_max)
+    d = 64
+    shape = _shape(B, Hq, Hkv, T, W, d)
+    prm = cfg.c_params()
+    lib = load_library()
+    need = int(lib.mmshiftkv_select_workspace(ctypes.byref(shape), ctypes.byref(prm)))
+    ws = workspace if workspace is not None else _ws(need, dev)
+    if out is None:
+        out = Selected(torch.empty((B, Hkv, c_max), dtype=torch.int32, device=dev),
+                       torch.empty((B, Hkv), dtype=torch.int32, device=dev),
+                       torch.empty((B, Hkv, T), dtype=torch.uint8, device=dev) if want_votes else None)
+    if budgets is not None:
+        budgets = budgets.to(device=dev, dtype=torch.int32).contiguous()
+    with torch.cuda.device(dev):
+        rc = lib.mmshiftkv_select_topk(ctypes.byref(shape), ctypes.byref(prm), _p(s.group_mass), _p(s.mass),
+                                       _p(s.anchor), _p(budgets), int(budget), c_max, _p(out.idx),
+                                       _p(out.counts), _p(out.votes), _p(ws),
+                                       ws.numel() * ws.element_size(), _stream(dev))
+    _check("mmshiftkv_select_topk", rc)
+    return out
+
+
+def gather_kv(k: torch.Tensor, v: torch.Tensor, sel: Selected, out=None):
+    """mmshiftkv_gather_kv: compacted K'/V' [B, Hkv, c_max, d] in temporal order."""
+    dev = _dev(k)
+    B, Hkv, T, d = k.shape
+    if v.shape != k.shape or v.dtype != k.dtype:
+        raise ValueError("k and v must have the same shape and dtype")
+    c_max = sel.idx.shape[2]
+    shape = _shape(B, Hkv, Hkv, T, 1, d)
+    if out is None:
+        out = (torch.empty((B, Hkv, c_max, d), dtype=k.dtype, device=dev),
+               torch.empty((B, Hkv, c_max, d), dtype=k.dtype, device=dev))
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_gather_kv(
+            ctypes.byref(shape), _p(k), _p(v), _dtype_code(k), ctypes.byref(_strides4(k)),
+            ctypes.byref(_strides4(v)), _p(sel.idx), _p(sel.counts), c_max, _p(out[0]), _p(out[1]),
+            _stream(dev))
+    _check("mmshiftkv_gather_kv", rc)
+    return out
+
+
+@dataclass
+class LayerOut:
+    proxies: torch.Tensor
+    q_last: torch.Tensor
+    scores: ScoreOut
+    sel: Selected
+    k_out: torch.Tensor
+    v_out: torch.Tensor
+
+
+def select_layer(q_win, k, v, budget: int, cfg: SelectionConfig | None = None, c_max=None,
+                 budgets=None, rope_f=None, rope_l=None, want_votes=False) -> LayerOut:
+    """All four calls for one layer (Algorithm 1), on the current stream."""
+    cfg = cfg or SelectionConfig()
+    B, Hkv, T, d = k.shape
+    Hq, W = q_win.shape[1], q_win.shape[2]
+    prox, ql = build_proxies(q_win, cfg, T, Hkv, rope_f, rope_l)
+    sc = score(prox, ql, k, cfg, W)
+    sel = select_topk(sc, cfg, budget, c_max, budgets, Hq, W, want_votes)
+    ko, vo = gather_kv(k, v, sel)
+    return LayerOut(prox, ql, sc, sel, ko, vo)

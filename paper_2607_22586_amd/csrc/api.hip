@@ -1,0 +1,344 @@
+// C ABI of libmmshiftkv: argument validation, workspace sizing and kernel
+// launches.  Every check runs on the host before anything is enqueued.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/mmshiftkv.h"
+#include "kernels.hpp"
+
+using namespace mmskv;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+int elem_bytes(int32_t dtype) { return dtype == MMSKV_F32 ? 4 : (dtype == MMSKV_BF16 ? 2 : 0); }
+
+int check_shape(const mmskv_shape* s) {
+    if (s == nullptr) return MMSKV_EINVAL;
+    if (s->B < 1 || s->B > 65535 || s->Hq < 1 || s->Hkv < 1 || s->T < 1 || s->W < 1 || s->d < 1)
+        return MMSKV_EINVAL;
+    if (s->Hq % s->Hkv != 0) return MMSKV_EINVAL;
+    if (s->Hkv > 65535) return MMSKV_EINVAL;
+    if (s->d != 64 && s->d != 128) return MMSKV_EUNSUPPORTED;
+    return MMSKV_OK;
+}
+
+int check_params(const mmskv_shape* s, const mmskv_params* p) {
+    if (p == nullptr) return MMSKV_EINVAL;
+    if (p->P < 1 || p->G < 1 || p->P % p->G != 0) return MMSKV_EINVAL;
+    if (p->G > 255) return MMSKV_EUNSUPPORTED;
+    if ((p->P / p->G) % 16 != 0) return MMSKV_EUNSUPPORTED;
+    if (!(p->gamma >= 0.0) || !isfinite(p->gamma)) return MMSKV_EINVAL;
+    if (!(p->tau > 0.0 && p->tau <= 1.0)) return MMSKV_EINVAL;
+    if (!(p->lambda >= 0.0) || !isfinite(p->lambda)) return MMSKV_EINVAL;
+    if (p->std_ddof != 0 && p->std_ddof != 1) return MMSKV_EINVAL;
+    if (s->W - p->std_ddof < 1) return MMSKV_EINVAL;
+    if (p->layer < 0 || p->layer > 65535) return MMSKV_EINVAL;
+    if (p->mode != MMSKV_VOTE && p->mode != MMSKV_MASS) return MMSKV_EINVAL;
+    if (p->keep_last != 0 && p->keep_last != 1) return MMSKV_EINVAL;
+    return MMSKV_OK;
+}
+
+int check_rows(const void* base, const mmskv_strides* st, int eb, bool vec16) {
+    if (st == nullptr) return MMSKV_EINVAL;
+    if (st->sb < 0 || st->sh < 0 || st->st < 0) return MMSKV_EINVAL;
+    if (vec16) {
+        if (!aligned(base, 16)) return MMSKV_EINVAL;
+        if ((st->sb * eb) % 16 || (st->sh * eb) % 16 || (st->st * eb) % 16) return MMSKV_EINVAL;
+    } else if (!aligned(base, static_cast<size_t>(eb))) {
+        return MMSKV_EINVAL;
+    }
+    return MMSKV_OK;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? MMSKV_OK : MMSKV_EHIP; }
+
+struct ScoreLayout {
+    int n_kb, rows, rows_pad;
+    size_t part_bytes, lse_off, total;
+};
+
+ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
+    ScoreLayout l;
+    const int Gh = s->Hq / s->Hkv;
+    l.n_kb = (s->T + kScoreBlockKeys - 1) / kScoreBlockKeys;
+    l.rows = Gh * p->P;
+    l.rows_pad = l.rows + 16 * ((Gh + 15) / 16);
+    const size_t heads = static_cast<size_t>(s->B) * s->Hkv;
+    l.part_bytes = heads * l.n_kb * l.rows_pad * sizeof(float2);
+    l.lse_off = align_up(l.part_bytes);
+    l.total = l.lse_off + align_up(heads * l.rows_pad * sizeof(float));
+    return l;
+}
+
+struct SelectLayout {
+    size_t theta_off, tcut_off, keys_off, total;
+};
+
+SelectLayout select_layout(const mmskv_shape* s, const mmskv_params* p) {
+    SelectLayout l;
+    const size_t heads = static_cast<size_t>(s->B) * s->Hkv;
+    l.theta_off = 0;
+    l.tcut_off = align_up(heads * p->G * sizeof(uint32_t));
+    l.keys_off = l.tcut_off + align_up(heads * p->G * sizeof(int32_t));
+    l.total = l.keys_off + align_up(heads * s->T * sizeof(uint64_t));
+    return l;
+}
+
+// Shared validation and argument packing of the three score entry points.
+int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                  const uint16_t* q_last, const void* k, int32_t k_dtype,
+                  const mmskv_strides* k_strides, void* ws, size_t ws_bytes, ScoreArgs* a) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    rc = check_params(shape, params);
+    if (rc) return rc;
+    const int eb = elem_bytes(k_dtype);
+    if (eb == 0) return MMSKV_EINVAL;
+    if (proxies == nullptr || q_last == nullptr || k == nullptr) return MMSKV_EINVAL;
+    if (!aligned(proxies, 16) || !aligned(q_last, 16)) return MMSKV_EINVAL;
+    rc = check_rows(k, k_strides, eb, true);
+    if (rc) return rc;
+    const ScoreLayout l = score_layout(shape, params);
+    if (ws == nullptr || !aligned(ws, kAlign) || ws_bytes < l.total) return MMSKV_EWORKSPACE;
+    a->proxies = proxies;
+    a->q_last = q_last;
+    a->k = k;
+    a->k_dtype = k_dtype;
+    a->ksb = k_strides->sb;
+    a->ksh = k_strides->sh;
+    a->kst = k_strides->st;
+    a->B = shape->B;
+    a->Hq = shape->Hq;
+    a->Hkv = shape->Hkv;
+    a->T = shape->T;
+    a->d = shape->d;
+    a->P = params->P;
+    a->G = params->G;
+    a->Gh = shape->Hq / shape->Hkv;
+    a->n_kb = l.n_kb;
+    a->rows = l.rows;
+    a->rows_pad = l.rows_pad;
+    a->kappa = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(shape->d)));
+    a->part = static_cast<float2*>(ws);
+    a->lse = reinterpret_cast<float*>(static_cast<char*>(ws) + l.lse_off);
+    a->group_mass = nullptr;
+    a->mass = nullptr;
+    a->anchor = nullptr;
+    return MMSKV_OK;
+}
+
+int check_score_outputs(const mmskv_params* p, const float* gm, const float* mass, const float* an) {
+    if (mass == nullptr || an == nullptr) return MMSKV_EINVAL;
+    if (p->mode == MMSKV_VOTE && gm == nullptr) return MMSKV_EINVAL;
+    if (!aligned(mass, 4) || !aligned(an, 4) || (gm && !aligned(gm, 4))) return MMSKV_EINVAL;
+    return MMSKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mmshiftkv_version(void) { return 100; }
+
+const char* mmshiftkv_status_string(int status) {
+    switch (status) {
+        case MMSKV_OK: return "ok";
+        case MMSKV_EINVAL: return "invalid argument";
+        case MMSKV_EUNSUPPORTED: return "unsupported configuration";
+        case MMSKV_EWORKSPACE: return "workspace missing, misaligned or too small";
+        case MMSKV_EHIP: return "HIP launch error";
+        default: return "unknown status";
+    }
+}
+
+int mmshiftkv_build_proxies(const mmskv_shape* shape, const mmskv_params* params, const void* q_win,
+                            int32_t q_dtype, const mmskv_strides* q_strides, const float* rope_cos_f,
+                            const float* rope_sin_f, const float* rope_cos_l, const float* rope_sin_l,
+                            uint16_t* proxies, uint16_t* q_last, double* stats, void* stream) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    rc = check_params(shape, params);
+    if (rc) return rc;
+    const int eb = elem_bytes(q_dtype);
+    if (eb == 0 || q_win == nullptr || proxies == nullptr || q_last == nullptr) return MMSKV_EINVAL;
+    rc = check_rows(q_win, q_strides, eb, false);
+    if (rc) return rc;
+    if ((rope_cos_f == nullptr) != (rope_sin_f == nullptr)) return MMSKV_EINVAL;
+    if ((rope_cos_l == nullptr) != (rope_sin_l == nullptr)) return MMSKV_EINVAL;
+    if (!aligned(proxies, 8) || !aligned(q_last, 2) || (stats && !aligned(stats, 8))) return MMSKV_EINVAL;
+    ProxyArgs a;
+    a.q = q_win;
+    a.q_dtype = q_dtype;
+    a.qsb = q_strides->sb;
+    a.qsh = q_strides->sh;
+    a.qst = q_strides->st;
+    a.cos_f = rope_cos_f;
+    a.sin_f = rope_sin_f;
+    a.cos_l = rope_cos_l;
+    a.sin_l = rope_sin_l;
+    a.proxies = proxies;
+    a.q_last = q_last;
+    a.stats = stats;
+    a.B = shape->B;
+    a.Hq = shape->Hq;
+    a.W = shape->W;
+    a.d = shape->d;
+    a.P = params->P;
+    a.ddof = params->std_ddof;
+    a.layer = params->layer;
+    a.gamma = params->gamma;
+    a.key0 = static_cast<uint32_t>(params->seed & 0xFFFFFFFFull);
+    a.key1 = static_cast<uint32_t>(params->seed >> 32);
+    return status_of(launch_build_proxies(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t mmshiftkv_score_workspace(const mmskv_shape* shape, const mmskv_params* params) {
+    if (check_shape(shape) || check_params(shape, params)) return 0;
+    return score_layout(shape, params).total;
+}
+
+int mmshiftkv_score_lse(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                        const uint16_t* q_last, const void* k, int32_t k_dtype,
+                        const mmskv_strides* k_strides, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+    ScoreArgs a;
+    int rc = prepare_score(shape, params, proxies, q_last, k, k_dtype, k_strides, workspace,
+                           workspace_bytes, &a);
+    if (rc) return rc;
+    return status_of(launch_score_lse(a, static_cast<hipStream_t>(stream)));
+}
+
+int mmshiftkv_score_mass(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                         const uint16_t* q_last, const void* k, int32_t k_dtype,
+                         const mmskv_strides* k_strides, float* group_mass, float* mass, float* anchor,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+    ScoreArgs a;
+    int rc = prepare_score(shape, params, proxies, q_last, k, k_dtype, k_strides, workspace,
+                           workspace_bytes, &a);
+    if (rc) return rc;
+    rc = check_score_outputs(params, group_mass, mass, anchor);
+    if (rc) return rc;
+    a.group_mass = group_mass;
+    a.mass = mass;
+    a.anchor = anchor;
+    return status_of(launch_score_mass(a, static_cast<hipStream_t>(stream)));
+}
+
+int mmshiftkv_score(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                    const uint16_t* q_last, const void* k, int32_t k_dtype,
+                    const mmskv_strides* k_strides, float* group_mass, float* mass, float* anchor,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+    ScoreArgs a;
+    int rc = prepare_score(shape, params, proxies, q_last, k, k_dtype, k_strides, workspace,
+                           workspace_bytes, &a);
+    if (rc) return rc;
+    rc = check_score_outputs(params, group_mass, mass, anchor);
+    if (rc) return rc;
+    a.group_mass = group_mass;
+    a.mass = mass;
+    a.anchor = anchor;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = status_of(launch_score_lse(a, s));
+    if (rc) return rc;
+    return status_of(launch_score_mass(a, s));
+}
+
+size_t mmshiftkv_select_workspace(const mmskv_shape* shape, const mmskv_params* params) {
+    if (check_shape(shape) || check_params(shape, params)) return 0;
+    return select_layout(shape, params).total;
+}
+
+int mmshiftkv_select_topk(const mmskv_shape* shape, const mmskv_params* params, const float* group_mass,
+                          const float* mass, const float* anchor, const int32_t* budgets, int32_t budget,
+                          int32_t c_max, int32_t* idx, int32_t* counts, uint8_t* votes, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    rc = check_params(shape, params);
+    if (rc) return rc;
+    if (idx == nullptr || counts == nullptr || c_max < 1) return MMSKV_EINVAL;
+    if (budgets == nullptr && (budget < 1 || c_max < (budget < shape->T ? budget : shape->T)))
+        return MMSKV_EINVAL;
+    if (params->mode == MMSKV_VOTE && (group_mass == nullptr || anchor == nullptr)) return MMSKV_EINVAL;
+    if (params->mode == MMSKV_MASS && mass == nullptr) return MMSKV_EINVAL;
+    if (params->mode == MMSKV_MASS && votes != nullptr) return MMSKV_EINVAL;
+    const SelectLayout l = select_layout(shape, params);
+    if (workspace == nullptr || !aligned(workspace, kAlign) || workspace_bytes < l.total)
+        return MMSKV_EWORKSPACE;
+    SelectArgs a;
+    a.group_mass = group_mass;
+    a.mass = mass;
+    a.anchor = anchor;
+    a.budgets = budgets;
+    a.B = shape->B;
+    a.Hkv = shape->Hkv;
+    a.T = shape->T;
+    a.G = params->G;
+    a.mode = params->mode;
+    a.keep_last = params->keep_last;
+    a.budget = budget;
+    a.c_max = c_max;
+    a.tau = params->tau;
+    a.lambda = params->lambda;
+    // fixed-point scale 2^S with S = 62 - bitlen(rows per group), so a
+    // group's total (<= rows per group, plus rounding) stays below 2^63
+    {
+        const int rows_per_group = (params->P / params->G) * (shape->Hq / shape->Hkv);
+        int bits = 0;
+        while ((1 << bits) <= rows_per_group) ++bits;
+        a.fix_scale = ldexp(1.0, 62 - bits);
+    }
+    char* w = static_cast<char*>(workspace);
+    a.theta = reinterpret_cast<uint32_t*>(w + l.theta_off);
+    a.tcut = reinterpret_cast<int32_t*>(w + l.tcut_off);
+    a.keys = reinterpret_cast<uint64_t*>(w + l.keys_off);
+    a.idx = idx;
+    a.counts = counts;
+    a.votes = votes;
+    return status_of(launch_select(a, static_cast<hipStream_t>(stream)));
+}
+
+int mmshiftkv_gather_kv(const mmskv_shape* shape, const void* k, const void* v, int32_t dtype,
+                        const mmskv_strides* k_strides, const mmskv_strides* v_strides,
+                        const int32_t* idx, const int32_t* counts, int32_t c_max, void* k_out,
+                        void* v_out, void* stream) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    const int eb = elem_bytes(dtype);
+    if (eb == 0 || k == nullptr || v == nullptr || idx == nullptr || counts == nullptr || c_max < 1 ||
+        k_out == nullptr || v_out == nullptr)
+        return MMSKV_EINVAL;
+    rc = check_rows(k, k_strides, eb, true);
+    if (rc) return rc;
+    rc = check_rows(v, v_strides, eb, true);
+    if (rc) return rc;
+    if (!aligned(k_out, 16) || !aligned(v_out, 16)) return MMSKV_EINVAL;
+    GatherArgs a;
+    a.k = k;
+    a.v = v;
+    a.ksb = k_strides->sb;
+    a.ksh = k_strides->sh;
+    a.kst = k_strides->st;
+    a.vsb = v_strides->sb;
+    a.vsh = v_strides->sh;
+    a.vst = v_strides->st;
+    a.elem_bytes = eb;
+    a.row_bytes = shape->d * eb;
+    a.idx = idx;
+    a.counts = counts;
+    a.B = shape->B;
+    a.Hkv = shape->Hkv;
+    a.T = shape->T;
+    a.c_max = c_max;
+    a.k_out = k_out;
+    a.v_out = v_out;
+    return status_of(launch_gather(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,80 @@
+// Internal launch interface between the C-ABI layer (api.cpp) and the
+// gfx950 kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mmskv {
+
+// Keys handled by one score workgroup: 4 waves x 4 sub-tiles x 16 keys.
+constexpr int kScoreWaves = 4;
+constexpr int kScoreSub = 4;
+constexpr int kScoreBlockKeys = kScoreWaves * kScoreSub * 16;
+// Rows per cross-wave merge chunk of the log-sum-exp pass.
+constexpr int kLseChunkTiles = 16;
+
+struct ProxyArgs {
+    const void* q;        // [B, Hq, W, d]
+    int q_dtype;          // 0 fp32, 1 bf16
+    int64_t qsb, qsh, qst;
+    const float* cos_f; const float* sin_f;   // [d/2] or null
+    const float* cos_l; const float* sin_l;   // [d/2] or null
+    uint16_t* proxies;    // [B, Hq, P, d]
+    uint16_t* q_last;     // [B, Hq, d]
+    double* stats;        // [B, Hq, 2, d] or null
+    int B, Hq, W, d, P, ddof, layer;
+    double gamma;
+    uint32_t key0, key1;
+};
+
+struct ScoreArgs {
+    const uint16_t* proxies;   // [B, Hq, P, d]
+    const uint16_t* q_last;    // [B, Hq, d]
+    const void* k;             // [B, Hkv, T, d]
+    int k_dtype;
+    int64_t ksb, ksh, kst;
+    int B, Hq, Hkv, T, d, P, G, Gh;
+    int n_kb;                  // key blocks of kScoreBlockKeys
+    int rows;                  // Gh * P proxy rows per KV head
+    int rows_pad;              // rows + 16 * anchor tiles
+    float kappa;               // log2(e) / sqrt(d)
+    float2* part;              // [B, Hkv, n_kb, rows_pad]  (max*kappa, sum)
+    float* lse;                // [B, Hkv, rows_pad]        log2-domain
+    float* group_mass;         // [B, Hkv, G, T] or null
+    float* mass;               // [B, Hkv, T]
+    float* anchor;             // [B, Hkv, T]
+};
+
+struct SelectArgs {
+    const float* group_mass;   // [B, Hkv, G, T]
+    const float* mass;         // [B, Hkv, T]
+    const float* anchor;       // [B, Hkv, T]
+    const int32_t* budgets;    // [B, Hkv] or null
+    int B, Hkv, T, G, mode, keep_last, budget, c_max;
+    double tau, lambda;
+    double fix_scale;          // 2^S: fixed-point scale of the tau sums
+    uint32_t* theta;           // [B, Hkv, G] cut mass (fp32 bits)
+    int32_t* tcut;             // [B, Hkv, G] last admitted index among equals
+    uint64_t* keys;            // [B, Hkv, T] score bits (fp64, non-negative)
+    int32_t* idx;              // [B, Hkv, c_max]
+    int32_t* counts;           // [B, Hkv]
+    uint8_t* votes;            // [B, Hkv, T] or null
+};
+
+struct GatherArgs {
+    const void* k; const void* v;
+    int64_t ksb, ksh, kst, vsb, vsh, vst;   // element strides
+    int elem_bytes, row_bytes;
+    const int32_t* idx; const int32_t* counts;
+    int B, Hkv, T, c_max;
+    void* k_out; void* v_out;
+};
+
+hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s);
+hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s);
+hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+
+}  // namespace mmskv

@@ -1,0 +1,189 @@
+"""The C-ABI library loads, exports every symbol include/mmshiftkv.h declares,
+and validates its arguments on the host (CPU only: no call here reaches a
+kernel launch; every call below is rejected before anything is enqueued)."""
+import ctypes
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2607_22586_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mmshiftkv.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bd.LIB_PATH):
+        from paper_2607_22586_amd import build
+        build.build()
+    return bd.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(mmshiftkv_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_select_topk", "mmshiftkv_gather_kv"):
+        assert n in names
+    assert set(names) == set(bd.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+    if shutil.which("nm"):
+        out = subprocess.run(["nm", "-D", "--defined-only", bd.LIB_PATH], capture_output=True,
+                             text=True).stdout
+        exported = set(re.findall(r" T (mmshiftkv_\w+)", out))
+        assert set(declared_functions()) <= exported
+
+
+def test_header_compiles_as_c99(tmp_path):
+    if shutil.which("gcc") is None:
+        pytest.skip("no gcc")
+    src = tmp_path / "t.c"
+    src.write_text('#include "mmshiftkv.h"\nint main(void){ mmskv_params p; mmskv_shape s; '
+                   '(void)p; (void)s; return (int)sizeof(mmskv_params); }\n')
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.dirname(HEADER), "-c",
+                    str(src), "-o", str(tmp_path / "t.o")], check=True)
+
+
+def test_struct_layout_matches_header(tmp_path):
+    if shutil.which("gcc") is None:
+        pytest.skip("no gcc")
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "mmshiftkv.h"\nint main(void){'
+                   'printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(mmskv_params), offsetof(mmskv_params, gamma),'
+                   ' offsetof(mmskv_params, seed), offsetof(mmskv_params, keep_last), sizeof(mmskv_shape),'
+                   ' sizeof(mmskv_strides)); return 0; }\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
+    want = [ctypes.sizeof(bd.Params), bd.Params.gamma.offset, bd.Params.seed.offset,
+            bd.Params.keep_last.offset, ctypes.sizeof(bd.Shape), ctypes.sizeof(bd.Strides)]
+    assert got == want
+
+
+def test_status_strings(lib):
+    assert bd.status_string(0) == "ok"
+    assert "workspace" in bd.status_string(-3)
+    assert lib.mmshiftkv_version() >= 100
+
+
+# ---------------------------------------------------------------- host validation
+FAKE = ctypes.c_void_p(0x10000)        # aligned, never dereferenced: calls fail validation first
+
+
+def _shape(B=1, Hq=4, Hkv=1, T=1024, W=16, d=64):
+    return bd.Shape(B, Hq, Hkv, T, W, d)
+
+
+def _params(**kw):
+    c = bd.SelectionConfig(**kw)
+    return c.c_params()
+
+
+def _build(lib, shape, prm, q=FAKE, prox=FAKE, ql=FAKE, strides=None, dtype=1, rope=(None, None)):
+    st = strides or bd.Strides(shape.Hq * shape.W * shape.d, shape.W * shape.d, shape.d)
+    return lib.mmshiftkv_build_proxies(ctypes.byref(shape), ctypes.byref(prm), q, dtype, ctypes.byref(st),
+                                       rope[0], rope[1], None, None, prox, ql, None, None)
+
+
+@pytest.mark.parametrize("shape,params,code", [
+    (dict(d=96), {}, bd.MMSKV_EUNSUPPORTED),
+    (dict(d=0), {}, bd.MMSKV_EINVAL),
+    (dict(Hq=6, Hkv=4), {}, bd.MMSKV_EINVAL),
+    (dict(B=0), {}, bd.MMSKV_EINVAL),
+    (dict(B=70000), {}, bd.MMSKV_EINVAL),
+    (dict(T=0), {}, bd.MMSKV_EINVAL),
+    (dict(W=0), {}, bd.MMSKV_EINVAL),
+    (dict(W=1), dict(std_ddof=1), bd.MMSKV_EINVAL),
+    ({}, dict(P=500, G=32), bd.MMSKV_EINVAL),
+    ({}, dict(P=256, G=32), bd.MMSKV_EUNSUPPORTED),      # groups of 8 rows
+    ({}, dict(P=512 * 16, G=512), bd.MMSKV_EUNSUPPORTED),
+    ({}, dict(tau=0.0), bd.MMSKV_EINVAL),
+    ({}, dict(tau=1.5), bd.MMSKV_EINVAL),
+    ({}, dict(lam=-1.0), bd.MMSKV_EINVAL),
+    ({}, dict(gamma=-1.0), bd.MMSKV_EINVAL),
+    ({}, dict(gamma=float("inf")), bd.MMSKV_EINVAL),
+    ({}, dict(layer=70000), bd.MMSKV_EINVAL),
+    ({}, dict(mode=7), bd.MMSKV_EINVAL),
+])
+def test_build_proxies_rejects(lib, shape, params, code):
+    assert _build(lib, _shape(**shape), _params(**params)) == code
+
+
+def test_build_proxies_rejects_pointers(lib):
+    s, p = _shape(), _params()
+    assert _build(lib, s, p, q=None) == bd.MMSKV_EINVAL
+    assert _build(lib, s, p, prox=None) == bd.MMSKV_EINVAL
+    assert _build(lib, s, p, dtype=5) == bd.MMSKV_EINVAL
+    assert _build(lib, s, p, rope=(FAKE, None)) == bd.MMSKV_EINVAL
+    assert _build(lib, s, p, strides=bd.Strides(-1, 0, 0)) == bd.MMSKV_EINVAL
+
+
+def test_workspace_queries(lib):
+    s, p = _shape(B=4, Hq=28, Hkv=4, T=16384, W=64, d=128), _params()
+    ws = lib.mmshiftkv_score_workspace(ctypes.byref(s), ctypes.byref(p))
+    # partial (max, sum) per (head, key block of 256, row) + one lse per row
+    rows_pad = 7 * 512 + 16
+    assert ws >= 16 * 64 * rows_pad * 8 + 16 * rows_pad * 4
+    assert ws % 256 == 0
+    wsel = lib.mmshiftkv_select_workspace(ctypes.byref(s), ctypes.byref(p))
+    assert wsel >= 16 * 16384 * 8
+    bad = _shape(d=96)
+    assert lib.mmshiftkv_score_workspace(ctypes.byref(bad), ctypes.byref(p)) == 0
+
+
+def test_score_rejects(lib):
+    s, p = _shape(), _params()
+    st = bd.Strides(1024 * 64, 1024 * 64, 64)
+    need = lib.mmshiftkv_score_workspace(ctypes.byref(s), ctypes.byref(p))
+    call = lambda ws, nbytes, gm=FAKE, k=FAKE, strides=st, dtype=1: lib.mmshiftkv_score(  # noqa: E731
+        ctypes.byref(s), ctypes.byref(p), FAKE, FAKE, k, dtype, ctypes.byref(strides), gm, FAKE, FAKE,
+        ws, nbytes, None)
+    assert call(FAKE, need - 1) == bd.MMSKV_EWORKSPACE
+    assert call(None, need) == bd.MMSKV_EWORKSPACE
+    assert call(ctypes.c_void_p(0x10010), need) == bd.MMSKV_EWORKSPACE      # not 256-byte aligned
+    assert call(FAKE, need, gm=None) == bd.MMSKV_EINVAL                    # VOTE needs group masses
+    assert call(FAKE, need, k=ctypes.c_void_p(0x10002)) == bd.MMSKV_EINVAL  # K rows not 16-byte aligned
+    assert call(FAKE, need, strides=bd.Strides(0, 0, 3)) == bd.MMSKV_EINVAL
+    assert call(FAKE, need, dtype=9) == bd.MMSKV_EINVAL
+
+
+def test_select_rejects(lib):
+    s, p = _shape(), _params()
+    need = lib.mmshiftkv_select_workspace(ctypes.byref(s), ctypes.byref(p))
+    call = lambda budget, c_max, ws=FAKE, nbytes=need, gm=FAKE, votes=None, prm=p: lib.mmshiftkv_select_topk(  # noqa: E731
+        ctypes.byref(s), ctypes.byref(prm), gm, FAKE, FAKE, None, budget, c_max, FAKE, FAKE, votes, ws,
+        nbytes, None)
+    assert call(0, 64) == bd.MMSKV_EINVAL
+    assert call(64, 63) == bd.MMSKV_EINVAL          # c_max below the budget
+    assert call(64, 64, nbytes=need - 8) == bd.MMSKV_EWORKSPACE
+    assert call(64, 64, gm=None) == bd.MMSKV_EINVAL
+    assert call(64, 64, votes=FAKE, prm=_params(mode=bd.MMSKV_MASS)) == bd.MMSKV_EINVAL
+
+
+def test_gather_rejects(lib):
+    s = _shape()
+    st = bd.Strides(1024 * 64, 1024 * 64, 64)
+    call = lambda k=FAKE, out=FAKE, dtype=1, c_max=64: lib.mmshiftkv_gather_kv(  # noqa: E731
+        ctypes.byref(s), k, FAKE, dtype, ctypes.byref(st), ctypes.byref(st), FAKE, FAKE, c_max, out, FAKE, None)
+    assert call(k=None) == bd.MMSKV_EINVAL
+    assert call(out=ctypes.c_void_p(0x10004)) == bd.MMSKV_EINVAL
+    assert call(dtype=3) == bd.MMSKV_EINVAL
+    assert call(c_max=0) == bd.MMSKV_EINVAL
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    q = torch.zeros((1, 4, 16, 64))
+    with pytest.raises(ValueError):
+        bd.build_proxies(q, bd.SelectionConfig(), T=1024, Hkv=1)
