@@ -18,6 +18,7 @@ ARCH = "gfx950"
 # Packed fp32 VALU instructions are disabled for every device compilation.
 HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=" + ARCH,
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               "-mllvm", "-amdgpu-mfma-vgpr-form",
                "-fno-fast-math", "-Wall", "-Wno-unused-command-line-argument"]
 
 

@@ -32,7 +32,7 @@ int check_params(const mmskv_shape* s, const mmskv_params* p) {
     if (p == nullptr) return MMSKV_EINVAL;
     if (p->P < 1 || p->G < 1 || p->P % p->G != 0) return MMSKV_EINVAL;
     if (p->G > 255) return MMSKV_EUNSUPPORTED;
-    if ((p->P / p->G) % 16 != 0) return MMSKV_EUNSUPPORTED;
+    if ((p->P / p->G) % 16 != 0 || p->P % 32 != 0) return MMSKV_EUNSUPPORTED;
     if (!(p->gamma >= 0.0) || !isfinite(p->gamma)) return MMSKV_EINVAL;
     if (!(p->tau > 0.0 && p->tau <= 1.0)) return MMSKV_EINVAL;
     if (!(p->lambda >= 0.0) || !isfinite(p->lambda)) return MMSKV_EINVAL;
@@ -59,16 +59,17 @@ int check_rows(const void* base, const mmskv_strides* st, int eb, bool vec16) {
 int status_of(hipError_t e) { return e == hipSuccess ? MMSKV_OK : MMSKV_EHIP; }
 
 struct ScoreLayout {
-    int n_kb, rows, rows_pad;
+    int block_keys, n_kb, rows, rows_pad;
     size_t part_bytes, lse_off, total;
 };
 
 ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
     ScoreLayout l;
     const int Gh = s->Hq / s->Hkv;
-    l.n_kb = (s->T + kScoreBlockKeys - 1) / kScoreBlockKeys;
+    l.block_keys = 64 * score_block_waves(s->B, s->Hkv, s->T);
+    l.n_kb = (s->T + l.block_keys - 1) / l.block_keys;
     l.rows = Gh * p->P;
-    l.rows_pad = l.rows + 16 * ((Gh + 15) / 16);
+    l.rows_pad = l.rows + 32 * ((Gh + 31) / 32);
     const size_t heads = static_cast<size_t>(s->B) * s->Hkv;
     l.part_bytes = heads * l.n_kb * l.rows_pad * sizeof(float2);
     l.lse_off = align_up(l.part_bytes);
@@ -121,6 +122,7 @@ int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const ui
     a->P = params->P;
     a->G = params->G;
     a->Gh = shape->Hq / shape->Hkv;
+    a->block_keys = l.block_keys;
     a->n_kb = l.n_kb;
     a->rows = l.rows;
     a->rows_pad = l.rows_pad;

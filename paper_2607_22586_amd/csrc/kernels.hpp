@@ -7,12 +7,8 @@
 
 namespace mmskv {
 
-// Keys handled by one score workgroup: 4 waves x 4 sub-tiles x 16 keys.
-constexpr int kScoreWaves = 4;
-constexpr int kScoreSub = 4;
-constexpr int kScoreBlockKeys = kScoreWaves * kScoreSub * 16;
-// Rows per cross-wave merge chunk of the log-sum-exp pass.
-constexpr int kLseChunkTiles = 16;
+// Waves per score workgroup (each wave scores 64 keys) for a problem size.
+int score_block_waves(int B, int Hkv, int T);
 
 struct ProxyArgs {
     const void* q;        // [B, Hq, W, d]
@@ -35,9 +31,10 @@ struct ScoreArgs {
     int k_dtype;
     int64_t ksb, ksh, kst;
     int B, Hq, Hkv, T, d, P, G, Gh;
-    int n_kb;                  // key blocks of kScoreBlockKeys
+    int block_keys;            // keys per workgroup (64 * waves)
+    int n_kb;                  // key blocks of block_keys
     int rows;                  // Gh * P proxy rows per KV head
-    int rows_pad;              // rows + 16 * anchor tiles
+    int rows_pad;              // rows + 32 * ceil(Gh / 32) (anchor rows, padded)
     float kappa;               // log2(e) / sqrt(d)
     float2* part;              // [B, Hkv, n_kb, rows_pad]  (max*kappa, sum)
     float* lse;                // [B, Hkv, rows_pad]        log2-domain
