@@ -15,6 +15,7 @@ namespace {
 
 constexpr int kProxyThreads = 256;
 constexpr int kProxiesPerBlock = 64;
+constexpr int kWinChunk = 64;       // window rows staged in LDS at a time
 
 // Philox4x32-10 (Salmon et al., SC 2011): ten rounds of
 // (c0,c1,c2,c3) <- (hi(M1 c2)^c1^k0, lo(M1 c2), hi(M0 c0)^c3^k1, lo(M0 c0))
@@ -136,27 +137,53 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
     double* mu = smem;            // [d]
     double* gs = smem + d;        // [d]  gamma * sigma
     double* last = smem + 2 * d;  // [d]  window query W-1
+    float* win = reinterpret_cast<float*>(smem + 3 * d);   // [kWinChunk][d] staged window rows
     const int h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     const int64_t qbase = static_cast<int64_t>(b) * a.qsb + static_cast<int64_t>(h) * a.qsh;
 
-    for (int j = tid; j < d; j += kProxyThreads) {
-        double acc = 0.0;
-        for (int w = 0; w < a.W; ++w) acc = acc + load_q(a, qbase + w * a.qst + j);
-        const double m = acc / static_cast<double>(a.W);
-        double sq = 0.0;
-        for (int w = 0; w < a.W; ++w) {
-            const double diff = load_q(a, qbase + w * a.qst + j) - m;
-            const double dd = diff * diff;
-            sq = sq + dd;
+    // stage window rows [w0, w0 + n) in LDS (values are exact in fp32)
+    auto stage = [&](int w0, int n) {
+        for (int e = tid; e < n * d; e += kProxyThreads) {
+            const int w = e / d, j = e - w * d;
+            win[e] = static_cast<float>(load_q(a, qbase + static_cast<int64_t>(w0 + w) * a.qst + j));
         }
+    };
+    // mean, then (population or sample) variance, summed in window order
+    double acc = 0.0;
+    for (int w0 = 0; w0 < a.W; w0 += kWinChunk) {
+        const int n = min(kWinChunk, a.W - w0);
+        __syncthreads();
+        stage(w0, n);
+        __syncthreads();
+        if (tid < d)
+            for (int w = 0; w < n; ++w) acc = acc + static_cast<double>(win[w * d + tid]);
+    }
+    const double m = acc / static_cast<double>(a.W);
+    double sq = 0.0;
+    const bool one_chunk = a.W <= kWinChunk;
+    for (int w0 = 0; w0 < a.W; w0 += kWinChunk) {
+        const int n = min(kWinChunk, a.W - w0);
+        if (!one_chunk) {
+            __syncthreads();
+            stage(w0, n);
+            __syncthreads();
+        }
+        if (tid < d)
+            for (int w = 0; w < n; ++w) {
+                const double diff = static_cast<double>(win[w * d + tid]) - m;
+                const double dd = diff * diff;
+                sq = sq + dd;
+            }
+    }
+    if (tid < d) {
         const double sg = sqrt(sq / static_cast<double>(a.W - a.ddof));
-        mu[j] = m;
-        gs[j] = a.gamma * sg;
-        last[j] = load_q(a, qbase + static_cast<int64_t>(a.W - 1) * a.qst + j);
+        mu[tid] = m;
+        gs[tid] = a.gamma * sg;
+        last[tid] = load_q(a, qbase + static_cast<int64_t>(a.W - 1) * a.qst + tid);
         if (a.stats != nullptr && blockIdx.x == 0) {
             double* st = a.stats + (static_cast<int64_t>(b) * a.Hq + h) * 2 * d;
-            st[j] = m;
-            st[d + j] = sg;
+            st[tid] = m;
+            st[d + tid] = sg;
         }
     }
     __syncthreads();
@@ -241,7 +268,8 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
 
 hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s) {
     dim3 grid((a.P + kProxiesPerBlock - 1) / kProxiesPerBlock, a.Hq, a.B);
-    const size_t lds = 3 * static_cast<size_t>(a.d) * sizeof(double);
+    const size_t lds = 3 * static_cast<size_t>(a.d) * sizeof(double) +
+                       static_cast<size_t>(kWinChunk) * a.d * sizeof(float);
     hipLaunchKernelGGL(build_proxies_kernel, grid, dim3(kProxyThreads), lds, s, a);
     return hipGetLastError();
 }

@@ -3,18 +3,19 @@
 //
 // tau_cut   one workgroup per (b, c, group): a mass-weighted radix select on
 //           the fp32 bit patterns of the group masses (non-negative floats
-//           order like their bits) finds the cut mass theta and, among keys
-//           whose mass equals theta, the last admitted index, such that the
-//           set {mass > theta} u {mass == theta, index <= tcut} is the shortest
-//           (mass desc, index asc) prefix whose mass reaches tau * total.
-//           Masses are summed as 2^S fixed-point integers, so every decision
-//           is independent of summation order.
+//           order like their bits; 11/11/10-bit digits) finds the cut mass
+//           theta and, among keys whose mass equals theta, the last admitted
+//           index, such that {mass > theta} u {mass == theta, index <= tcut}
+//           is the shortest (mass desc, index asc) prefix whose mass reaches
+//           tau * total.  Masses are summed as 2^S fixed-point integers, so
+//           every decision is independent of summation order.
 // vote      one thread per key: vote = #groups whose set holds the key;
 //           score = vote + lambda*anchor (fp64) or the total mass.
-// topk      one workgroup per (b, c): radix select of the (C-1)-th largest
-//           score key over [0, T-1) (or the C-th over [0, T)), then an
-//           index-ordered compaction writes the kept tokens in ascending
-//           order and appends token T-1.
+// topk      one workgroup per (b, c): radix select (11-bit digits, stopping
+//           early once a bucket is taken whole) of the (C-1)-th largest score
+//           key over [0, T-1) (or the C-th over [0, T)), then an index-ordered
+//           compaction writes the kept tokens in ascending order and appends
+//           token T-1.
 #include <math.h>
 
 #include "common.hpp"
@@ -78,6 +79,62 @@ __device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* wtot, 
     return before + below;
 }
 
+// Block-wide exclusive prefix sum of `v` over the 1024 threads in thread
+// order; also returns the block total.
+template <typename U>
+__device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
+    const int lane = lane_id(), wave = static_cast<int>(threadIdx.x) / kWave;
+    U x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        U y;
+        if constexpr (sizeof(U) == 8)
+            y = shfl_u64(x, lane >= o ? lane - o : lane);
+        else
+            y = __shfl(x, lane >= o ? lane - o : lane, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) wtot[wave] = x;
+    __syncthreads();
+    U before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+        const U t = wtot[w];
+        before += (w < wave) ? t : U(0);
+        tot += t;
+    }
+    __syncthreads();
+    total = tot;
+    return before + x - v;
+}
+
+// Digits [0, 2048) visited in descending order, thread i covering digits
+// 2047-2i and 2046-2i: finds the digit whose bucket takes the running total
+// (from the top) to `need` (need >= 1, need <= total).  Returns, through
+// shared memory, the digit, `need` minus the total of higher buckets, and the
+// bucket's count.
+template <typename U>
+__device__ __forceinline__ void descending_crossing(const U* val, const uint32_t* cnt, U need, U* wtot,
+                                                    uint32_t* s_digit, U* s_rem, uint32_t* s_cnt) {
+    const int i = static_cast<int>(threadIdx.x);
+    const int d_hi = 2047 - 2 * i, d_lo = 2046 - 2 * i;
+    const U v_hi = val[d_hi], v_lo = val[d_lo];
+    U total;
+    const U excl = block_excl_scan<U>(v_hi + v_lo, wtot, total);
+    if (excl < need && need <= excl + v_hi + v_lo) {
+        if (excl + v_hi >= need) {
+            *s_digit = d_hi;
+            *s_rem = need - excl;
+            *s_cnt = cnt[d_hi];
+        } else {
+            *s_digit = d_lo;
+            *s_rem = need - excl - v_hi;
+            *s_cnt = cnt[d_lo];
+        }
+    }
+    __syncthreads();
+}
+
 __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long* scratch) {
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     v = wave_sum_u64(v);
@@ -91,12 +148,12 @@ __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long
 
 // ---------------------------------------------------------------- tau cut
 __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
-    __shared__ uint32_t cnt[256];
-    __shared__ unsigned long long sum[256];
-    __shared__ unsigned long long scratch[kSelWaves];
+    __shared__ uint32_t cnt[2048];
+    __shared__ unsigned long long sum[2048];
+    __shared__ unsigned long long wtot64[kSelWaves];
     __shared__ uint32_t wtot[kSelWaves];
-    __shared__ uint32_t s_digit;
-    __shared__ unsigned long long s_need;
+    __shared__ uint32_t s_digit, s_cnt;
+    __shared__ unsigned long long s_rem;
     __shared__ int32_t s_tcut;
 
     const int g = blockIdx.x, c = blockIdx.y, b = blockIdx.z;
@@ -106,65 +163,47 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
 
     uint64_t local = 0;
     for (int t = tid; t < a.T; t += kSelThreads) local += to_fixed(m[t], a.fix_scale);
-    const uint64_t total = block_sum_u64(local, scratch);
-    uint64_t need = static_cast<uint64_t>(ceil(a.tau * static_cast<double>(total)));
-    if (need < 1) need = 1;
-    if (need > total) need = total;
+    const uint64_t total = block_sum_u64(local, wtot64);
     if (total == 0) {
         // every mass is below the fixed-point resolution: empty set
         if (tid == 0) { a.theta[hcg] = 0xFFFFFFFFu; a.tcut[hcg] = -1; }
         return;
     }
+    unsigned long long need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(total)));
+    if (need < 1) need = 1;
+    if (need > total) need = total;
 
-    uint32_t prefix = 0, mask = 0;
-    for (int pass = 0; pass < 4; ++pass) {
-        const int shift = 24 - 8 * pass;
-        for (int i = tid; i < 256; i += kSelThreads) { cnt[i] = 0; sum[i] = 0; }
-        if (tid == 0) { s_digit = 0; s_need = need; }
+    // digits: bits 31..21, 20..10, 9..0 (the sign bit is 0)
+    const int shifts[3] = {21, 10, 0};
+    const uint32_t masks[3] = {0u, 0xFFE00000u, 0xFFFFFC00u};
+    uint32_t prefix = 0;
+    for (int pass = 0; pass < 3; ++pass) {
+        const int shift = shifts[pass];
+        const uint32_t mask = masks[pass];
+        for (int i = tid; i < 2048; i += kSelThreads) { cnt[i] = 0; sum[i] = 0; }
         __syncthreads();
-        for (int base = 0; base < a.T; base += kSelThreads) {
-            const int t = base + tid;
-            const bool in = t < a.T;
-            const float mv = in ? m[t] : 0.f;
+        for (int t = tid; t < a.T; t += kSelThreads) {
+            const float mv = m[t];
             const uint32_t bits = __float_as_uint(mv);
-            const bool cand = in && (bits & mask) == prefix;
-            hist_add(cand, (bits >> shift) & 255u, to_fixed(mv, a.fix_scale), cnt, sum);
-        }
-        __syncthreads();
-        if (tid < kWave) {
-            // lane l covers digits 255-4l .. 252-4l (descending)
-            const int lane = tid;
-            uint64_t s4[4];
-            uint64_t mine = 0;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) { s4[j] = sum[255 - 4 * lane - j]; mine += s4[j]; }
-            uint64_t incl = mine;
-            for (int o = 1; o < kWave; o <<= 1) {
-                const uint64_t y = shfl_u64(incl, lane >= o ? lane - o : lane);
-                if (lane >= o) incl += y;
-            }
-            const uint64_t excl = incl - mine;
-            const bool hit = excl < need && need <= incl;
-            if (hit) {
-                uint64_t acc = excl;
-                int j = 0;
-                for (; j < 3; ++j) {
-                    if (acc + s4[j] >= need) break;
-                    acc += s4[j];
-                }
-                s_digit = 255 - 4 * lane - j;
-                s_need = need - acc;
+            if ((bits & mask) == prefix) {
+                const uint32_t dg = (bits >> shift) & 2047u;
+                atomicAdd(&cnt[dg], 1u);
+                atomicAdd(&sum[dg], static_cast<unsigned long long>(to_fixed(mv, a.fix_scale)));
             }
         }
         __syncthreads();
+        descending_crossing<unsigned long long>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
         prefix |= s_digit << shift;
-        mask |= 255u << shift;
-        need = s_need;
-        __syncthreads();
+        need = s_rem;
     }
-    // keys with mass == theta each carry f_theta; take the first k_eq by index
+    // keys with mass == theta each carry f_theta; the first k_eq by index
+    // enter the set (all of them when k_eq covers the bucket)
     const uint64_t f_theta = to_fixed(__uint_as_float(prefix), a.fix_scale);
     const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
+    if (k_eq >= s_cnt) {
+        if (tid == 0) { a.theta[hcg] = prefix; a.tcut[hcg] = a.T; }
+        return;
+    }
     if (tid == 0) s_tcut = a.T - 1;
     __syncthreads();
     uint64_t seen = 0;
@@ -218,9 +257,9 @@ __global__ void __launch_bounds__(256) vote_score_kernel(SelectArgs a) {
 
 // ---------------------------------------------------------------- top-k
 __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
-    __shared__ uint32_t cnt[256];
+    __shared__ uint32_t cnt[2048];
     __shared__ uint32_t wtot[kSelWaves];
-    __shared__ uint32_t s_digit, s_need;
+    __shared__ uint32_t s_digit, s_cnt, s_rem;
 
     const int c = blockIdx.x, b = blockIdx.y;
     const int64_t hc = static_cast<int64_t>(b) * a.Hkv + c;
@@ -238,61 +277,50 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
     const uint32_t want = static_cast<uint32_t>(a.keep_last ? budget - 1 : budget);
     const uint64_t* key = a.keys + hc * a.T;
 
-    uint64_t prefix = 0, mask = 0;
-    uint32_t need = want;
+    // selected: key > theta, or key == theta among the first k_eq by index
+    uint64_t theta = 0;
+    uint32_t k_eq = 0;
     if (want > 0) {
-        for (int pass = 0; pass < 8; ++pass) {
-            const int shift = 56 - 8 * pass;
-            for (int i = tid; i < 256; i += kSelThreads) cnt[i] = 0;
-            if (tid == 0) { s_digit = 0; s_need = need; }
+        const int shifts[6] = {53, 42, 31, 20, 9, 0};
+        uint64_t prefix = 0, mask = 0;
+        uint32_t need = want;
+        bool settled = false;
+        for (int pass = 0; pass < 6 && !settled; ++pass) {
+            const int shift = shifts[pass];
+            for (int i = tid; i < 2048; i += kSelThreads) cnt[i] = 0;
             __syncthreads();
             for (int base = 0; base < pool; base += kSelThreads) {
                 const int t = base + tid;
                 const bool in = t < pool;
                 const uint64_t kv = in ? key[t] : 0ull;
                 const bool cand = in && (kv & mask) == prefix;
-                hist_add(cand, static_cast<uint32_t>(kv >> shift) & 255u, 0ull, cnt, nullptr);
+                hist_add(cand, static_cast<uint32_t>(kv >> shift) & 2047u, 0ull, cnt, nullptr);
             }
             __syncthreads();
-            if (tid < kWave) {
-                const int lane = tid;
-                uint32_t c4[4], mine = 0;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) { c4[j] = cnt[255 - 4 * lane - j]; mine += c4[j]; }
-                uint32_t incl = mine;
-                for (int o = 1; o < kWave; o <<= 1) {
-                    const uint32_t y = __shfl(incl, lane >= o ? lane - o : lane, kWave);
-                    if (lane >= o) incl += y;
-                }
-                const uint32_t excl = incl - mine;
-                if (excl < need && need <= incl) {
-                    uint32_t acc = excl;
-                    int j = 0;
-                    for (; j < 3; ++j) {
-                        if (acc + c4[j] >= need) break;
-                        acc += c4[j];
-                    }
-                    s_digit = 255 - 4 * lane - j;
-                    s_need = need - acc;
-                }
-            }
-            __syncthreads();
+            descending_crossing<uint32_t>(cnt, cnt, need, wtot, &s_digit, &s_rem, &s_cnt);
             prefix |= static_cast<uint64_t>(s_digit) << shift;
-            mask |= 255ull << shift;
-            need = s_need;
-            __syncthreads();
+            mask |= (shift == 0 ? 0x1FFull : 0x7FFull) << shift;
+            need = s_rem;
+            if (s_cnt == need) {
+                // the whole bucket is taken: every key >= its lower bound
+                // (> 0, since the pool holds more keys than are wanted)
+                theta = prefix - 1;
+                k_eq = 0;
+                settled = true;
+            }
+        }
+        if (!settled) {
+            theta = prefix;
+            k_eq = need;
         }
     }
-    // selected: key > theta, or key == theta among the first `need` by index
-    const uint64_t theta = prefix;
-    const uint32_t k_eq = (want > 0) ? need : 0u;
     uint32_t eq_seen = 0, written = 0;
     for (int base = 0; base < pool; base += kSelThreads) {
         const int t = base + tid;
         const bool in = t < pool;
         const uint64_t kv = in ? key[t] : 0ull;
         const bool gt = in && want > 0 && kv > theta;
-        const bool eq = in && want > 0 && kv == theta;
+        const bool eq = in && want > 0 && k_eq > 0 && kv == theta;
         uint32_t eq_tot;
         const uint32_t eq_before = block_excl_count(eq, wtot, eq_tot);
         const bool sel = gt || (eq && eq_seen + eq_before < k_eq);

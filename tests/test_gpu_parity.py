@@ -103,7 +103,17 @@ CASES = {
     "gamma_zero": (lambda: wl.custom_layer(1, 4, 2, 513, 8, 128, seed=14), dict(P=32, G=2, seed=14, gamma=0.0), 33),
     "fp32_d128_mass": (lambda: wl.custom_layer(2, 4, 2, 777, 8, 128, dtype="f32", seed=15),
                        dict(P=64, G=4, seed=15, mode=bd.MMSKV_MASS), 60),
+    "window_150": (lambda: wl.custom_layer(1, 4, 1, 520, 150, 128, seed=16), dict(P=64, G=4, seed=16), 50),
+    "identical_keys": (lambda: _identical_keys(), dict(P=64, G=4, seed=17), 64),
 }
+
+
+def _identical_keys():
+    """Every key equal: equal masses everywhere, so tau-sets and the top-k are
+    decided by index order alone (the equal-mass paths of the selection)."""
+    x = wl.custom_layer(1, 4, 1, 1024, 16, 64, seed=17)
+    x["k"] = x["k"][:, :, :1].expand(-1, -1, 1024, -1).contiguous()
+    return x
 
 
 @pytest.mark.parametrize("case", sorted(CASES))
