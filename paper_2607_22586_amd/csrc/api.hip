@@ -11,6 +11,7 @@ using namespace mmskv;
 namespace {
 
 constexpr size_t kAlign = 256;
+constexpr size_t kMaxRowLds = 96 * 1024;   // Gh * P + 32 rows of fp32 in LDS
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -106,6 +107,8 @@ int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const ui
     rc = check_rows(k, k_strides, eb, true);
     if (rc) return rc;
     const ScoreLayout l = score_layout(shape, params);
+    // the mass pass keeps one head's row normalisers (rows_pad floats) in LDS
+    if (static_cast<size_t>(l.rows_pad) * sizeof(float) > kMaxRowLds) return MMSKV_EUNSUPPORTED;
     if (ws == nullptr || !aligned(ws, kAlign) || ws_bytes < l.total) return MMSKV_EWORKSPACE;
     a->proxies = proxies;
     a->q_last = q_last;

@@ -71,17 +71,21 @@ __device__ __forceinline__ void block_work(int n_kb, int& head, int& kb) {
     kb = logical - head * n_kb;
 }
 
-// A 32-row tile of bf16 rows of D elements in LDS: 16-byte chunk c of row r
-// is stored at slot r*(D/8) + (c ^ (r & 7)).
+// A 32-row tile of bf16 rows of D elements in LDS, each row padded by one
+// 16-byte chunk: chunk c of row r sits at slot r*(D/8 + 1) + c.  The padding
+// shifts consecutive rows by 4 banks, so the 16 rows read by 16 consecutive
+// lanes (same chunk) hit 16 different bank groups, and a lane's fragment
+// reads differ only by an immediate offset.
 template <int D>
 struct TileLds {
     static constexpr int kChunks = D / 8;             // 16-byte chunks per row
-    static constexpr int kSlots = 32 * kChunks;       // per tile
+    static constexpr int kRow = kChunks + 1;          // padded row, in chunks
+    static constexpr int kSlots = 32 * kRow;          // per tile
 };
 
 template <int D>
 __device__ __forceinline__ bf16x8 lds_frag(const u32x4* stage, int row, int chunk) {
-    return __builtin_bit_cast(bf16x8, stage[row * (D / 8) + (chunk ^ (row & 7))]);
+    return __builtin_bit_cast(bf16x8, stage[row * TileLds<D>::kRow + chunk]);
 }
 
 // Global address of row `r` of the padded row space of head (b, c): rows
@@ -97,34 +101,51 @@ __device__ __forceinline__ const uint16_t* row_ptr(const ScoreArgs& a, int b, in
     return a.q_last + (hq0 + hl) * D;
 }
 
-// Per-thread share of staging one tile: thread j moves chunk slots
-// j, j + threads, ... (global -> registers now, registers -> LDS later).
+// Per-thread share of staging one tile: thread j moves 16-byte chunks
+// j, j + threads, ... of the tile's 32 x D/8 chunks (global -> registers now,
+// registers -> LDS later).  For a tile of proxy rows the source is one
+// contiguous 32-row block, so the per-thread offsets are fixed and only the
+// tile's base pointer changes.
 template <int D, int WAVES>
 struct Stager {
     static constexpr int kThreads = 64 * WAVES;
-    static constexpr int kSlots = TileLds<D>::kSlots;
-    static constexpr int kPer = (kSlots + kThreads - 1) / kThreads;
-    static constexpr bool kExact = (kSlots % kThreads) == 0;
+    static constexpr int kChunks = 32 * TileLds<D>::kChunks;
+    static constexpr int kPer = (kChunks + kThreads - 1) / kThreads;
+    static constexpr bool kExact = (kChunks % kThreads) == 0;
     u32x4 v[kPer];
 
-    __device__ __forceinline__ void load(const ScoreArgs& a, int b, int c, int row0) {
+    static __device__ __forceinline__ int chunk_of(int k) { return static_cast<int>(threadIdx.x) + k * kThreads; }
+    static __device__ __forceinline__ bool active(int k) { return kExact || chunk_of(k) < kChunks; }
+    // element offset of the chunk within a contiguous 32-row block
+    static __device__ __forceinline__ int src_off(int k) { return 8 * chunk_of(k); }
+    // LDS slot of the chunk
+    static __device__ __forceinline__ int dst_slot(int k) {
+        const int q = chunk_of(k);
+        const int r = q / TileLds<D>::kChunks;
+        return r * TileLds<D>::kRow + (q - r * TileLds<D>::kChunks);
+    }
+    // 32 consecutive proxy rows starting at `base`
+    __device__ __forceinline__ void load_block(const uint16_t* base, const int (&off)[kPer]) {
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+            if (active(k)) v[k] = *reinterpret_cast<const u32x4*>(base + off[k]);
+    }
+    // any tile of the padded row space (anchor rows)
+    __device__ __forceinline__ void load_rows(const ScoreArgs& a, int b, int c, int row0) {
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
-            const int slot = static_cast<int>(threadIdx.x) + k * kThreads;
-            if (kExact || slot < kSlots) {
-                const int r = slot / TileLds<D>::kChunks;
-                const int cs = slot - r * TileLds<D>::kChunks;
-                const int cg = cs ^ (r & 7);
-                v[k] = *reinterpret_cast<const u32x4*>(row_ptr<D>(a, b, c, row0 + r) + 8 * cg);
+            if (active(k)) {
+                const int q = chunk_of(k);
+                const int r = q / TileLds<D>::kChunks;
+                const int cs = q - r * TileLds<D>::kChunks;
+                v[k] = *reinterpret_cast<const u32x4*>(row_ptr<D>(a, b, c, row0 + r) + 8 * cs);
             }
         }
     }
     __device__ __forceinline__ void store(u32x4* stage) const {
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int slot = static_cast<int>(threadIdx.x) + k * kThreads;
-            if (kExact || slot < kSlots) stage[slot] = v[k];
-        }
+        for (int k = 0; k < kPer; ++k)
+            if (active(k)) stage[dst_slot(k)] = v[k];
     }
 };
 
@@ -153,21 +174,48 @@ __device__ __forceinline__ void load_keys(const ScoreArgs& a, int b, int c, int 
     }
 }
 
-// The MFMAs of one tile.  KEYS_AS_ROWS: D = K * P^T (lane holds one proxy
-// column, 16 keys per sub-tile); otherwise D = P * K^T (lane holds one key
-// column, 16 proxy rows).
+// Fragments of one 32-row tile for this lane: row (lane % 32), 16-byte
+// chunks 2*kc + lane/32.
+template <int D>
+__device__ __forceinline__ void read_frags(const u32x4* sp, bf16x8 (&A)[D / 16], int lane) {
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) A[kc] = lds_frag<D>(sp, lane & 31, 2 * kc + (lane >> 5));
+}
+
+// The MFMAs of one tile from the fragments in A; as soon as chunk kc has been
+// issued, A[kc] is refilled from the next tile's LDS slot, so the LDS latency
+// hides behind the remaining MFMAs.  KEYS_AS_ROWS: D = K * P^T (lane holds one
+// proxy column, 16 keys per sub-tile); otherwise D = P * K^T (lane holds one
+// key column, 16 proxy rows).
 template <int D, bool KEYS_AS_ROWS>
-__device__ __forceinline__ void tile_mfma(const u32x4* sp, const bf16x8 (&kf)[kSub][D / 16],
-                                          floatx16 (&acc)[kSub], int lane) {
+__device__ __forceinline__ void tile_mfma(bf16x8 (&A)[D / 16], const u32x4* next,
+                                          const bf16x8 (&kf)[kSub][D / 16], floatx16 (&acc)[kSub],
+                                          int lane, const floatx16& init) {
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) {
-        const bf16x8 pf = lds_frag<D>(sp, lane & 31, 2 * kc + (lane >> 5));
 #pragma unroll
         for (int s = 0; s < kSub; ++s) {
-            const floatx16 c0 = (kc == 0) ? zero16() : acc[s];
-            acc[s] = KEYS_AS_ROWS ? mfma32(kf[s][kc], pf, c0) : mfma32(pf, kf[s][kc], c0);
+            const floatx16 c0 = (kc == 0) ? init : acc[s];
+            acc[s] = KEYS_AS_ROWS ? mfma32(kf[s][kc], A[kc], c0) : mfma32(A[kc], kf[s][kc], c0);
         }
+        A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
     }
+}
+
+// Accumulator start for a P * K^T tile whose rows begin at `rowv`: each
+// lane's 16 rows (8*m + 4*(lane/32) + j) get -L_row/kappa, so the MFMA result
+// is s - L/kappa and the probability is 2^(kappa * acc).
+__device__ __forceinline__ floatx16 row_offsets(const float* rowv, int lane) {
+    floatx16 c;
+#pragma unroll
+    for (int m4 = 0; m4 < 4; ++m4) {
+        const float4 v = *reinterpret_cast<const float4*>(rowv + 8 * m4 + 4 * (lane >> 5));
+        c[4 * m4 + 0] = v.x;
+        c[4 * m4 + 1] = v.y;
+        c[4 * m4 + 2] = v.z;
+        c[4 * m4 + 3] = v.w;
+    }
+    return c;
 }
 
 // ---------------------------------------------------------------- pass 1
@@ -197,10 +245,13 @@ __device__ __forceinline__ float2 column_lse(const floatx16 (&acc)[kSub], uint32
     return make_float2(mk, l);
 }
 
+constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batched
+
 template <int D, int WAVES, bool FULL>
 __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, int b, int c,
-                                         u32x4 (&stage)[2][TileLds<D>::kSlots],
-                                         float2 (&mrg)[2][WAVES][32]) {
+                                         u32x4 (&stage)[3][TileLds<D>::kSlots],
+                                         float2 (&mrg)[2][kMergeTiles][WAVES][32]) {
+    using St = Stager<D, WAVES>;
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
     const int key0 = kb * 64 * WAVES + wave * kWaveKeys;
     const float kappa = a.kappa;
@@ -218,50 +269,77 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     }
 
     const int n_tiles = a.rows_pad / 32;
-    float2* part = a.part + (static_cast<int64_t>(head) * a.n_kb + kb) * a.rows_pad;
-    auto merge = [&](int slot, int tile) {
-        float M = -INFINITY;
+    const int n_prox = a.rows / 32;
+    const uint16_t* pbase =
+        a.proxies + (static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh) * a.P * D;
+    int off[St::kPer];
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) M = fmaxf(M, mrg[slot][w][lane].x);
-        float S = 0.f;
-        if (M != -INFINITY) {
-#pragma unroll
-            for (int w = 0; w < WAVES; ++w) S += mrg[slot][w][lane].y * exp2f(mrg[slot][w][lane].x - M);
-        }
-        part[32 * tile + lane] = make_float2(M, S);
+    for (int k = 0; k < St::kPer; ++k) off[k] = St::src_off(k);
+    // tile t = rows [32t, 32t+32) of the padded row space
+    auto load_tile = [&](St& st, int t) {
+        if (t < n_prox) st.load_block(pbase + static_cast<int64_t>(32 * t) * D, off);
+        else st.load_rows(a, b, c, 32 * t);
     };
 
-    Stager<D, WAVES> st0, st1;
-    st0.load(a, b, c, 0);
-    st0.store(stage[0]);
-    if (n_tiles > 1) st1.load(a, b, c, 32);
-    if (n_tiles > 2) st0.load(a, b, c, 64);
+    float2* part = a.part + (static_cast<int64_t>(head) * a.n_kb + kb) * a.rows_pad;
+    // merged (max, sum) over the waves of tiles [16k, 16k+16), all threads
+    auto merge_chunk = [&](int k) {
+        const int n_in = min(kMergeTiles, n_tiles - kMergeTiles * k);
+        for (int i = static_cast<int>(threadIdx.x); i < n_in * 32; i += 64 * WAVES) {
+            const int tl = i >> 5, r = i & 31;
+            float M = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < WAVES; ++w) M = fmaxf(M, mrg[k & 1][tl][w][r].x);
+            float S = 0.f;
+            if (M != -INFINITY) {
+#pragma unroll
+                for (int w = 0; w < WAVES; ++w)
+                    S += mrg[k & 1][tl][w][r].y * fast_exp2(mrg[k & 1][tl][w][r].x - M);
+            }
+            part[32 * (kMergeTiles * k + tl) + r] = make_float2(M, S);
+        }
+    };
+
+    // Pipeline (LDS slots t % 3): in iteration t the proxy rows of tile t+2
+    // go registers -> LDS, tile t+3 is fetched into registers, the MFMAs of
+    // tile t run from A while A is refilled with tile t+1, and the column
+    // statistics of tile t-1 are computed.
+    St st;
+    bf16x8 A[D / 16];
+    load_tile(st, 0);
+    st.store(stage[0]);
+    if (n_tiles > 1) {
+        load_tile(st, 1);
+        st.store(stage[1]);
+    }
+    if (n_tiles > 2) load_tile(st, 2);
     __syncthreads();
+    read_frags<D>(stage[0], A, lane);
 
     floatx16 acc[2][kSub];
-    // tile t: staged in stage[t & 1] during iteration t-1; MFMA in iteration
-    // t; column statistics in iteration t+1; merged over waves in t+2
-    auto stage_next = [&](auto parity, int t) {
-        constexpr int cur = decltype(parity)::value;
-        if (t + 1 < n_tiles) {
-            if constexpr (cur == 0) st1.store(stage[1]); else st0.store(stage[0]);
-            if (t + 3 < n_tiles) {
-                if constexpr (cur == 0) st1.load(a, b, c, 32 * (t + 3)); else st0.load(a, b, c, 32 * (t + 3));
-            }
+    auto stage_next = [&](int t) {
+        if (t + 2 < n_tiles) {
+            st.store(stage[(t + 2) % 3]);
+            if (t + 3 < n_tiles) load_tile(st, t + 3);
         }
     };
+    auto stats_of = [&](const floatx16 (&ac)[kSub], int tile) {
+        const float2 r = column_lse<FULL>(ac, valid, kappa);
+        if (lane < 32) mrg[(tile / kMergeTiles) & 1][tile % kMergeTiles][wave][lane] = r;
+    };
     // iteration 0
-    stage_next(Parity<0>{}, 0);
-    tile_mfma<D, true>(stage[0], kf, acc[0], lane);
+    stage_next(0);
+    tile_mfma<D, true>(A, stage[1 % 3], kf, acc[0], lane, zero16());
     __syncthreads();
-    // steady state: MFMA of tile t next to the statistics of tile t-1
+    // steady state; the merge of chunk k once its last tile's statistics are
+    // in LDS
     auto body = [&](auto parity, int t) {
         constexpr int cur = decltype(parity)::value, prev = cur ^ 1;
-        stage_next(parity, t);
-        tile_mfma<D, true>(stage[cur], kf, acc[cur], lane);
-        const float2 r = column_lse<FULL>(acc[prev], valid, kappa);
-        if (lane < 32) mrg[prev][wave][lane] = r;
-        if (t >= 2 && wave == (t % WAVES) && lane < 32) merge(cur, t - 2);
+        stage_next(t);
+        tile_mfma<D, true>(A, stage[(t + 1) % 3], kf, acc[cur], lane, zero16());
+        stats_of(acc[prev], t - 1);
+        if (t >= kMergeTiles + 1 && ((t - kMergeTiles - 1) % kMergeTiles) == 0)
+            merge_chunk((t - kMergeTiles - 1) / kMergeTiles);
         __syncthreads();
     };
     int t = 1;
@@ -273,22 +351,18 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         body(Parity<1>{}, t);
         ++t;
     }
-    // t == n_tiles: statistics of the last tile, merges of the last two
-    {
-        const int last = n_tiles - 1;
-        const int ps = last & 1;
-        const float2 r = ps ? column_lse<FULL>(acc[1], valid, kappa) : column_lse<FULL>(acc[0], valid, kappa);
-        if (lane < 32) mrg[ps][wave][lane] = r;
-        if (n_tiles >= 2 && wave == 0 && lane < 32) merge(ps ^ 1, last - 1);
-        __syncthreads();
-        if (wave == 1 % WAVES && lane < 32) merge(ps, last);
-    }
+    // t == n_tiles: statistics of the last tile, then the unmerged chunks
+    if ((n_tiles - 1) & 1) stats_of(acc[1], n_tiles - 1); else stats_of(acc[0], n_tiles - 1);
+    __syncthreads();
+    // the loop merged chunk k at t = 16k + 17 for every such t <= n_tiles - 1
+    const int merged = n_tiles >= kMergeTiles + 2 ? (n_tiles - kMergeTiles - 2) / kMergeTiles + 1 : 0;
+    for (int k = merged; k * kMergeTiles < n_tiles; ++k) merge_chunk(k);
 }
 
 template <int D, int WAVES>
 __global__ void __launch_bounds__(64 * WAVES) score_lse_kernel(ScoreArgs a) {
-    __shared__ u32x4 stage[2][TileLds<D>::kSlots];
-    __shared__ float2 mrg[2][WAVES][32];
+    __shared__ u32x4 stage[3][TileLds<D>::kSlots];
+    __shared__ float2 mrg[2][kMergeTiles][WAVES][32];
     int head, kb;
     block_work(a.n_kb, head, kb);
     const int b = head / a.Hkv, c = head - b * a.Hkv;
@@ -318,22 +392,19 @@ __global__ void __launch_bounds__(256) lse_combine_kernel(ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------- pass 2
-// p = 2^(s*kappa - L) of one tile, summed over this lane's rows 0-15 (hA)
-// and rows 16-31 (hB) of the tile; lrow = the tile's 32 L values in LDS.
-__device__ __forceinline__ void tile_probs(const floatx16 (&acc)[kSub], const float* lrow, float kappa,
-                                           int lane, float (&hA)[kSub], float (&hB)[kSub]) {
-    float4 l4[4];
-#pragma unroll
-    for (int m4 = 0; m4 < 4; ++m4) l4[m4] = *reinterpret_cast<const float4*>(lrow + 8 * m4 + 4 * (lane >> 5));
+// p = 2^(kappa * acc) of one tile (acc already holds s - L/kappa), summed
+// over this lane's rows 0-15 (hA) and rows 16-31 (hB) of the tile.
+__device__ __forceinline__ void tile_probs(const floatx16 (&acc)[kSub], float kappa, float (&hA)[kSub],
+                                           float (&hB)[kSub]) {
 #pragma unroll
     for (int s = 0; s < kSub; ++s) {
         float sa = 0.f, sb = 0.f;
 #pragma unroll
         for (int m4 = 0; m4 < 4; ++m4) {
-            const float e0 = fast_exp2(fmaf(acc[s][4 * m4 + 0], kappa, -l4[m4].x));
-            const float e1 = fast_exp2(fmaf(acc[s][4 * m4 + 1], kappa, -l4[m4].y));
-            const float e2 = fast_exp2(fmaf(acc[s][4 * m4 + 2], kappa, -l4[m4].z));
-            const float e3 = fast_exp2(fmaf(acc[s][4 * m4 + 3], kappa, -l4[m4].w));
+            const float e0 = fast_exp2(acc[s][4 * m4 + 0] * kappa);
+            const float e1 = fast_exp2(acc[s][4 * m4 + 1] * kappa);
+            const float e2 = fast_exp2(acc[s][4 * m4 + 2] * kappa);
+            const float e3 = fast_exp2(acc[s][4 * m4 + 3] * kappa);
             if (m4 < 2) sa += (e0 + e1) + (e2 + e3); else sb += (e0 + e1) + (e2 + e3);
         }
         hA[s] = sa;
@@ -341,10 +412,25 @@ __device__ __forceinline__ void tile_probs(const floatx16 (&acc)[kSub], const fl
     }
 }
 
+// Position of a pass-2 tile: proxy block u (rows 32u.. of each head) and
+// head h, visited u-major; advance() steps to the next tile.
+struct TileCursor {
+    int t, u, h;
+    __device__ __forceinline__ void advance(int Gh) {
+        ++t;
+        if (++h == Gh) {
+            h = 0;
+            ++u;
+        }
+    }
+};
+
 template <int D, int WAVES>
 __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
-    __shared__ u32x4 stage[2][TileLds<D>::kSlots];
-    __shared__ __align__(16) float lring[4][32];
+    using St = Stager<D, WAVES>;
+    __shared__ u32x4 stage[3][TileLds<D>::kSlots];
+    extern __shared__ float4 dyn_lds[];
+    float* Llds = reinterpret_cast<float*>(dyn_lds);     // [rows_pad]
 
     int head, kb;
     block_work(a.n_kb, head, kb);
@@ -358,41 +444,45 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     load_keys<D>(a, b, c, key0, kf);
 
     const int g = a.P / a.G;                 // proxies per group, multiple of 16
-    const int n_u = a.P / 32;
-    const int n_prox_tiles = n_u * a.Gh;
+    const int n_prox_tiles = (a.P / 32) * a.Gh;
     const int n_tiles = n_prox_tiles + (a.rows_pad - a.rows) / 32;
-    // tile t < n_prox_tiles: proxies 32u.. of head h with u = t / Gh, h = t % Gh;
-    // later tiles: anchor rows
-    auto tile_row0 = [&](int t) -> int {
-        if (t < n_prox_tiles) {
-            const int u = t / a.Gh;
-            return (t - u * a.Gh) * a.P + 32 * u;
-        }
-        return a.rows + 32 * (t - n_prox_tiles);
+    const uint16_t* pbase =
+        a.proxies + (static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh) * a.P * D;
+    int off[St::kPer];
+#pragma unroll
+    for (int k = 0; k < St::kPer; ++k) off[k] = St::src_off(k);
+
+    // this head's row offsets -L/kappa, all rows, stay in LDS for the whole kernel
+    const float inv_kappa = 1.0f / kappa;
+    for (int i = static_cast<int>(threadIdx.x); i < a.rows_pad; i += 64 * WAVES) Llds[i] = -L[i] * inv_kappa;
+
+    // tiles t < n_prox_tiles: proxies 32u.. of head h; later: anchor rows
+    auto load_tile = [&](St& st, const TileCursor& q) {
+        if (q.t < n_prox_tiles)
+            st.load_block(pbase + static_cast<int64_t>(q.h * a.P + 32 * q.u) * D, off);
+        else
+            st.load_rows(a, b, c, a.rows + 32 * (q.t - n_prox_tiles));
     };
 
-    Stager<D, WAVES> st0, st1;
-    float4 lg0 = make_float4(0.f, 0.f, 0.f, 0.f), lg1 = lg0;   // L staging, threads < 8
-    const bool lthr = threadIdx.x < 8;
-    auto load_l = [&](int t) {
-        return *reinterpret_cast<const float4*>(L + tile_row0(t) + 4 * static_cast<int>(threadIdx.x));
-    };
-    auto store_l = [&](int t, float4 v) {
-        *reinterpret_cast<float4*>(&lring[t & 3][4 * threadIdx.x]) = v;
-    };
-    st0.load(a, b, c, tile_row0(0));
-    if (lthr) lg0 = load_l(0);
-    st0.store(stage[0]);
-    if (lthr) store_l(0, lg0);
+    // Pipeline (LDS slots t % 3): in iteration t the rows of tile t+2 go
+    // registers -> LDS, tile t+3 is fetched into registers, the MFMAs of tile
+    // t run from A while A is refilled with tile t+1, and the probabilities
+    // of tile t-1 are formed.
+    St st;
+    bf16x8 A[D / 16];
+    TileCursor q3{0, 0, 0};                  // next tile to fetch
+    load_tile(st, q3);
+    st.store(stage[0]);
+    q3.advance(a.Gh);
     if (n_tiles > 1) {
-        st1.load(a, b, c, tile_row0(1));
-        if (lthr) lg1 = load_l(1);
+        load_tile(st, q3);
+        st.store(stage[1]);
     }
-    if (n_tiles > 2) {
-        st0.load(a, b, c, tile_row0(2));
-        if (lthr) lg0 = load_l(2);
-    }
+    q3.advance(a.Gh);
+    if (n_tiles > 2) load_tile(st, q3);
+    q3.advance(a.Gh);
     __syncthreads();
+    read_frags<D>(stage[0], A, lane);
 
     const int64_t gm_base = static_cast<int64_t>(head) * a.G * a.T;
     const int my_key = key0 + lane;          // lanes < 32: sub-tile 0, lanes >= 32: sub-tile 1
@@ -415,14 +505,15 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     // rows 0-15 of tile (u, h) belong to proxy group (32u)/g, rows 16-31 to
     // (32u+16)/g; runA / runB sum each half over the Gh heads and `open`
     // carries a group that spans several tiles
-    auto group_step = [&](int tp, const float (&hA)[kSub], const float (&hB)[kSub]) {
+    TileCursor q1{0, 0, 0};                  // tile whose probabilities come next
+    auto group_step = [&](const float (&hA)[kSub], const float (&hB)[kSub]) {
 #pragma unroll
         for (int s = 0; s < kSub; ++s) {
             runA[s] += hA[s];
             runB[s] += hB[s];
         }
-        const int u = tp / a.Gh;
-        if (tp - u * a.Gh == a.Gh - 1) {
+        if (q1.h == a.Gh - 1) {
+            const int u = q1.u;
 #pragma unroll
             for (int s = 0; s < kSub; ++s) {
                 open[s] += runA[s];
@@ -436,61 +527,48 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
             }
             if (((32 * u + 32) % g) == 0) flush_group(open, (32 * u + 16) / g);
         }
+        q1.advance(a.Gh);
     };
     auto anchor_step = [&](int tp, const floatx16 (&ac)[kSub]) {
         // anchor rows of tile tp: query head 32*(tp - n_prox_tiles) + row
-        const float* lrow = lring[tp & 3];
         const int h0 = 32 * (tp - n_prox_tiles) + 4 * (lane >> 5);
 #pragma unroll
-        for (int m4 = 0; m4 < 4; ++m4) {
-            const float4 l4 = *reinterpret_cast<const float4*>(lrow + 8 * m4 + 4 * (lane >> 5));
-            const float lj[4] = {l4.x, l4.y, l4.z, l4.w};
+        for (int m4 = 0; m4 < 4; ++m4)
 #pragma unroll
             for (int s = 0; s < kSub; ++s)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const float e = fast_exp2(fmaf(ac[s][4 * m4 + j], kappa, -lj[j]));
+                    const float e = fast_exp2(ac[s][4 * m4 + j] * kappa);
                     aacc[s] += (h0 + 8 * m4 + j < a.Gh) ? e : 0.f;
                 }
-        }
     };
 
     floatx16 acc[2][kSub];
-    // tile t: staged during iteration t-1 (proxy rows in stage[t & 1], L
-    // values in lring[t & 3]); MFMA in iteration t; probabilities in t+1
-    auto stage_next = [&](auto parity, int t) {
-        constexpr int cur = decltype(parity)::value;
-        if (t + 1 < n_tiles) {
-            if constexpr (cur == 0) {
-                st1.store(stage[1]);
-                if (lthr) store_l(t + 1, lg1);
-            } else {
-                st0.store(stage[0]);
-                if (lthr) store_l(t + 1, lg0);
-            }
-            if (t + 3 < n_tiles) {
-                if constexpr (cur == 0) {
-                    st1.load(a, b, c, tile_row0(t + 3));
-                    if (lthr) lg1 = load_l(t + 3);
-                } else {
-                    st0.load(a, b, c, tile_row0(t + 3));
-                    if (lthr) lg0 = load_l(t + 3);
-                }
-            }
+    auto stage_next = [&](int t) {
+        if (t + 2 < n_tiles) {
+            st.store(stage[(t + 2) % 3]);
+            if (t + 3 < n_tiles) load_tile(st, q3);
         }
+        q3.advance(a.Gh);
     };
-    stage_next(Parity<0>{}, 0);
-    tile_mfma<D, false>(stage[0], kf, acc[0], lane);
+    TileCursor q0{0, 0, 0};                  // tile whose MFMAs come next
+    auto tile_row = [&](const TileCursor& q) {
+        return q.t < n_prox_tiles ? q.h * a.P + 32 * q.u : a.rows + 32 * (q.t - n_prox_tiles);
+    };
+    stage_next(0);
+    tile_mfma<D, false>(A, stage[1 % 3], kf, acc[0], lane, row_offsets(Llds + tile_row(q0), lane));
+    q0.advance(a.Gh);
     __syncthreads();
     // steady state over proxy tiles: MFMA of tile t next to the
     // probabilities of tile t-1 (the last of these MFMAs may be an anchor tile)
     auto body = [&](auto parity, int t) {
         constexpr int cur = decltype(parity)::value, prev = cur ^ 1;
-        stage_next(parity, t);
-        tile_mfma<D, false>(stage[cur], kf, acc[cur], lane);
+        stage_next(t);
+        tile_mfma<D, false>(A, stage[(t + 1) % 3], kf, acc[cur], lane, row_offsets(Llds + tile_row(q0), lane));
+        q0.advance(a.Gh);
         float hA[kSub], hB[kSub];
-        tile_probs(acc[prev], lring[(t - 1) & 3], kappa, lane, hA, hB);
-        group_step(t - 1, hA, hB);
+        tile_probs(acc[prev], kappa, hA, hB);
+        group_step(hA, hB);
         __syncthreads();
     };
     int t = 1;
@@ -506,8 +584,9 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     auto anchor_body = [&](auto parity, int t) {
         constexpr int cur = decltype(parity)::value, prev = cur ^ 1;
         if (t < n_tiles) {
-            stage_next(parity, t);
-            tile_mfma<D, false>(stage[cur], kf, acc[cur], lane);
+            stage_next(t);
+            tile_mfma<D, false>(A, stage[(t + 1) % 3], kf, acc[cur], lane, row_offsets(Llds + tile_row(q0), lane));
+            q0.advance(a.Gh);
         }
         anchor_step(t - 1, acc[prev]);
         __syncthreads();
@@ -537,7 +616,8 @@ hipError_t lse_impl(const ScoreArgs& a, hipStream_t s) {
 
 template <int D, int WAVES>
 hipError_t mass_impl(const ScoreArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((score_mass_kernel<D, WAVES>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES), 0, s, a);
+    hipLaunchKernelGGL((score_mass_kernel<D, WAVES>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES),
+                       static_cast<size_t>(a.rows_pad) * sizeof(float), s, a);
     return hipGetLastError();
 }
 
