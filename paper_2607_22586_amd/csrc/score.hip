@@ -182,26 +182,6 @@ __device__ __forceinline__ void read_frags(const u32x4* sp, bf16x8 (&A)[D / 16],
     for (int kc = 0; kc < D / 16; ++kc) A[kc] = lds_frag<D>(sp, lane & 31, 2 * kc + (lane >> 5));
 }
 
-// The MFMAs of one tile from the fragments in A; as soon as chunk kc has been
-// issued, A[kc] is refilled from the next tile's LDS slot, so the LDS latency
-// hides behind the remaining MFMAs.  KEYS_AS_ROWS: D = K * P^T (lane holds one
-// proxy column, 16 keys per sub-tile); otherwise D = P * K^T (lane holds one
-// key column, 16 proxy rows).
-template <int D, bool KEYS_AS_ROWS>
-__device__ __forceinline__ void tile_mfma(bf16x8 (&A)[D / 16], const u32x4* next,
-                                          const bf16x8 (&kf)[kSub][D / 16], floatx16 (&acc)[kSub],
-                                          int lane, const floatx16& init) {
-#pragma unroll
-    for (int kc = 0; kc < D / 16; ++kc) {
-#pragma unroll
-        for (int s = 0; s < kSub; ++s) {
-            const floatx16 c0 = (kc == 0) ? init : acc[s];
-            acc[s] = KEYS_AS_ROWS ? mfma32(kf[s][kc], A[kc], c0) : mfma32(A[kc], kf[s][kc], c0);
-        }
-        A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
-    }
-}
-
 // Accumulator start for a P * K^T tile whose rows begin at `rowv`: each
 // lane's 16 rows (8*m + 4*(lane/32) + j) get -L_row/kappa, so the MFMA result
 // is s - L/kappa and the probability is 2^(kappa * acc).
@@ -218,38 +198,45 @@ __device__ __forceinline__ floatx16 row_offsets(const float* rowv, int lane) {
     return c;
 }
 
-// ---------------------------------------------------------------- pass 1
-// (max*kappa, sum 2^(s*kappa - max*kappa)) of one proxy column over the
-// wave's keys; FULL: every key of the block is < T.
-template <bool FULL>
-__device__ __forceinline__ float2 column_lse(const floatx16 (&acc)[kSub], uint32_t valid, float kappa) {
-    float m = -INFINITY;
-#pragma unroll
-    for (int s = 0; s < kSub; ++s)
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-            m = (FULL || ((valid >> (16 * s + i)) & 1u)) ? fmaxf(m, acc[s][i]) : m;
-    m = fmaxf(m, shfl_xor_f(m, 32));
-    const float mk = m * kappa;
-    float l = 0.f;
-    if (FULL || m != -INFINITY) {
-#pragma unroll
-        for (int s = 0; s < kSub; ++s)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const float e = fast_exp2(fmaf(acc[s][i], kappa, -mk));
-                l += (FULL || ((valid >> (16 * s + i)) & 1u)) ? e : 0.f;
-            }
-    }
-    l += shfl_xor_f(l, 32);
-    return make_float2(mk, l);
+// Column totals over both half-waves for the wave's 64 keys: lane l < 32
+// returns x0(l) + x0(l + 32) (sub-tile 0, key l), lane l >= 32 returns
+// x1(l - 32) + x1(l) (sub-tile 1, key l), so lane l ends with key key0 + l.
+__device__ __forceinline__ float pair_sum(float x0, float x1) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Both half-waves' maximum in every lane.
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Both half-waves' sum in every lane.
+__device__ __forceinline__ float pair_total(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+constexpr int kRing = 4;   // LDS tile slots of the pipelined passes
+
+template <int N>
+struct Tag {
+    static constexpr int value = N;
+};
+
+// ---------------------------------------------------------------- pass 1
 constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batched
 
+// Pass 1 in the K * P^T layout: lane l holds proxy column l % 32 of a tile and
+// keys key0 + 32*s + 8*(i/4) + 4*(l/32) + i%4 of sub-tile s (value 16*s + i of
+// the lane).  Per tile and column, m = max over the wave's 64 keys and
+// l = sum 2^(s*kappa - m*kappa); the pair (m*kappa, l) goes to LDS and the
+// waves' pairs are merged every kMergeTiles tiles into one partial per
+// (row, key block).  FULL: every key of the block is < T.
 template <int D, int WAVES, bool FULL>
 __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, int b, int c,
-                                         u32x4 (&stage)[3][TileLds<D>::kSlots],
+                                         u32x4 (&stage)[kRing][TileLds<D>::kSlots],
                                          float2 (&mrg)[2][kMergeTiles][WAVES][32]) {
     using St = Stager<D, WAVES>;
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
@@ -258,7 +245,6 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
 
     bf16x8 kf[kSub][D / 16];
     load_keys<D>(a, b, c, key0, kf);
-    // keys this lane sees in the K*P^T layout: key0 + 32*s + 8*(i/4) + 4*(lane/32) + i%4
     uint32_t valid = 0;
     if (!FULL) {
 #pragma unroll
@@ -275,8 +261,9 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     int off[St::kPer];
 #pragma unroll
     for (int k = 0; k < St::kPer; ++k) off[k] = St::src_off(k);
+    St st;
     // tile t = rows [32t, 32t+32) of the padded row space
-    auto load_tile = [&](St& st, int t) {
+    auto load_tile = [&](int t) {
         if (t < n_prox) st.load_block(pbase + static_cast<int64_t>(32 * t) * D, off);
         else st.load_rows(a, b, c, 32 * t);
     };
@@ -300,68 +287,117 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         }
     };
 
-    // Pipeline (LDS slots t % 3): in iteration t the proxy rows of tile t+2
-    // go registers -> LDS, tile t+3 is fetched into registers, the MFMAs of
-    // tile t run from A while A is refilled with tile t+1, and the column
-    // statistics of tile t-1 are computed.
-    St st;
-    bf16x8 A[D / 16];
-    load_tile(st, 0);
-    st.store(stage[0]);
-    if (n_tiles > 1) {
-        load_tile(st, 1);
-        st.store(stage[1]);
+    // Pipeline over the tiles t (LDS slot t % 4), as in pass 2: iteration t
+    // issues the MFMAs of tile t while refilling the fragments with tile t+1
+    // and forming the column statistics of tile t-1, then stages tile t+3
+    // (registers -> LDS) and fetches tile t+4; one barrier after every even
+    // iteration.  The chunk of tiles [16k, 16k+16) is merged in iteration
+    // 16k+17, after the barrier that follows its last statistics.
+    for (int k = 0; k < 3; ++k) {
+        if (k < n_tiles) {
+            load_tile(k);
+            st.store(stage[k]);
+        }
     }
-    if (n_tiles > 2) load_tile(st, 2);
+    if (3 < n_tiles) load_tile(3);
     __syncthreads();
+    bf16x8 A[D / 16];
     read_frags<D>(stage[0], A, lane);
 
+    constexpr int kMfmas = kSub * (D / 16);
+    constexpr int kMaxSlots = kMfmas / 4;                   // MFMA slots carrying the maximum
+    constexpr int kMaxPer = 16 / kMaxSlots;                 // value pairs per such slot
+    constexpr int kExpSlots = kMfmas - kMaxSlots - 1;       // slots carrying exp and sum
+    constexpr int kExpPer = (32 + kExpSlots - 1) / kExpSlots;
     floatx16 acc[2][kSub];
-    auto stage_next = [&](int t) {
-        if (t + 2 < n_tiles) {
-            st.store(stage[(t + 2) % 3]);
-            if (t + 3 < n_tiles) load_tile(st, t + 3);
+    auto value = [&](const floatx16 (&ac)[kSub], int idx) { return ac[idx >> 4][idx & 15]; };
+    auto ok = [&](int idx) { return FULL || ((valid >> idx) & 1u); };
+    // One pipeline iteration; STATS: tile t-1 exists.  FAST: tile t exists,
+    // tile t+3 is staged and tile t+4 is a proxy tile.
+    auto iter = [&](auto t4, auto stats, auto fast, int t) {
+        constexpr int T4 = decltype(t4)::value;
+        constexpr bool STATS = decltype(stats)::value != 0, FAST = decltype(fast)::value != 0;
+        constexpr int cur = T4 & 1, prev = cur ^ 1;
+        const u32x4* next = stage[(T4 + 1) % kRing];
+        const bool mfma_on = FAST || t < n_tiles;
+        float m = -INFINITY, nmk = 0.f, l0 = 0.f, l1 = 0.f;
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc) {
+#pragma unroll
+            for (int s = 0; s < kSub; ++s) {
+                const int slot = kSub * kc + s;
+                if (mfma_on) acc[cur][s] = mfma32(kf[s][kc], A[kc], kc == 0 ? zero16() : acc[cur][s]);
+                if (STATS) {
+                    if (slot < kMaxSlots) {
+#pragma unroll
+                        for (int q = 0; q < kMaxPer; ++q) {
+                            const int i0 = 2 * (slot * kMaxPer + q), i1 = i0 + 1;
+                            const float x0 = ok(i0) ? value(acc[prev], i0) : -INFINITY;
+                            const float x1 = ok(i1) ? value(acc[prev], i1) : -INFINITY;
+                            m = fmaxf(fmaxf(m, x0), x1);
+                        }
+                    } else if (slot == kMaxSlots) {
+                        m = pair_max(m);
+                        nmk = (FULL || m != -INFINITY) ? -m * kappa : 0.f;
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < kExpPer; ++q) {
+                            const int idx = (slot - kMaxSlots - 1) * kExpPer + q;
+                            if (idx < 32) {
+                                const float e = fast_exp2(fmaf(value(acc[prev], idx), kappa, nmk));
+                                const float ev = ok(idx) ? e : 0.f;
+                                if (q & 1) l1 += ev; else l0 += ev;
+                            }
+                        }
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if (mfma_on) A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
+            __builtin_amdgcn_sched_barrier(0);
         }
+        if (FAST) {
+            st.store(stage[(T4 + 3) % kRing]);
+            st.load_block(pbase + static_cast<int64_t>(32 * (t + 4)) * D, off);
+        } else if (t + 3 < n_tiles) {
+            st.store(stage[(T4 + 3) % kRing]);
+            if (t + 4 < n_tiles) load_tile(t + 4);
+        }
+        if (STATS) {
+            const int tp = t - 1;
+            const float l = pair_total(l0 + l1);
+            if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(-nmk, l);
+            if (T4 == 1 && tp >= kMergeTiles && (tp - kMergeTiles) % kMergeTiles == 0)
+                merge_chunk((tp - kMergeTiles) / kMergeTiles);
+        }
+        if ((T4 & 1) == 0) __syncthreads();
     };
-    auto stats_of = [&](const floatx16 (&ac)[kSub], int tile) {
-        const float2 r = column_lse<FULL>(ac, valid, kappa);
-        if (lane < 32) mrg[(tile / kMergeTiles) & 1][tile % kMergeTiles][wave][lane] = r;
-    };
-    // iteration 0
-    stage_next(0);
-    tile_mfma<D, true>(A, stage[1 % 3], kf, acc[0], lane, zero16());
-    __syncthreads();
-    // steady state; the merge of chunk k once its last tile's statistics are
-    // in LDS
-    auto body = [&](auto parity, int t) {
-        constexpr int cur = decltype(parity)::value, prev = cur ^ 1;
-        stage_next(t);
-        tile_mfma<D, true>(A, stage[(t + 1) % 3], kf, acc[cur], lane, zero16());
-        stats_of(acc[prev], t - 1);
-        if (t >= kMergeTiles + 1 && ((t - kMergeTiles - 1) % kMergeTiles) == 0)
-            merge_chunk((t - kMergeTiles - 1) / kMergeTiles);
-        __syncthreads();
-    };
+    using Off = Tag<0>;
+    using On = Tag<1>;
+    iter(Tag<0>{}, Off{}, Off{}, 0);
     int t = 1;
-    for (; t + 1 < n_tiles; t += 2) {
-        body(Parity<1>{}, t);
-        body(Parity<0>{}, t + 1);
+    __builtin_amdgcn_s_waitcnt(0);
+    for (; t + 3 + 4 < n_prox; t += 4) {
+        iter(Tag<1>{}, On{}, On{}, t);
+        iter(Tag<2>{}, On{}, On{}, t + 1);
+        iter(Tag<3>{}, On{}, On{}, t + 2);
+        iter(Tag<0>{}, On{}, On{}, t + 3);
     }
-    if (t < n_tiles) {
-        body(Parity<1>{}, t);
-        ++t;
+    for (; t <= n_tiles; t += 4) {
+        iter(Tag<1>{}, On{}, Off{}, t);
+        if (t + 1 <= n_tiles) iter(Tag<2>{}, On{}, Off{}, t + 1);
+        if (t + 2 <= n_tiles) iter(Tag<3>{}, On{}, Off{}, t + 2);
+        if (t + 3 <= n_tiles) iter(Tag<0>{}, On{}, Off{}, t + 3);
     }
-    // t == n_tiles: statistics of the last tile, then the unmerged chunks
-    if ((n_tiles - 1) & 1) stats_of(acc[1], n_tiles - 1); else stats_of(acc[0], n_tiles - 1);
     __syncthreads();
-    // the loop merged chunk k at t = 16k + 17 for every such t <= n_tiles - 1
-    const int merged = n_tiles >= kMergeTiles + 2 ? (n_tiles - kMergeTiles - 2) / kMergeTiles + 1 : 0;
+    // chunk k was merged in iteration 16k+17 when that iteration ran (t <= n_tiles)
+    const int merged = n_tiles >= kMergeTiles + 1 ? (n_tiles - kMergeTiles - 1) / kMergeTiles + 1 : 0;
     for (int k = merged; k * kMergeTiles < n_tiles; ++k) merge_chunk(k);
 }
 
 template <int D, int WAVES>
 __global__ void __launch_bounds__(64 * WAVES) score_lse_kernel(ScoreArgs a) {
-    __shared__ u32x4 stage[3][TileLds<D>::kSlots];
+    __shared__ u32x4 stage[kRing][TileLds<D>::kSlots];
     __shared__ float2 mrg[2][kMergeTiles][WAVES][32];
     int head, kb;
     block_work(a.n_kb, head, kb);
@@ -392,28 +428,8 @@ __global__ void __launch_bounds__(256) lse_combine_kernel(ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------- pass 2
-// p = 2^(kappa * acc) of one tile (acc already holds s - L/kappa), summed
-// over this lane's rows 0-15 (hA) and rows 16-31 (hB) of the tile.
-__device__ __forceinline__ void tile_probs(const floatx16 (&acc)[kSub], float kappa, float (&hA)[kSub],
-                                           float (&hB)[kSub]) {
-#pragma unroll
-    for (int s = 0; s < kSub; ++s) {
-        float sa = 0.f, sb = 0.f;
-#pragma unroll
-        for (int m4 = 0; m4 < 4; ++m4) {
-            const float e0 = fast_exp2(acc[s][4 * m4 + 0] * kappa);
-            const float e1 = fast_exp2(acc[s][4 * m4 + 1] * kappa);
-            const float e2 = fast_exp2(acc[s][4 * m4 + 2] * kappa);
-            const float e3 = fast_exp2(acc[s][4 * m4 + 3] * kappa);
-            if (m4 < 2) sa += (e0 + e1) + (e2 + e3); else sb += (e0 + e1) + (e2 + e3);
-        }
-        hA[s] = sa;
-        hB[s] = sb;
-    }
-}
-
 // Position of a pass-2 tile: proxy block u (rows 32u.. of each head) and
-// head h, visited u-major; advance() steps to the next tile.
+// head h, visited u-major, then the anchor tiles.
 struct TileCursor {
     int t, u, h;
     __device__ __forceinline__ void advance(int Gh) {
@@ -428,7 +444,7 @@ struct TileCursor {
 template <int D, int WAVES>
 __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     using St = Stager<D, WAVES>;
-    __shared__ u32x4 stage[3][TileLds<D>::kSlots];
+    __shared__ u32x4 stage[kRing][TileLds<D>::kSlots];
     extern __shared__ float4 dyn_lds[];
     float* Llds = reinterpret_cast<float*>(dyn_lds);     // [rows_pad]
 
@@ -443,95 +459,230 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     bf16x8 kf[kSub][D / 16];
     load_keys<D>(a, b, c, key0, kf);
 
-    const int g = a.P / a.G;                 // proxies per group, multiple of 16
-    const int n_prox_tiles = (a.P / 32) * a.Gh;
-    const int n_tiles = n_prox_tiles + (a.rows_pad - a.rows) / 32;
-    const uint16_t* pbase =
-        a.proxies + (static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh) * a.P * D;
+    const int g16 = a.P / a.G / 16;          // 16-row halves per proxy group
+    const int n_prox = (a.P / 32) * a.Gh;
+    const int n_anc = (a.rows_pad - a.rows) / 32;
+    const int64_t hq0 = static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh;
+    const uint16_t* pbase = a.proxies + hq0 * a.P * D;
     int off[St::kPer];
 #pragma unroll
     for (int k = 0; k < St::kPer; ++k) off[k] = St::src_off(k);
 
-    // this head's row offsets -L/kappa, all rows, stay in LDS for the whole kernel
-    const float inv_kappa = 1.0f / kappa;
-    for (int i = static_cast<int>(threadIdx.x); i < a.rows_pad; i += 64 * WAVES) Llds[i] = -L[i] * inv_kappa;
-
-    // tiles t < n_prox_tiles: proxies 32u.. of head h; later: anchor rows
+    // proxy tile (u, h): rows 32u.. of head h, first row h*P + 32u
+    auto tile_row = [&](const TileCursor& q) { return q.h * a.P + 32 * q.u; };
     auto load_tile = [&](St& st, const TileCursor& q) {
-        if (q.t < n_prox_tiles)
-            st.load_block(pbase + static_cast<int64_t>(q.h * a.P + 32 * q.u) * D, off);
-        else
-            st.load_rows(a, b, c, a.rows + 32 * (q.t - n_prox_tiles));
+        st.load_block(pbase + static_cast<int64_t>(tile_row(q)) * D, off);
     };
 
-    // Pipeline (LDS slots t % 3): in iteration t the rows of tile t+2 go
-    // registers -> LDS, tile t+3 is fetched into registers, the MFMAs of tile
-    // t run from A while A is refilled with tile t+1, and the probabilities
-    // of tile t-1 are formed.
-    St st;
-    bf16x8 A[D / 16];
-    TileCursor q3{0, 0, 0};                  // next tile to fetch
-    load_tile(st, q3);
-    st.store(stage[0]);
-    q3.advance(a.Gh);
-    if (n_tiles > 1) {
-        load_tile(st, q3);
-        st.store(stage[1]);
-    }
-    q3.advance(a.Gh);
-    if (n_tiles > 2) load_tile(st, q3);
-    q3.advance(a.Gh);
+    // Pipeline over the proxy tiles t (LDS slot t % 4).  Iteration t issues
+    // the MFMAs of tile t (fragments in A, accumulator start in Cn) while
+    // refilling A with tile t+1, forms the probabilities of tile t-1 from the
+    // other accumulator set, writes tile t+3 from registers to LDS, fetches
+    // tile t+5 into registers and reads the accumulator start of tile t+1.
+    // A slot is written two iterations before it is read and rewritten two
+    // iterations after its last read, so one barrier after every even
+    // iteration orders all LDS traffic.
+    // Prologue: every load (keys above, the row offsets, tiles 0-4) is in
+    // flight before the first store waits on any of them.  Tiles 0-2 go to
+    // LDS slots 0-2; tiles 3 and 4 wait in the two staging register sets
+    // (tile k in set k % 2), so each tile is fetched two iterations before
+    // it is stored.
+    St pre[3], st[2];
+    TileCursor ld{0, 0, 0};                  // next tile to fetch
+    constexpr int kLBatch = 8;               // row offsets fetched per thread at once
+    const float inv_kappa = 1.0f / kappa;
+    auto l_batch = [&](int i0, auto&& between) {
+        float lv[kLBatch];
+#pragma unroll
+        for (int j = 0; j < kLBatch; ++j) {
+            const int i = i0 + j * 64 * WAVES;
+            lv[j] = i < a.rows_pad ? L[i] : 0.f;
+        }
+        between();
+#pragma unroll
+        for (int j = 0; j < kLBatch; ++j) {
+            const int i = i0 + j * 64 * WAVES;
+            if (i < a.rows_pad) Llds[i] = -lv[j] * inv_kappa;
+        }
+    };
+    l_batch(static_cast<int>(threadIdx.x), [&]() {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            if (ld.t < n_prox) load_tile(pre[k], ld);
+            ld.advance(a.Gh);
+        }
+#pragma unroll
+        for (int k = 3; k < 5; ++k) {
+            if (ld.t < n_prox) load_tile(st[k & 1], ld);
+            ld.advance(a.Gh);
+        }
+    });
+    for (int i0 = static_cast<int>(threadIdx.x) + kLBatch * 64 * WAVES; i0 < a.rows_pad; i0 += kLBatch * 64 * WAVES)
+        l_batch(i0, []() {});
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        if (k < n_prox) pre[k].store(stage[k]);
     __syncthreads();
+    bf16x8 A[D / 16];
     read_frags<D>(stage[0], A, lane);
+    TileCursor mm{0, 0, 0};                  // tile whose accumulator start is read next
+    floatx16 Cn = row_offsets(Llds + tile_row(mm), lane);
+    mm.advance(a.Gh);
 
     const int64_t gm_base = static_cast<int64_t>(head) * a.G * a.T;
-    const int my_key = key0 + lane;          // lanes < 32: sub-tile 0, lanes >= 32: sub-tile 1
+    const int my_key = key0 + lane;
     const bool my_ok = my_key < a.T;
-    float runA[kSub] = {0.f, 0.f}, runB[kSub] = {0.f, 0.f}, open[kSub] = {0.f, 0.f};
-    float macc[kSub] = {0.f, 0.f}, aacc[kSub] = {0.f, 0.f};
-    // completes group `gi` for this wave's 64 key columns: sum the two
-    // half-waves, add to the total mass, store, reset
-    auto flush_group = [&](float (&o)[kSub], int gi) {
+    float runA[kSub][2] = {}, runB[kSub][2] = {}, open[kSub] = {0.f, 0.f};
+    float macc = 0.f;
+    int g_half = 0, g_idx = 0;               // halves in the open group, its index
+    auto close_half = [&](float (&run)[kSub][2]) {
 #pragma unroll
         for (int s = 0; s < kSub; ++s) {
-            o[s] += shfl_xor_f(o[s], 32);
-            macc[s] += o[s];
+            open[s] += run[s][0] + run[s][1];
+            run[s][0] = run[s][1] = 0.f;
         }
-        if (a.group_mass != nullptr && my_ok)
-            a.group_mass[gm_base + static_cast<int64_t>(gi) * a.T + my_key] = (lane < 32) ? o[0] : o[1];
+        if (++g_half == g16) {
+            const float tot = pair_sum(open[0], open[1]);
+            macc += tot;
+            if (a.group_mass != nullptr && my_ok) a.group_mass[gm_base + static_cast<int64_t>(g_idx) * a.T + my_key] = tot;
 #pragma unroll
-        for (int s = 0; s < kSub; ++s) o[s] = 0.f;
+            for (int s = 0; s < kSub; ++s) open[s] = 0.f;
+            g_half = 0;
+            ++g_idx;
+        }
     };
-    // rows 0-15 of tile (u, h) belong to proxy group (32u)/g, rows 16-31 to
-    // (32u+16)/g; runA / runB sum each half over the Gh heads and `open`
-    // carries a group that spans several tiles
-    TileCursor q1{0, 0, 0};                  // tile whose probabilities come next
-    auto group_step = [&](const float (&hA)[kSub], const float (&hB)[kSub]) {
-#pragma unroll
-        for (int s = 0; s < kSub; ++s) {
-            runA[s] += hA[s];
-            runB[s] += hB[s];
+    // rows 0-15 of proxy tile (u, h) are half 2u of head h, rows 16-31 half
+    // 2u+1; runA / runB sum each half over the Gh heads, and after the last
+    // head both halves are closed
+    int gs_h = 0;                            // head of the tile whose probabilities come next
+    auto group_step = [&]() {
+        if (++gs_h == a.Gh) {
+            gs_h = 0;
+            close_half(runA);
+            close_half(runB);
         }
-        if (q1.h == a.Gh - 1) {
-            const int u = q1.u;
+    };
+
+    floatx16 acc[2][kSub];
+    // One pipeline iteration; PROBS: tile t-1 exists (t > 0).  FAST: tile t
+    // exists, tile t+3 is staged and tile t+5 fetched, so nothing branches.
+    // The issue order is fixed by hand: after MFMA slot j of tile t come the
+    // sums of value group j-2, the exps of group j-1 and the kappa products of
+    // group j of tile t-1 (kPer32 of its 32 accumulator values per group), so
+    // no VALU step waits on the one before it and the matrix pipe and the
+    // VALU work side by side; the fragment refill follows the second MFMA of
+    // each k-chunk, the accumulator start of tile t+1 is read halfway and the
+    // staging sits at the end.
+    constexpr int kMfmas = kSub * (D / 16);
+    constexpr int kPer32 = 32 / kMfmas;
+    auto iter = [&](auto t4, auto probs, auto fast, int t) {
+        constexpr int T4 = decltype(t4)::value;
+        constexpr bool PROBS = decltype(probs)::value != 0, FAST = decltype(fast)::value != 0;
+        constexpr int cur = T4 & 1, prev = cur ^ 1;
+        const u32x4* next = stage[(T4 + 1) % kRing];
+        const bool mfma_on = FAST || t < n_prox;
+        floatx16 Cnext;
+        float mv[kPer32], ev[kPer32];
+        auto add_group = [&](int g) {
+#pragma unroll
+            for (int v = 0; v < kPer32; ++v) {
+                const int idx = g * kPer32 + v, s2 = idx / 16, i = idx % 16;
+                if (i < 8) runA[s2][v & 1] += ev[v]; else runB[s2][v & 1] += ev[v];
+            }
+        };
+        auto exp_group = [&]() {
+#pragma unroll
+            for (int v = 0; v < kPer32; ++v) ev[v] = fast_exp2(mv[v]);
+        };
+        auto mul_group = [&](int g) {
+#pragma unroll
+            for (int v = 0; v < kPer32; ++v) {
+                const int idx = g * kPer32 + v;
+                mv[v] = acc[prev][idx / 16][idx % 16] * kappa;
+            }
+        };
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc) {
 #pragma unroll
             for (int s = 0; s < kSub; ++s) {
-                open[s] += runA[s];
-                runA[s] = 0.f;
+                const int slot = kSub * kc + s;
+                if (mfma_on) acc[cur][s] = mfma32(A[kc], kf[s][kc], kc == 0 ? Cn : acc[cur][s]);
+                if (PROBS) {
+                    if (slot >= 2) add_group(slot - 2);
+                    if (slot >= 1) exp_group();
+                    mul_group(slot);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
-            if (((32 * u + 16) % g) == 0) flush_group(open, (32 * u) / g);
-#pragma unroll
-            for (int s = 0; s < kSub; ++s) {
-                open[s] += runB[s];
-                runB[s] = 0.f;
+            if (mfma_on) A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
+            if (kc == D / 32) {
+                // accumulator start of tile t+1 (a valid row block even past the end)
+                Cnext = row_offsets(Llds + ((FAST || mm.t < n_prox) ? tile_row(mm) : 0), lane);
+                mm.advance(a.Gh);
             }
-            if (((32 * u + 32) % g) == 0) flush_group(open, (32 * u + 16) / g);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        q1.advance(a.Gh);
+        if (PROBS) {
+            add_group(kMfmas - 2);
+            exp_group();
+            add_group(kMfmas - 1);
+#pragma unroll
+            for (int s = 0; s < kSub; ++s)
+#pragma unroll
+                for (int q = 0; q < 2; ++q) asm volatile("" : "+v"(runA[s][q]), "+v"(runB[s][q]));
+        }
+        // tile t+3 (set (t+3) % 2) to LDS, then tile t+5 into the same set
+        constexpr int set = (T4 + 1) & 1;
+        if (FAST) {
+            st[set].store(stage[(T4 + 3) % kRing]);
+            load_tile(st[set], ld);
+        } else if (t + 3 < n_prox) {
+            st[set].store(stage[(T4 + 3) % kRing]);
+            if (ld.t < n_prox) load_tile(st[set], ld);
+        }
+        ld.advance(a.Gh);
+        Cn = Cnext;
+        if (PROBS) group_step();
+        if ((T4 & 1) == 0) __syncthreads();
     };
-    auto anchor_step = [&](int tp, const floatx16 (&ac)[kSub]) {
-        // anchor rows of tile tp: query head 32*(tp - n_prox_tiles) + row
-        const int h0 = 32 * (tp - n_prox_tiles) + 4 * (lane >> 5);
+    using Off = Tag<0>;
+    using On = Tag<1>;
+    iter(Tag<0>{}, Off{}, Off{}, 0);
+    int t = 1;
+    // drain the key and staging loads of the prologue here, once, so that no
+    // wait for them lands inside the loop
+    __builtin_amdgcn_s_waitcnt(0);
+    // steady state: t + 5 < n_prox
+    for (; t + 3 + 5 < n_prox; t += 4) {
+        iter(Tag<1>{}, On{}, On{}, t);
+        iter(Tag<2>{}, On{}, On{}, t + 1);
+        iter(Tag<3>{}, On{}, On{}, t + 2);
+        iter(Tag<0>{}, On{}, On{}, t + 3);
+    }
+    // the rest, up to the probabilities of the last proxy tile (t = 1 mod 4 here)
+    for (; t <= n_prox; t += 4) {
+        iter(Tag<1>{}, On{}, Off{}, t);
+        if (t + 1 <= n_prox) iter(Tag<2>{}, On{}, Off{}, t + 1);
+        if (t + 2 <= n_prox) iter(Tag<3>{}, On{}, Off{}, t + 2);
+        if (t + 3 <= n_prox) iter(Tag<0>{}, On{}, Off{}, t + 3);
+    }
+
+    // anchor tiles (the last window query of each of the Gh heads), outside
+    // the pipeline: query head 32*ta + row of anchor tile ta
+    float aacc[kSub] = {0.f, 0.f};
+    for (int ta = 0; ta < n_anc; ++ta) {
+        __syncthreads();
+        st[0].load_rows(a, b, c, a.rows + 32 * ta);
+        st[0].store(stage[0]);
+        __syncthreads();
+        read_frags<D>(stage[0], A, lane);
+        floatx16 ac[kSub];
+        const floatx16 c0 = row_offsets(Llds + a.rows + 32 * ta, lane);
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc)
+#pragma unroll
+            for (int s = 0; s < kSub; ++s) ac[s] = mfma32(A[kc], kf[s][kc], kc == 0 ? c0 : ac[s]);
+        const int h0 = 32 * ta + 4 * (lane >> 5);
 #pragma unroll
         for (int m4 = 0; m4 < 4; ++m4)
 #pragma unroll
@@ -541,66 +692,12 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
                     const float e = fast_exp2(ac[s][4 * m4 + j] * kappa);
                     aacc[s] += (h0 + 8 * m4 + j < a.Gh) ? e : 0.f;
                 }
-    };
-
-    floatx16 acc[2][kSub];
-    auto stage_next = [&](int t) {
-        if (t + 2 < n_tiles) {
-            st.store(stage[(t + 2) % 3]);
-            if (t + 3 < n_tiles) load_tile(st, q3);
-        }
-        q3.advance(a.Gh);
-    };
-    TileCursor q0{0, 0, 0};                  // tile whose MFMAs come next
-    auto tile_row = [&](const TileCursor& q) {
-        return q.t < n_prox_tiles ? q.h * a.P + 32 * q.u : a.rows + 32 * (q.t - n_prox_tiles);
-    };
-    stage_next(0);
-    tile_mfma<D, false>(A, stage[1 % 3], kf, acc[0], lane, row_offsets(Llds + tile_row(q0), lane));
-    q0.advance(a.Gh);
-    __syncthreads();
-    // steady state over proxy tiles: MFMA of tile t next to the
-    // probabilities of tile t-1 (the last of these MFMAs may be an anchor tile)
-    auto body = [&](auto parity, int t) {
-        constexpr int cur = decltype(parity)::value, prev = cur ^ 1;
-        stage_next(t);
-        tile_mfma<D, false>(A, stage[(t + 1) % 3], kf, acc[cur], lane, row_offsets(Llds + tile_row(q0), lane));
-        q0.advance(a.Gh);
-        float hA[kSub], hB[kSub];
-        tile_probs(acc[prev], kappa, hA, hB);
-        group_step(hA, hB);
-        __syncthreads();
-    };
-    int t = 1;
-    for (; t + 1 <= n_prox_tiles; t += 2) {
-        body(Parity<1>{}, t);
-        body(Parity<0>{}, t + 1);
     }
-    if (t <= n_prox_tiles) {
-        body(Parity<1>{}, t);
-        ++t;
-    }
-    // anchor tiles (t - 1 >= n_prox_tiles)
-    auto anchor_body = [&](auto parity, int t) {
-        constexpr int cur = decltype(parity)::value, prev = cur ^ 1;
-        if (t < n_tiles) {
-            stage_next(t);
-            tile_mfma<D, false>(A, stage[(t + 1) % 3], kf, acc[cur], lane, row_offsets(Llds + tile_row(q0), lane));
-            q0.advance(a.Gh);
-        }
-        anchor_step(t - 1, acc[prev]);
-        __syncthreads();
-    };
-    for (; t <= n_tiles; ++t) {
-        if (t & 1) anchor_body(Parity<1>{}, t); else anchor_body(Parity<0>{}, t);
-    }
-    const float inv_gh = 1.0f / static_cast<float>(a.Gh);
-#pragma unroll
-    for (int s = 0; s < kSub; ++s) aacc[s] = (aacc[s] + shfl_xor_f(aacc[s], 32)) * inv_gh;
+    const float anc = pair_sum(aacc[0], aacc[1]) * (1.0f / static_cast<float>(a.Gh));
     if (my_ok) {
         const int64_t o = static_cast<int64_t>(head) * a.T + my_key;
-        a.mass[o] = (lane < 32) ? macc[0] : macc[1];
-        a.anchor[o] = (lane < 32) ? aacc[0] : aacc[1];
+        a.mass[o] = macc;
+        a.anchor[o] = anc;
     }
 }
 
