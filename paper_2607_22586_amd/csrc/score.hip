@@ -408,20 +408,31 @@ __global__ void __launch_bounds__(64 * WAVES) score_lse_kernel(ScoreArgs a) {
         lse_body<D, WAVES, false>(a, head, kb, b, c, stage, mrg);
 }
 
-// L_row = M + log2(sum_kb S_kb * 2^(M_kb - M)), one thread per row.
+// L_row = M + log2(sum_kb S_kb * 2^(M_kb - M)), one thread per row; the
+// partials are fetched kCombineBatch at a time so their latencies overlap.
+constexpr int kCombineBatch = 16;
 __global__ void __launch_bounds__(256) lse_combine_kernel(ScoreArgs a) {
     const int r = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x);
     const int head = static_cast<int>(blockIdx.y);
     if (r >= a.rows_pad) return;
     const float2* p = a.part + static_cast<int64_t>(head) * a.n_kb * a.rows_pad + r;
     float M = -INFINITY, S = 0.f;
-    for (int kb = 0; kb < a.n_kb; ++kb) {
-        const float2 v = p[static_cast<int64_t>(kb) * a.rows_pad];
-        if (v.x > M) {
-            S = S * exp2f(M - v.x) + v.y;
-            M = v.x;
-        } else if (v.x != -INFINITY) {
-            S += v.y * exp2f(v.x - M);
+    for (int kb0 = 0; kb0 < a.n_kb; kb0 += kCombineBatch) {
+        float2 v[kCombineBatch];
+#pragma unroll
+        for (int j = 0; j < kCombineBatch; ++j)
+            v[j] = kb0 + j < a.n_kb ? p[static_cast<int64_t>(kb0 + j) * a.rows_pad] : make_float2(-INFINITY, 0.f);
+        float bm = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < kCombineBatch; ++j) bm = fmaxf(bm, v[j].x);
+        if (bm > M) {
+            S = (M == -INFINITY) ? 0.f : S * exp2f(M - bm);
+            M = bm;
+        }
+        if (M != -INFINITY) {
+#pragma unroll
+            for (int j = 0; j < kCombineBatch; ++j)
+                if (v[j].x != -INFINITY) S += v[j].y * exp2f(v[j].x - M);
         }
     }
     a.lse[static_cast<int64_t>(head) * a.rows_pad + r] = M + log2f(S);

@@ -338,12 +338,205 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
     if (tid == 0) a.counts[hc] = static_cast<int32_t>(written);
 }
 
+// ------------------------------------------- register-resident variants
+// For T <= 1024 * KPT the whole row of one workgroup fits in registers:
+// thread j holds elements [KPT*j, KPT*j + KPT) (index order), so the data
+// is read from memory once and every index-ordered step (ties, compaction)
+// needs one block scan instead of a sweep.
+
+// tau cut of one (b, c, group); same result as tau_cut_kernel.
+template <int KPT>
+__global__ void __launch_bounds__(kSelThreads) tau_cut_reg_kernel(SelectArgs a) {
+    __shared__ uint32_t cnt[2048];
+    __shared__ unsigned long long sum[2048];
+    __shared__ unsigned long long wtot64[kSelWaves];
+    __shared__ uint32_t wtot[kSelWaves];
+    __shared__ uint32_t s_digit, s_cnt;
+    __shared__ unsigned long long s_rem;
+    __shared__ int32_t s_tcut;
+
+    const int g = blockIdx.x, c = blockIdx.y, b = blockIdx.z;
+    const int64_t hcg = (static_cast<int64_t>(b) * a.Hkv + c) * a.G + g;
+    const float* m = a.group_mass + hcg * a.T;
+    const int tid = threadIdx.x;
+    const int t0 = tid * KPT;
+
+    float mv[KPT];
+    uint64_t local = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+        mv[j] = (t0 + j < a.T) ? m[t0 + j] : 0.f;
+        local += to_fixed(mv[j], a.fix_scale);
+    }
+    const uint64_t total = block_sum_u64(local, wtot64);
+    if (total == 0) {
+        if (tid == 0) { a.theta[hcg] = 0xFFFFFFFFu; a.tcut[hcg] = -1; }
+        return;
+    }
+    unsigned long long need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(total)));
+    if (need < 1) need = 1;
+    if (need > total) need = total;
+
+    const int shifts[3] = {21, 10, 0};
+    const uint32_t masks[3] = {0u, 0xFFE00000u, 0xFFFFFC00u};
+    uint32_t prefix = 0;
+    for (int pass = 0; pass < 3; ++pass) {
+        const int shift = shifts[pass];
+        const uint32_t mask = masks[pass];
+        for (int i = tid; i < 2048; i += kSelThreads) { cnt[i] = 0; sum[i] = 0; }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) {
+            const uint32_t bits = __float_as_uint(mv[j]);
+            if (t0 + j < a.T && (bits & mask) == prefix) {
+                const uint32_t dg = (bits >> shift) & 2047u;
+                atomicAdd(&cnt[dg], 1u);
+                atomicAdd(&sum[dg], static_cast<unsigned long long>(to_fixed(mv[j], a.fix_scale)));
+            }
+        }
+        __syncthreads();
+        descending_crossing<unsigned long long>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
+        prefix |= s_digit << shift;
+        need = s_rem;
+    }
+    const uint64_t f_theta = to_fixed(__uint_as_float(prefix), a.fix_scale);
+    const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
+    if (k_eq >= s_cnt) {
+        if (tid == 0) { a.theta[hcg] = prefix; a.tcut[hcg] = a.T; }
+        return;
+    }
+    // the k_eq-th key (by index) whose mass equals theta
+    uint32_t n_eq = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) n_eq += (t0 + j < a.T && __float_as_uint(mv[j]) == prefix) ? 1u : 0u;
+    uint32_t eq_total;
+    const uint32_t eq_before = block_excl_scan<uint32_t>(n_eq, wtot, eq_total);
+    if (eq_before < k_eq && k_eq <= eq_before + n_eq) {
+        uint32_t seen = eq_before;
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) {
+            if (t0 + j < a.T && __float_as_uint(mv[j]) == prefix) {
+                if (++seen == k_eq) s_tcut = t0 + j;
+            }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        a.theta[hcg] = prefix;
+        a.tcut[hcg] = s_tcut;
+    }
+}
+
+// Budgeted selection of one (b, c); same result as topk_kernel.
+template <int KPT>
+__global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
+    __shared__ uint32_t cnt[2048];
+    __shared__ uint32_t wtot[kSelWaves];
+    __shared__ uint32_t s_digit, s_cnt, s_rem;
+
+    const int c = blockIdx.x, b = blockIdx.y;
+    const int64_t hc = static_cast<int64_t>(b) * a.Hkv + c;
+    const int tid = threadIdx.x;
+    int32_t* out = a.idx + hc * a.c_max;
+    int budget = a.budget;
+    if (a.budgets != nullptr) budget = min(max(a.budgets[hc], 1), a.c_max);
+
+    if (a.T <= budget) {
+        for (int j = tid; j < a.c_max; j += kSelThreads) out[j] = (j < a.T) ? j : -1;
+        if (tid == 0) a.counts[hc] = a.T;
+        return;
+    }
+    const int pool = a.keep_last ? a.T - 1 : a.T;
+    const uint32_t want = static_cast<uint32_t>(a.keep_last ? budget - 1 : budget);
+    const uint64_t* key = a.keys + hc * a.T;
+    const int t0 = tid * KPT;
+    uint64_t kv[KPT];
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) kv[j] = (t0 + j < pool) ? key[t0 + j] : 0ull;
+
+    uint64_t theta = 0;
+    uint32_t k_eq = 0;
+    if (want > 0) {
+        const int shifts[6] = {53, 42, 31, 20, 9, 0};
+        uint64_t prefix = 0, mask = 0;
+        uint32_t need = want;
+        bool settled = false;
+        for (int pass = 0; pass < 6 && !settled; ++pass) {
+            const int shift = shifts[pass];
+            for (int i = tid; i < 2048; i += kSelThreads) cnt[i] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < KPT; ++j) {
+                const bool cand = t0 + j < pool && (kv[j] & mask) == prefix;
+                hist_add(cand, static_cast<uint32_t>(kv[j] >> shift) & 2047u, 0ull, cnt, nullptr);
+            }
+            __syncthreads();
+            descending_crossing<uint32_t>(cnt, cnt, need, wtot, &s_digit, &s_rem, &s_cnt);
+            prefix |= static_cast<uint64_t>(s_digit) << shift;
+            mask |= (shift == 0 ? 0x1FFull : 0x7FFull) << shift;
+            need = s_rem;
+            if (s_cnt == need) {
+                theta = prefix - 1;
+                k_eq = 0;
+                settled = true;
+            }
+        }
+        if (!settled) {
+            theta = prefix;
+            k_eq = need;
+        }
+    }
+    // index-ordered compaction: keys > theta, then the first k_eq equal keys
+    uint32_t n_eq = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) n_eq += (want > 0 && k_eq > 0 && t0 + j < pool && kv[j] == theta) ? 1u : 0u;
+    uint32_t eq_total;
+    uint32_t eq_seen = block_excl_scan<uint32_t>(n_eq, wtot, eq_total);
+    uint32_t sel_mask = 0, n_sel = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+        const bool in = want > 0 && t0 + j < pool;
+        const bool gt = in && kv[j] > theta;
+        bool eq = in && k_eq > 0 && kv[j] == theta;
+        if (eq) eq = eq_seen++ < k_eq;
+        if (gt || eq) {
+            sel_mask |= 1u << j;
+            ++n_sel;
+        }
+    }
+    uint32_t sel_total;
+    uint32_t pos = block_excl_scan<uint32_t>(n_sel, wtot, sel_total);
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+        if ((sel_mask >> j) & 1u) {
+            if (pos < want) out[pos] = t0 + j;
+            ++pos;
+        }
+    }
+    uint32_t written = min(sel_total, want);
+    if (a.keep_last) {
+        if (tid == 0) out[written] = a.T - 1;
+        written += 1;
+    }
+    for (int j = static_cast<int>(written) + tid; j < a.c_max; j += kSelThreads) out[j] = -1;
+    if (tid == 0) a.counts[hc] = static_cast<int32_t>(written);
+}
+
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+    // register-resident kernels while a row fits in 16 (tau cut) or 32
+    // (top-k) elements per thread
+    const int per = (a.T + kSelThreads - 1) / kSelThreads;
+    const int kpt = per <= 4 ? 4 : per <= 8 ? 8 : per <= 16 ? 16 : per <= 32 ? 32 : 0;
     if (a.mode == 0) {
         dim3 g1(a.G, a.Hkv, a.B);
-        hipLaunchKernelGGL(tau_cut_kernel, g1, dim3(kSelThreads), 0, s, a);
+        switch (kpt) {
+            case 4: hipLaunchKernelGGL(tau_cut_reg_kernel<4>, g1, dim3(kSelThreads), 0, s, a); break;
+            case 8: hipLaunchKernelGGL(tau_cut_reg_kernel<8>, g1, dim3(kSelThreads), 0, s, a); break;
+            case 16: hipLaunchKernelGGL(tau_cut_reg_kernel<16>, g1, dim3(kSelThreads), 0, s, a); break;
+            default: hipLaunchKernelGGL(tau_cut_kernel, g1, dim3(kSelThreads), 0, s, a); break;
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -352,7 +545,13 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g3(a.Hkv, a.B);
-    hipLaunchKernelGGL(topk_kernel, g3, dim3(kSelThreads), 0, s, a);
+    switch (kpt) {
+        case 4: hipLaunchKernelGGL(topk_reg_kernel<4>, g3, dim3(kSelThreads), 0, s, a); break;
+        case 8: hipLaunchKernelGGL(topk_reg_kernel<8>, g3, dim3(kSelThreads), 0, s, a); break;
+        case 16: hipLaunchKernelGGL(topk_reg_kernel<16>, g3, dim3(kSelThreads), 0, s, a); break;
+        case 32: hipLaunchKernelGGL(topk_reg_kernel<32>, g3, dim3(kSelThreads), 0, s, a); break;
+        default: hipLaunchKernelGGL(topk_kernel, g3, dim3(kSelThreads), 0, s, a); break;
+    }
     return hipGetLastError();
 }
 
