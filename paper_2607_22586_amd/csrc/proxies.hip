@@ -14,8 +14,9 @@ namespace mmskv {
 namespace {
 
 constexpr int kProxyThreads = 256;
-constexpr int kProxiesPerBlock = 64;
+constexpr int kBlockDims = 16;      // dimensions (of every proxy of a head) per workgroup
 constexpr int kWinChunk = 64;       // window rows staged in LDS at a time
+constexpr int kStatBatch = 16;      // staged rows read per LDS round trip
 
 // Philox4x32-10 (Salmon et al., SC 2011): ten rounds of
 // (c0,c1,c2,c3) <- (hi(M1 c2)^c1^k0, lo(M1 c2), hi(M0 c0)^c3^k1, lo(M0 c0))
@@ -24,8 +25,10 @@ __device__ __forceinline__ void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32
                                               uint32_t& c3, uint32_t k0, uint32_t k1) {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
-        const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+        const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * c0;   // one 32x32->64 multiply each
+        const uint64_t p1 = static_cast<uint64_t>(0xCD9E8D57u) * c2;
+        const uint32_t lo0 = static_cast<uint32_t>(p0), hi0 = static_cast<uint32_t>(p0 >> 32);
+        const uint32_t lo1 = static_cast<uint32_t>(p1), hi1 = static_cast<uint32_t>(p1 >> 32);
         const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
         c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
         k0 += 0x9E3779B9u;
@@ -134,29 +137,48 @@ __device__ __forceinline__ uint16_t to_bf16(double x) {
 __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs a) {
     extern __shared__ double smem[];
     const int d = a.d, half = d / 2;
-    double* mu = smem;            // [d]
+    double* mu = smem;            // [d]  (this block's dims only)
     double* gs = smem + d;        // [d]  gamma * sigma
-    double* last = smem + 2 * d;  // [d]  window query W-1
-    float* win = reinterpret_cast<float*>(smem + 3 * d);   // [kWinChunk][d] staged window rows
+    float* win = reinterpret_cast<float*>(smem + 2 * d);   // [kWinChunk][kBlockDims] staged window values
     const int h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     const int64_t qbase = static_cast<int64_t>(b) * a.qsb + static_cast<int64_t>(h) * a.qsh;
 
-    // stage window rows [w0, w0 + n) in LDS (values are exact in fp32)
+    // Workgroup x owns quads [x*qpb, (x+1)*qpb) of every proxy of the head
+    // (with rotary placement also their partner quads d/8 further on), so it
+    // needs the statistics of kBlockDims = 16 dimensions only.
+    const bool rope = a.cos_f != nullptr;
+    const int qpb = rope ? kBlockDims / 8 : kBlockDims / 4;
+    const int q0 = blockIdx.x * qpb;
+    auto dim_of = [&](int slot) {
+        return rope ? (slot < kBlockDims / 2 ? 4 * q0 + slot : half + 4 * q0 + slot - kBlockDims / 2) : 4 * q0 + slot;
+    };
+    // stage window rows [w0, w0 + n) of the block's dims in LDS (exact in fp32)
     auto stage = [&](int w0, int n) {
-        for (int e = tid; e < n * d; e += kProxyThreads) {
-            const int w = e / d, j = e - w * d;
-            win[e] = static_cast<float>(load_q(a, qbase + static_cast<int64_t>(w0 + w) * a.qst + j));
+        for (int e = tid; e < n * kBlockDims; e += kProxyThreads) {
+            const int w = e / kBlockDims, slot = e % kBlockDims;
+            win[e] = static_cast<float>(load_q(a, qbase + static_cast<int64_t>(w0 + w) * a.qst + dim_of(slot)));
         }
     };
-    // mean, then (population or sample) variance, summed in window order
+    // mean, then (population or sample) variance, summed in window order;
+    // thread `slot` < kBlockDims owns one dimension
+    const bool owner = tid < kBlockDims;
     double acc = 0.0;
     for (int w0 = 0; w0 < a.W; w0 += kWinChunk) {
         const int n = min(kWinChunk, a.W - w0);
         __syncthreads();
         stage(w0, n);
         __syncthreads();
-        if (tid < d)
-            for (int w = 0; w < n; ++w) acc = acc + static_cast<double>(win[w * d + tid]);
+        if (owner) {
+            // LDS reads kStatBatch rows at a time, so one read latency covers a batch
+            for (int w0b = 0; w0b < n; w0b += kStatBatch) {
+                float v[kStatBatch];
+#pragma unroll
+                for (int k = 0; k < kStatBatch; ++k) v[k] = w0b + k < n ? win[(w0b + k) * kBlockDims + tid] : 0.f;
+#pragma unroll
+                for (int k = 0; k < kStatBatch; ++k)
+                    if (w0b + k < n) acc = acc + static_cast<double>(v[k]);
+            }
+        }
     }
     const double m = acc / static_cast<double>(a.W);
     double sq = 0.0;
@@ -168,34 +190,39 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
             stage(w0, n);
             __syncthreads();
         }
-        if (tid < d)
-            for (int w = 0; w < n; ++w) {
-                const double diff = static_cast<double>(win[w * d + tid]) - m;
-                const double dd = diff * diff;
-                sq = sq + dd;
+        if (owner) {
+            for (int w0b = 0; w0b < n; w0b += kStatBatch) {
+                float v[kStatBatch];
+#pragma unroll
+                for (int k = 0; k < kStatBatch; ++k) v[k] = w0b + k < n ? win[(w0b + k) * kBlockDims + tid] : 0.f;
+#pragma unroll
+                for (int k = 0; k < kStatBatch; ++k) {
+                    if (w0b + k < n) {
+                        const double diff = static_cast<double>(v[k]) - m;
+                        const double dd = diff * diff;
+                        sq = sq + dd;
+                    }
+                }
             }
+        }
     }
-    if (tid < d) {
+    if (owner) {
+        const int j = dim_of(tid);
         const double sg = sqrt(sq / static_cast<double>(a.W - a.ddof));
-        mu[tid] = m;
-        gs[tid] = a.gamma * sg;
-        last[tid] = load_q(a, qbase + static_cast<int64_t>(a.W - 1) * a.qst + tid);
-        if (a.stats != nullptr && blockIdx.x == 0) {
+        mu[j] = m;
+        gs[j] = a.gamma * sg;
+        if (a.stats != nullptr) {
             double* st = a.stats + (static_cast<int64_t>(b) * a.Hq + h) * 2 * d;
-            st[tid] = m;
-            st[d + tid] = sg;
+            st[j] = m;
+            st[d + j] = sg;
         }
     }
     __syncthreads();
 
-    const bool rope = a.cos_f != nullptr;
-    const int i0 = blockIdx.x * kProxiesPerBlock;
-    const int n_prox = min(kProxiesPerBlock, a.P - i0);
-    const int quads = rope ? d / 8 : d / 4;
     uint16_t* out_head = a.proxies + (static_cast<int64_t>(b) * a.Hq + h) * a.P * d;
-    for (int item = tid; item < n_prox * quads; item += kProxyThreads) {
-        const int i = i0 + item / quads;
-        const int jq = item % quads;
+    for (int item = tid; item < a.P * qpb; item += kProxyThreads) {
+        const int i = item / qpb;
+        const int jq = q0 + item % qpb;
         uint16_t* row = out_head + static_cast<int64_t>(i) * d;
         double z[4];
         normal_quad(a.key0, a.key1, b, a.layer, h, i, jq, z);
@@ -242,20 +269,22 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
         }
     }
 
+    // anchor query: window row W-1, all dims, by workgroup 0
     if (blockIdx.x == 0) {
         uint16_t* ql = a.q_last + (static_cast<int64_t>(b) * a.Hq + h) * d;
+        const int64_t lrow = qbase + static_cast<int64_t>(a.W - 1) * a.qst;
         const bool rope_l = a.cos_l != nullptr;
         for (int j = tid; j < d; j += kProxyThreads) {
-            double v = last[j];
+            double v = load_q(a, lrow + j);
             if (rope_l) {
                 if (j < half) {
                     const double c = static_cast<double>(a.cos_l[j]), s = static_cast<double>(a.sin_l[j]);
-                    const double a0 = last[j] * c, a1 = last[j + half] * s;
+                    const double a0 = v * c, a1 = load_q(a, lrow + j + half) * s;
                     v = a0 - a1;
                 } else {
                     const int jj = j - half;
                     const double c = static_cast<double>(a.cos_l[jj]), s = static_cast<double>(a.sin_l[jj]);
-                    const double b0 = last[j] * c, b1 = last[jj] * s;
+                    const double b0 = v * c, b1 = load_q(a, lrow + jj) * s;
                     v = b0 + b1;
                 }
             }
@@ -267,9 +296,9 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
 }  // namespace
 
 hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s) {
-    dim3 grid((a.P + kProxiesPerBlock - 1) / kProxiesPerBlock, a.Hq, a.B);
-    const size_t lds = 3 * static_cast<size_t>(a.d) * sizeof(double) +
-                       static_cast<size_t>(kWinChunk) * a.d * sizeof(float);
+    dim3 grid(a.d / kBlockDims, a.Hq, a.B);
+    const size_t lds = 2 * static_cast<size_t>(a.d) * sizeof(double) +
+                       static_cast<size_t>(kWinChunk) * kBlockDims * sizeof(float);
     hipLaunchKernelGGL(build_proxies_kernel, grid, dim3(kProxyThreads), lds, s, a);
     return hipGetLastError();
 }
