@@ -9,6 +9,10 @@ this module only marshals numpy arrays into it.  bf16 tensors are carried as
 Paper steps and where they are computed:
   * Sec. 3.2.1 Eqs. 4-5 (statistics, variance-expanded sampling) and the
     optional rotary placement of the proxies       -> ``build_proxies``
+  * Sec. 3.2.1 Eqs. 4-6 in hidden-state form (statistics of the prefill
+    hidden states, samples, projection by W_Q)     -> ``hidden_stats``,
+                                                      ``hidden_proxies``,
+                                                      ``project_proxies``
   * Sec. 3.2.2 Eqs. 7-8 (proxy softmax, group mass), Sec. 3.2.3 Eq. 11 (anchor)
                                                    -> ``score``
   * Sec. 3.2.2 Eqs. 9-10 (tau-sets, votes), Sec. 3.2.3 (keep-last + top C-1),
@@ -75,6 +79,12 @@ def _load():
     lib.oracle_gather.argtypes = [i32, i32, i32, i64, i32, P, P, P, P]
     lib.oracle_gather.restype = i32
     lib.oracle_num_threads.restype = i32
+    lib.oracle_hidden_stats.argtypes = [i32, i32, i32, i32, i32, P, i32, P]
+    lib.oracle_hidden_stats.restype = i32
+    lib.oracle_hidden_proxies.argtypes = [i32, i32, i32, f64, u64, i32, i32, P, P]
+    lib.oracle_hidden_proxies.restype = i32
+    lib.oracle_project_proxies.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, P, P]
+    lib.oracle_project_proxies.restype = i32
     _lib = lib
     return lib
 
@@ -269,3 +279,56 @@ def select_layer(q_win, k, v, Hkv: int, budget: int, P: int = 512, G: int = 32, 
     sel = select(gm, mass, anchor, budget, tau, lam, mode, keep_last, c_max)
     return LayerResult(prox, ql, st, gm, mass, anchor, sel, gather(k, sel.idx, sel.counts),
                        gather(v, sel.idx, sel.counts))
+
+
+HIDDEN_STATS_CHUNK = 256
+
+
+def hidden_stats(hidden: np.ndarray, ddof: int = 0, chunk: int = HIDDEN_STATS_CHUNK) -> np.ndarray:
+    """Sec. 3.2.1 Eq. 4 over the prefill hidden states [B, T, D] (fp32, or
+    bf16 bits as uint16): per (batch row, dim) mean and std, chunked merge in
+    token order.  Returns [B, 2, D] fp64."""
+    lib = _load()
+    h = np.ascontiguousarray(hidden)
+    B, T, D = h.shape
+    st = np.zeros((B, 2, D), dtype=np.float64)
+    rc = lib.oracle_hidden_stats(B, T, D, chunk, ddof, _ptr(h), _dtype_code(h), _ptr(st))
+    if rc != 0:
+        raise ValueError("oracle_hidden_stats: invalid arguments")
+    return st
+
+
+def hidden_proxies(stats: np.ndarray, P: int, gamma: float, seed: int, layer: int = 0, b0: int = 0) -> np.ndarray:
+    """Sec. 3.2.1 Eq. 5 in hidden space: [B, P, D] bf16 bits."""
+    lib = _load()
+    st = np.ascontiguousarray(stats, dtype=np.float64)
+    B, _, D = st.shape
+    hp = np.zeros((B, P, D), dtype=np.uint16)
+    rc = lib.oracle_hidden_proxies(B, D, P, gamma, seed, layer, b0, _ptr(st), _ptr(hp))
+    if rc != 0:
+        raise ValueError("oracle_hidden_proxies: invalid arguments")
+    return hp
+
+
+def project_proxies(hp: np.ndarray, wq: np.ndarray, Hq: int, rope=None, with_pre: bool = False):
+    """Sec. 3.2.1 Eq. 6: query proxies [B, Hq, P, d] bf16 bits from hidden
+    proxies hp [B, P, D] (bf16 bits) and W_Q [Hq*d, D] (bf16 bits); rope =
+    (cos, sin) [d/2] fp32 tables or None.  with_pre also returns the fp64
+    values before rounding."""
+    lib = _load()
+    hp = np.ascontiguousarray(hp, dtype=np.uint16)
+    wq = np.ascontiguousarray(wq, dtype=np.uint16)
+    B, P, D = hp.shape
+    d = wq.shape[0] // Hq
+    out = np.zeros((B, Hq, P, d), dtype=np.uint16)
+    pre = np.zeros((B, Hq, P, d), dtype=np.float64) if with_pre else None
+    c = s = None
+    if rope is not None:
+        c = np.ascontiguousarray(rope[0], dtype=np.float32)
+        s = np.ascontiguousarray(rope[1], dtype=np.float32)
+    rc = lib.oracle_project_proxies(B, P, D, Hq, d, _ptr(hp), _ptr(wq), _ptr(c) if c is not None else None,
+                                    _ptr(s) if s is not None else None, _ptr(out),
+                                    _ptr(pre) if pre is not None else None)
+    if rc != 0:
+        raise ValueError("oracle_project_proxies: invalid arguments")
+    return (out, pre) if with_pre else out

@@ -40,6 +40,12 @@
  *   - Selection: if T <= C keep all; else keep token T-1 plus the top C-1 of
  *     [0, T-1) by (score desc, index asc); output in ascending index order
  *     (Sec. 3.2.3; Appendix B; Algorithm 1).
+ *   - Hidden-state form (Sec. 3.2.1 as written, Algorithm 1): statistics of
+ *     the layer's prefill hidden states (the query projection's input) per
+ *     batch row and feature over all T prompt tokens; one set of N samples
+ *     per (batch row, layer) shared by every head, projected by each head's
+ *     query weights W_Q (no bias term, as in Eq. 6); the same rotary
+ *     placement and roundings as the query-space form.
  *
  * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (see build.py).
  * The -ffp-contract=off flag keeps every a*b+c as two rounded operations,
@@ -323,6 +329,159 @@ int oracle_build_proxies_at(int B, int Hq, int W, int d, int P, double gamma, in
             free(mu);
             free(sg);
             free(x);
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Step 1, hidden-state form (Sec. 3.2.1 Eqs. 4-6, Algorithm 1): statistics  */
+/* of the prefill hidden states of one layer, variance-expanded samples of  */
+/* them, and their projection by the query weights of every head.          */
+/* ------------------------------------------------------------------------ */
+/*
+ * Per (batch row, feature dimension): mean and std over the T prompt tokens
+ * (Eq. 4).  The tokens are taken in consecutive chunks of `chunk`; inside a
+ * chunk the sum and the sum of squared deviations from the chunk mean are
+ * accumulated in token order, and the chunks are merged in order by the
+ * pairwise update of Chan, Golub and LeVeque (1979):
+ *   n = nA + nB,  delta = mB - mA,  m = mA + delta * (nB / n),
+ *   M2 = (M2A + M2B) + (delta * delta) * ((nA * nB) / n);
+ * std = sqrt(M2 / (T - ddof)).  This fixes every rounding step.
+ * hidden [B, T, D] (row stride D), dtype 0 fp32 / 1 bf16; stats [B, 2, D].
+ */
+int oracle_hidden_stats(int B, int T, int D, int chunk, int ddof, const void *hidden, int dtype,
+                        double *stats)
+{
+    if (B < 1 || T < 1 || D < 1 || chunk < 1 || ddof < 0 || T - ddof < 1)
+        return -1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int j = 0; j < D; ++j) {
+            double n = 0.0, m = 0.0, M2 = 0.0;
+            for (int c0 = 0; c0 < T; c0 += chunk) {
+                int c1 = c0 + chunk < T ? c0 + chunk : T;
+                double s = 0.0;
+                for (int t = c0; t < c1; ++t)
+                    s = s + load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j);
+                double nB = (double)(c1 - c0);
+                double mB = s / nB;
+                double q = 0.0;
+                for (int t = c0; t < c1; ++t) {
+                    double diff = load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j) - mB;
+                    double dd = diff * diff;
+                    q = q + dd;
+                }
+                if (c0 == 0) {
+                    n = nB;
+                    m = mB;
+                    M2 = q;
+                } else {
+                    double nN = n + nB;
+                    double delta = mB - m;
+                    double w = nB / nN;
+                    double mN = m + delta * w;
+                    double cross = (n * nB) / nN;
+                    double dd = delta * delta;
+                    double M2N = (M2 + q) + dd * cross;
+                    n = nN;
+                    m = mN;
+                    M2 = M2N;
+                }
+            }
+            stats[((int64_t)b * 2) * D + j] = m;
+            stats[((int64_t)b * 2 + 1) * D + j] = sqrt(M2 / (double)(T - ddof));
+        }
+    }
+    return 0;
+}
+
+/*
+ * N proxy hidden states per batch row (Eq. 5): x = mu + (gamma*sigma)*z,
+ * z from the same counter-based generator with the head field of the
+ * counter set to 0xFFFFFFFF (hidden space, shared by all heads of the
+ * layer), fp64 -> fp32 -> bf16.  stats [B, 2, D]; hp [B, P, D] bf16.
+ * b0: global batch row of the first row.
+ */
+int oracle_hidden_proxies(int B, int D, int P, double gamma, uint64_t seed, int layer, int b0,
+                          const double *stats, uint16_t *hp)
+{
+    if (B < 1 || D < 4 || (D % 4) != 0 || P < 1 || layer < 0 || layer > 0xFFFF || b0 < 0 ||
+        B + b0 > 0xFFFF)
+        return -1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int i = 0; i < P; ++i) {
+            const double *mu = stats + ((int64_t)b * 2) * D;
+            const double *sg = stats + ((int64_t)b * 2 + 1) * D;
+            uint16_t *out = hp + ((int64_t)b * P + i) * D;
+            for (int jq = 0; jq < D / 4; ++jq) {
+                double z[4];
+                oracle_normal4(seed, b0 + b, layer, -1, i, jq, z);
+                for (int e = 0; e < 4; ++e) {
+                    int j = 4 * jq + e;
+                    double gs = gamma * sg[j];
+                    double t = gs * z[e];
+                    double x = mu[j] + t;
+                    out[j] = oracle_f32_to_bf16((float)x);
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Query proxies (Eq. 6): q[b, h, i, e] = sum_k H~[b, i, k] * W_Q[h*d + e, k]
+ * over the bf16 values, summed in k order in fp64, then the optional rotary
+ * placement (rotate-half pairs e, e + d/2, caller tables for one future
+ * position), fp64 -> fp32 -> bf16.  hp [B, P, D]; wq [Hq*d, D] bf16;
+ * proxies [B, Hq, P, d] bf16; pre [B, Hq, P, d] fp64 values before the
+ * rounding, or NULL.
+ */
+int oracle_project_proxies(int B, int P, int D, int Hq, int d, const uint16_t *hp, const uint16_t *wq,
+                           const float *rope_cos, const float *rope_sin, uint16_t *proxies, double *pre)
+{
+    if (B < 1 || P < 1 || D < 1 || Hq < 1 || d < 2 || (d % 2) != 0)
+        return -1;
+    int use_rope = (rope_cos != NULL && rope_sin != NULL);
+    int half = d / 2;
+#pragma omp parallel for collapse(3) schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int h = 0; h < Hq; ++h) {
+            for (int i = 0; i < P; ++i) {
+                double *x = (double *)malloc(sizeof(double) * (size_t)d);
+                const uint16_t *hv = hp + ((int64_t)b * P + i) * D;
+                for (int e = 0; e < d; ++e) {
+                    const uint16_t *wr = wq + ((int64_t)h * d + e) * D;
+                    double acc = 0.0;
+                    for (int k = 0; k < D; ++k) {
+                        double pr = oracle_bf16_to_f64(hv[k]) * oracle_bf16_to_f64(wr[k]);
+                        acc = acc + pr;
+                    }
+                    x[e] = acc;
+                }
+                int64_t o = (((int64_t)b * Hq + h) * P + i) * d;
+                for (int e = 0; e < (use_rope ? half : d); ++e) {
+                    if (use_rope) {
+                        double c = (double)rope_cos[e], s = (double)rope_sin[e];
+                        double a0 = x[e] * c, a1 = x[e + half] * s;
+                        double b0 = x[e + half] * c, b1 = x[e] * s;
+                        double lo = a0 - a1, hi = b0 + b1;
+                        proxies[o + e] = oracle_f32_to_bf16((float)lo);
+                        proxies[o + e + half] = oracle_f32_to_bf16((float)hi);
+                        if (pre) {
+                            pre[o + e] = lo;
+                            pre[o + e + half] = hi;
+                        }
+                    } else {
+                        proxies[o + e] = oracle_f32_to_bf16((float)x[e]);
+                        if (pre)
+                            pre[o + e] = x[e];
+                    }
+                }
+                free(x);
+            }
         }
     }
     return 0;
