@@ -341,13 +341,11 @@ int oracle_build_proxies_at(int B, int Hq, int W, int d, int P, double gamma, in
 /* ------------------------------------------------------------------------ */
 /*
  * Per (batch row, feature dimension): mean and std over the T prompt tokens
- * (Eq. 4).  The tokens are taken in consecutive chunks of `chunk`; inside a
- * chunk the sum and the sum of squared deviations from the chunk mean are
- * accumulated in token order, and the chunks are merged in order by the
- * pairwise update of Chan, Golub and LeVeque (1979):
- *   n = nA + nB,  delta = mB - mA,  m = mA + delta * (nB / n),
- *   M2 = (M2A + M2B) + (delta * delta) * ((nA * nB) / n);
- * std = sqrt(M2 / (T - ddof)).  This fixes every rounding step.
+ * (Eq. 4), from the sums of the values and of their squares:
+ *   mean = S / T,  var = (SS - S * mean) / (T - ddof),  std = sqrt(var)
+ * (var clamped at 0).  S and SS are accumulated in consecutive chunks of
+ * `chunk` tokens, each summed in token order, and the chunk sums are added
+ * in chunk order; this fixes every rounding step.
  * hidden [B, T, D] (row stride D), dtype 0 fp32 / 1 bf16; stats [B, 2, D].
  */
 int oracle_hidden_stats(int B, int T, int D, int chunk, int ddof, const void *hidden, int dtype,
@@ -358,39 +356,26 @@ int oracle_hidden_stats(int B, int T, int D, int chunk, int ddof, const void *hi
 #pragma omp parallel for collapse(2) schedule(static)
     for (int b = 0; b < B; ++b) {
         for (int j = 0; j < D; ++j) {
-            double n = 0.0, m = 0.0, M2 = 0.0;
+            double S = 0.0, SS = 0.0;
             for (int c0 = 0; c0 < T; c0 += chunk) {
                 int c1 = c0 + chunk < T ? c0 + chunk : T;
-                double s = 0.0;
-                for (int t = c0; t < c1; ++t)
-                    s = s + load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j);
-                double nB = (double)(c1 - c0);
-                double mB = s / nB;
-                double q = 0.0;
+                double s = 0.0, ss = 0.0;
                 for (int t = c0; t < c1; ++t) {
-                    double diff = load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j) - mB;
-                    double dd = diff * diff;
-                    q = q + dd;
+                    double v = load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j);
+                    double sq = v * v;
+                    s = s + v;
+                    ss = ss + sq;
                 }
-                if (c0 == 0) {
-                    n = nB;
-                    m = mB;
-                    M2 = q;
-                } else {
-                    double nN = n + nB;
-                    double delta = mB - m;
-                    double w = nB / nN;
-                    double mN = m + delta * w;
-                    double cross = (n * nB) / nN;
-                    double dd = delta * delta;
-                    double M2N = (M2 + q) + dd * cross;
-                    n = nN;
-                    m = mN;
-                    M2 = M2N;
-                }
+                S = S + s;
+                SS = SS + ss;
             }
-            stats[((int64_t)b * 2) * D + j] = m;
-            stats[((int64_t)b * 2 + 1) * D + j] = sqrt(M2 / (double)(T - ddof));
+            double mean = S / (double)T;
+            double sm = S * mean;
+            double var = (SS - sm) / (double)(T - ddof);
+            if (var < 0.0)
+                var = 0.0;
+            stats[((int64_t)b * 2) * D + j] = mean;
+            stats[((int64_t)b * 2 + 1) * D + j] = sqrt(var);
         }
     }
     return 0;

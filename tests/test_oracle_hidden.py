@@ -30,7 +30,7 @@ def hidden_states(B, T, D, seed, scale=1.0):
 @pytest.mark.parametrize("T,chunk", [(1, 256), (5, 2), (300, 256), (512, 256), (777, 64), (40, 1), (33, 33)])
 def test_hidden_stats_match_numpy(oracle_lib, T, chunk):
     """Mean and std per (batch row, feature) over all prompt tokens; a wrong
-    axis, a dropped chunk or a bad merge term moves these far off."""
+    axis, a dropped chunk or a wrong divisor moves these far off."""
     h = hidden_states(2, T, 24, T)
     st = oracle_lib.hidden_stats(h, ddof=0, chunk=chunk)
     h64 = h.astype(np.float64)
@@ -42,8 +42,9 @@ def test_hidden_stats_match_numpy(oracle_lib, T, chunk):
 
 
 def test_hidden_stats_chunk_merge_exact_small_case(oracle_lib):
-    """Tokens 1, 2, 3 | 4, 5 (chunk 3): mean 3 and M2 = 10 exactly, so the
-    population std is sqrt(2); checks the merge update term by term."""
+    """Tokens 1, 2, 3 | 4, 5 (chunk 3): S = 15, SS = 55, so mean 3 and
+    SS - S*mean = 10 exactly: population std sqrt(2), sample std sqrt(2.5);
+    a dropped chunk or a square missing from SS fails."""
     h = np.array([1, 2, 3, 4, 5], dtype=np.float32).reshape(1, 5, 1)
     st = oracle_lib.hidden_stats(h, ddof=0, chunk=3)
     assert st[0, 0, 0] == 3.0
