@@ -181,6 +181,58 @@ int mmshiftkv_gather_kv(const mmskv_shape *shape, const void *k, const void *v, 
                         const int32_t *idx, const int32_t *counts, int32_t c_max,
                         void *k_out, void *v_out, void *stream);
 
+/* ---- Hidden-state form of the proxies (Sec. 3.2.1 Eqs. 4-6 as written;
+ * Algorithm 1).  The statistics are taken over a layer's prefill hidden
+ * states (the input of the query projection), the samples are drawn in
+ * hidden space, and every query head's proxies are its projection W_Q^(h) of
+ * the same samples, rotated to the future position.  The three calls replace
+ * mmshiftkv_build_proxies; their output feeds mmshiftkv_score unchanged, with
+ * q_last taken from the model's own last query.
+ *
+ * Sizes of one layer's hidden states: B batch rows (<= 65535), T prompt
+ * tokens (>= 1), D hidden features (a multiple of 8). */
+typedef struct {
+    int32_t B, T, D;
+} mmskv_hshape;
+
+/* Eq. 4 over hidden [B, T, D] (dtype, element strides sb / st; features
+ * contiguous, rows on 16-byte boundaries): per (b, feature) fp64 mean and
+ * std with divisor T - std_ddof (std_ddof 0 or 1, T - std_ddof >= 1).  Sums
+ * of values and of squares are taken per chunk of 256 tokens in token order,
+ * then added in chunk order; var = (SS - S*mean) / (T - std_ddof), negative
+ * values clamped to 0.
+ *   stats [B, 2, D] fp64 out (mean row, then std row), contiguous
+ * Workspace: mmshiftkv_hidden_stats_workspace bytes (256-byte aligned). */
+size_t mmshiftkv_hidden_stats_workspace(const mmskv_hshape *shape);
+int mmshiftkv_hidden_stats(const mmskv_hshape *shape, int32_t std_ddof,
+                           const void *hidden, int32_t dtype, int64_t sb, int64_t st,
+                           double *stats, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Eq. 5 in hidden space: sample i of batch row b, feature j,
+ *   x = mu_j + (gamma * sigma_j) * z,
+ * z from the generator of mmshiftkv_build_proxies with the head field of the
+ * counter set to 0xFFFFFFFF (one sample set per layer, shared by all heads);
+ * fp64 -> fp32 -> bf16.  Uses params->P, gamma, seed and layer only.
+ *   stats [B, 2, D] fp64 from mmshiftkv_hidden_stats
+ *   hp    [B, P, D] bf16 out, contiguous, 8-byte aligned */
+int mmshiftkv_hidden_proxies(const mmskv_hshape *shape, const mmskv_params *params,
+                             const double *stats, uint16_t *hp, void *stream);
+
+/* Eq. 6: proxies[b, h, i, :] = W_Q^(h) hp[b, i, :] (bf16 operands, fp32
+ * accumulation on the matrix cores), then, when rope_cos / rope_sin are
+ * given, the rotate-half rotary embedding at the future position (pairs
+ * e, e + d/2, fp32), rounded to bf16.
+ *   hp        [B, P, D] bf16, contiguous
+ *   wq        [Hq * d, D] bf16, contiguous (row h*d + e is output feature e
+ *             of head h; no bias)
+ *   rope_*    [d/2] fp32 or both NULL
+ *   proxies   [B, Hq, P, d] bf16 out, contiguous
+ * d is 64 or 128; hp, wq and proxies start on 16-byte boundaries. */
+int mmshiftkv_project_proxies(const mmskv_hshape *shape, int32_t P, int32_t Hq, int32_t d,
+                              const uint16_t *hp, const uint16_t *wq,
+                              const float *rope_cos, const float *rope_sin,
+                              uint16_t *proxies, void *stream);
+
 /* Human-readable text for an mmskv_status value (static storage). */
 const char *mmshiftkv_status_string(int status);
 

@@ -23,12 +23,17 @@ MMSKV_VOTE, MMSKV_MASS = 0, 1
 EXPORTED = ("mmshiftkv_build_proxies", "mmshiftkv_score_workspace", "mmshiftkv_score",
             "mmshiftkv_score_lse", "mmshiftkv_score_mass", "mmshiftkv_select_workspace",
             "mmshiftkv_select_topk", "mmshiftkv_gather_kv", "mmshiftkv_status_string",
-            "mmshiftkv_version")
+            "mmshiftkv_version", "mmshiftkv_hidden_stats_workspace", "mmshiftkv_hidden_stats",
+            "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies")
 
 
 class Shape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32),
                 ("T", ctypes.c_int32), ("W", ctypes.c_int32), ("d", ctypes.c_int32)]
+
+
+class HShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("D", ctypes.c_int32)]
 
 
 class Strides(ctypes.Structure):
@@ -73,11 +78,18 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_select_workspace.restype = SZ
     lib.mmshiftkv_select_topk.argtypes = [PS, PP, V, V, V, V, I32, I32, V, V, V, V, SZ, V]
     lib.mmshiftkv_gather_kv.argtypes = [PS, V, V, I32, PT, PT, V, V, I32, V, V, V]
+    PH = ctypes.POINTER(HShape)
+    lib.mmshiftkv_hidden_stats_workspace.argtypes = [PH]
+    lib.mmshiftkv_hidden_stats_workspace.restype = SZ
+    lib.mmshiftkv_hidden_stats.argtypes = [PH, I32, V, I32, I64, I64, V, V, SZ, V]
+    lib.mmshiftkv_hidden_proxies.argtypes = [PH, PP, V, V, V]
+    lib.mmshiftkv_project_proxies.argtypes = [PH, I32, I32, I32, V, V, V, V, V, V]
     lib.mmshiftkv_status_string.argtypes = [ctypes.c_int]
     lib.mmshiftkv_status_string.restype = ctypes.c_char_p
     lib.mmshiftkv_version.restype = ctypes.c_int
     for name in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_score_lse",
-                 "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_gather_kv"):
+                 "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_gather_kv",
+                 "mmshiftkv_hidden_stats", "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -180,6 +192,74 @@ def build_proxies(q_win: torch.Tensor, cfg: SelectionConfig, T: int, Hkv: int, r
             _p(stats), _stream(dev))
     _check("mmshiftkv_build_proxies", rc)
     return (proxies, q_last, stats) if with_stats else (proxies, q_last)
+
+
+# hidden-state form of the proxies (statistics of the prefill hidden states,
+# samples in hidden space, projection by each head's W_Q)
+def hidden_stats_workspace(B: int, T: int, D: int) -> int:
+    return int(load_library().mmshiftkv_hidden_stats_workspace(ctypes.byref(HShape(int(B), int(T), int(D)))))
+
+
+def hidden_stats(hidden: torch.Tensor, std_ddof: int = 0, out=None, workspace=None) -> torch.Tensor:
+    """mmshiftkv_hidden_stats: hidden [B, T, D] (features contiguous) -> [B, 2, D] fp64."""
+    dev = _dev(hidden)
+    if hidden.dim() != 3 or hidden.stride(2) != 1:
+        raise ValueError("expected a [batch, token, feature] tensor with contiguous features")
+    B, T, D = hidden.shape
+    hs = HShape(B, T, D)
+    st = out if out is not None else torch.empty((B, 2, D), dtype=torch.float64, device=dev)
+    if st.dtype != torch.float64 or not st.is_contiguous() or tuple(st.shape) != (B, 2, D):
+        raise ValueError("preallocated stats do not match")
+    ws = workspace if workspace is not None else _ws(hidden_stats_workspace(B, T, D), dev)
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_hidden_stats(
+            ctypes.byref(hs), int(std_ddof), _p(hidden), _dtype_code(hidden), hidden.stride(0),
+            hidden.stride(1), _p(st), _p(ws), ws.numel() * ws.element_size(), _stream(dev))
+    _check("mmshiftkv_hidden_stats", rc)
+    return st
+
+
+def hidden_proxies(stats: torch.Tensor, cfg: SelectionConfig, T: int = 1, out=None) -> torch.Tensor:
+    """mmshiftkv_hidden_proxies: stats [B, 2, D] fp64 -> samples [B, P, D] bf16."""
+    dev = _dev(stats)
+    B, two, D = stats.shape
+    if two != 2 or stats.dtype != torch.float64 or not stats.is_contiguous():
+        raise ValueError("expected contiguous fp64 stats [B, 2, D]")
+    hp = out if out is not None else torch.empty((B, cfg.P, D), dtype=torch.bfloat16, device=dev)
+    if hp.dtype != torch.bfloat16 or not hp.is_contiguous() or tuple(hp.shape) != (B, cfg.P, D):
+        raise ValueError("preallocated samples do not match")
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_hidden_proxies(ctypes.byref(HShape(B, int(T), D)),
+                                                     ctypes.byref(cfg.c_params()), _p(stats), _p(hp),
+                                                     _stream(dev))
+    _check("mmshiftkv_hidden_proxies", rc)
+    return hp
+
+
+def project_proxies(hp: torch.Tensor, wq: torch.Tensor, Hq: int, rope=None, out=None) -> torch.Tensor:
+    """mmshiftkv_project_proxies: samples [B, P, D] bf16 and W_Q [Hq*d, D] bf16
+    -> proxies [B, Hq, P, d] bf16; rope = (cos, sin) [d/2] fp32 or None."""
+    dev = _dev(hp)
+    B, P, D = hp.shape
+    N, D2 = wq.shape
+    if D2 != D or N % Hq != 0:
+        raise ValueError("W_Q must be [Hq*d, D]")
+    d = N // Hq
+    if hp.dtype != torch.bfloat16 or wq.dtype != torch.bfloat16 or not hp.is_contiguous() \
+            or not wq.is_contiguous():
+        raise ValueError("samples and W_Q must be contiguous bf16")
+    pr = out if out is not None else torch.empty((B, Hq, P, d), dtype=torch.bfloat16, device=dev)
+    if pr.dtype != torch.bfloat16 or not pr.is_contiguous() or tuple(pr.shape) != (B, Hq, P, d):
+        raise ValueError("preallocated proxies do not match")
+    tabs = [None, None]
+    if rope is not None:
+        tabs = [rope[0].to(device=dev, dtype=torch.float32).contiguous(),
+                rope[1].to(device=dev, dtype=torch.float32).contiguous()]
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_project_proxies(ctypes.byref(HShape(B, 1, D)), P, int(Hq), d, _p(hp),
+                                                      _p(wq), _p(tabs[0]), _p(tabs[1]), _p(pr), _stream(dev))
+    _check("mmshiftkv_project_proxies", rc)
+    return pr
 
 
 def score_workspace(B, Hq, Hkv, T, W, d, cfg: SelectionConfig) -> int:

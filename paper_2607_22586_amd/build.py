@@ -11,8 +11,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmmshiftkv.so")
-SOURCES = ["api.hip", "proxies.hip", "score.hip", "select.hip", "gather.hip"]
-HEADERS = ["common.hpp", "kernels.hpp"]
+SOURCES = ["api.hip", "proxies.hip", "score.hip", "select.hip", "gather.hip", "hidden.hip"]
+HEADERS = ["common.hpp", "kernels.hpp", "normal.hpp"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are disabled for every device compilation.

@@ -145,6 +145,19 @@ int check_score_outputs(const mmskv_params* p, const float* gm, const float* mas
     return MMSKV_OK;
 }
 
+constexpr int kHiddenChunk = 256;   // tokens per partial sum of the hidden statistics
+
+int check_hshape(const mmskv_hshape* s) {
+    if (s == nullptr) return MMSKV_EINVAL;
+    if (s->B < 1 || s->B > 65535 || s->T < 1 || s->D < 8 || s->D % 8 != 0) return MMSKV_EINVAL;
+    return MMSKV_OK;
+}
+
+size_t hidden_stats_ws(const mmskv_hshape* s) {
+    const size_t chunks = (static_cast<size_t>(s->T) + kHiddenChunk - 1) / kHiddenChunk;
+    return align_up(static_cast<size_t>(s->B) * chunks * s->D * sizeof(double2));
+}
+
 }  // namespace
 
 extern "C" {
@@ -344,6 +357,89 @@ int mmshiftkv_gather_kv(const mmskv_shape* shape, const void* k, const void* v, 
     a.k_out = k_out;
     a.v_out = v_out;
     return status_of(launch_gather(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t mmshiftkv_hidden_stats_workspace(const mmskv_hshape* shape) {
+    if (check_hshape(shape)) return 0;
+    return hidden_stats_ws(shape);
+}
+
+int mmshiftkv_hidden_stats(const mmskv_hshape* shape, int32_t std_ddof, const void* hidden, int32_t dtype,
+                           int64_t sb, int64_t st, double* stats, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+    int rc = check_hshape(shape);
+    if (rc) return rc;
+    const int eb = elem_bytes(dtype);
+    if (eb == 0 || hidden == nullptr || stats == nullptr) return MMSKV_EINVAL;
+    if (std_ddof != 0 && std_ddof != 1) return MMSKV_EINVAL;
+    if (shape->T - std_ddof < 1) return MMSKV_EINVAL;
+    if (sb < 0 || st < 0 || !aligned(hidden, 16) || (sb * eb) % 16 || (st * eb) % 16) return MMSKV_EINVAL;
+    if (!aligned(stats, 8)) return MMSKV_EINVAL;
+    if (workspace == nullptr || !aligned(workspace, kAlign) || workspace_bytes < hidden_stats_ws(shape))
+        return MMSKV_EWORKSPACE;
+    HiddenArgs a = {};
+    a.hidden = hidden;
+    a.dtype = dtype;
+    a.sb = sb;
+    a.st = st;
+    a.B = shape->B;
+    a.T = shape->T;
+    a.D = shape->D;
+    a.chunk = kHiddenChunk;
+    a.n_chunks = (shape->T + kHiddenChunk - 1) / kHiddenChunk;
+    a.ddof = std_ddof;
+    a.partial = static_cast<double2*>(workspace);
+    a.stats = stats;
+    return status_of(launch_hidden_stats(a, static_cast<hipStream_t>(stream)));
+}
+
+int mmshiftkv_hidden_proxies(const mmskv_hshape* shape, const mmskv_params* params, const double* stats,
+                             uint16_t* hp, void* stream) {
+    int rc = check_hshape(shape);
+    if (rc) return rc;
+    if (params == nullptr || stats == nullptr || hp == nullptr) return MMSKV_EINVAL;
+    if (params->P < 1 || !(params->gamma >= 0.0) || !isfinite(params->gamma)) return MMSKV_EINVAL;
+    if (params->layer < 0 || params->layer > 65535) return MMSKV_EINVAL;
+    if (!aligned(stats, 8) || !aligned(hp, 8)) return MMSKV_EINVAL;
+    HiddenArgs a = {};
+    a.B = shape->B;
+    a.T = shape->T;
+    a.D = shape->D;
+    a.stats = const_cast<double*>(stats);
+    a.hp = hp;
+    a.P = params->P;
+    a.layer = params->layer;
+    a.gamma = params->gamma;
+    a.key0 = static_cast<uint32_t>(params->seed & 0xFFFFFFFFull);
+    a.key1 = static_cast<uint32_t>(params->seed >> 32);
+    return status_of(launch_hidden_proxies(a, static_cast<hipStream_t>(stream)));
+}
+
+int mmshiftkv_project_proxies(const mmskv_hshape* shape, int32_t P, int32_t Hq, int32_t d, const uint16_t* hp,
+                              const uint16_t* wq, const float* rope_cos, const float* rope_sin,
+                              uint16_t* proxies, void* stream) {
+    int rc = check_hshape(shape);
+    if (rc) return rc;
+    if (P < 1 || Hq < 1 || hp == nullptr || wq == nullptr || proxies == nullptr) return MMSKV_EINVAL;
+    if (d != 64 && d != 128) return MMSKV_EUNSUPPORTED;
+    if ((rope_cos == nullptr) != (rope_sin == nullptr)) return MMSKV_EINVAL;
+    if (!aligned(hp, 16) || !aligned(wq, 16) || !aligned(proxies, 16)) return MMSKV_EINVAL;
+    if (rope_cos && (!aligned(rope_cos, 4) || !aligned(rope_sin, 4))) return MMSKV_EINVAL;
+    const int64_t M = static_cast<int64_t>(shape->B) * P, N = static_cast<int64_t>(Hq) * d;
+    if (M > (1 << 30) || N > (1 << 30)) return MMSKV_EINVAL;
+    ProjectArgs a = {};
+    a.a = hp;
+    a.w = wq;
+    a.cos = rope_cos;
+    a.sin = rope_sin;
+    a.out = proxies;
+    a.M = static_cast<int>(M);
+    a.N = static_cast<int>(N);
+    a.K = shape->D;
+    a.P = P;
+    a.Hq = Hq;
+    a.d = d;
+    return status_of(launch_project(a, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

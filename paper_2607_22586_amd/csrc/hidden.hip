@@ -1,0 +1,316 @@
+// Hidden-state form of the proxies (Sec. 3.2.1 Eqs. 4-6 as written, and
+// Algorithm 1): statistics of a layer's prefill hidden states, variance-
+// expanded samples of them, and their projection by every head's query
+// weights, on gfx950.
+//
+// hidden_stats   per (batch row, feature): S = sum h and SS = sum h^2 over
+//                chunks of tokens (token order inside a chunk, one thread
+//                per 8 features, fp64), then the chunk sums in chunk order;
+//                mean = S/T, std = sqrt((SS - S*mean)/(T - ddof)).
+// hidden_proxies x = mu + (gamma*sigma) z per (batch row, sample, feature),
+//                z from the counter-based generator with the head field set
+//                to 0xFFFFFFFF (one set of samples per layer, shared by all
+//                heads), fp64 -> fp32 -> bf16.
+// project        q[b, h, i, :] = W_Q^(h) H~[b, i, :]: a bf16 GEMM of the
+//                (B*P) x D samples against the (Hq*d) x D weights (both with
+//                the reduction dimension contiguous) on
+//                v_mfma_f32_32x32x16_bf16 with fp32 accumulation: 128x128
+//                output tiles, 64-wide k steps double buffered in LDS through
+//                registers, four waves of 64x64; the epilogue goes through
+//                LDS so that the rotary pairs (e, e + d/2) of a head meet in
+//                one thread, then rounds to bf16.
+#pragma clang fp contract(off)
+
+#include <math.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+#include "normal.hpp"
+
+namespace mmskv {
+namespace {
+
+constexpr int kStatThreads = 256;
+constexpr int kStatVec = 8;                 // features per thread (one 16-byte bf16 load)
+
+// 8 consecutive features of one token as fp64.
+__device__ __forceinline__ void load8(const HiddenArgs& a, int64_t off, double (&v)[kStatVec]) {
+    if (a.dtype == 1) {
+        const u32x4 r = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.hidden) + off);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            v[2 * q] = static_cast<double>(__uint_as_float(r[q] << 16));
+            v[2 * q + 1] = static_cast<double>(__uint_as_float(r[q] & 0xFFFF0000u));
+        }
+    } else {
+        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.hidden) + off);
+        const float4 y = *reinterpret_cast<const float4*>(static_cast<const float*>(a.hidden) + off + 4);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+        v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+    }
+}
+
+// Chunk sums: grid (n_chunks, ceil(D / (8*256)), B).
+__global__ void __launch_bounds__(kStatThreads) hidden_stats_partial_kernel(HiddenArgs a) {
+    const int c = blockIdx.x, b = blockIdx.z;
+    const int j0 = (static_cast<int>(blockIdx.y) * kStatThreads + static_cast<int>(threadIdx.x)) * kStatVec;
+    if (j0 >= a.D) return;
+    const int t0 = c * a.chunk, t1 = min(t0 + a.chunk, a.T);
+    double s[kStatVec], ss[kStatVec];
+#pragma unroll
+    for (int e = 0; e < kStatVec; ++e) { s[e] = 0.0; ss[e] = 0.0; }
+    const int64_t base = static_cast<int64_t>(b) * a.sb + j0;
+    int t = t0;
+    // four tokens' loads in flight, accumulated in token order
+    for (; t + 4 <= t1; t += 4) {
+        double v[4][kStatVec];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) load8(a, base + static_cast<int64_t>(t + u) * a.st, v[u]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int e = 0; e < kStatVec; ++e) {
+                const double sq = v[u][e] * v[u][e];
+                s[e] = s[e] + v[u][e];
+                ss[e] = ss[e] + sq;
+            }
+    }
+    for (; t < t1; ++t) {
+        double v[kStatVec];
+        load8(a, base + static_cast<int64_t>(t) * a.st, v);
+#pragma unroll
+        for (int e = 0; e < kStatVec; ++e) {
+            const double sq = v[e] * v[e];
+            s[e] = s[e] + v[e];
+            ss[e] = ss[e] + sq;
+        }
+    }
+    double2* out = a.partial + (static_cast<int64_t>(b) * a.n_chunks + c) * a.D + j0;
+#pragma unroll
+    for (int e = 0; e < kStatVec; ++e) out[e] = make_double2(s[e], ss[e]);
+}
+
+// Chunk sums in chunk order -> mean, std: grid (ceil(D/256), B).
+__global__ void __launch_bounds__(256) hidden_stats_final_kernel(HiddenArgs a) {
+    const int j = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x), b = blockIdx.y;
+    if (j >= a.D) return;
+    const double2* p = a.partial + static_cast<int64_t>(b) * a.n_chunks * a.D + j;
+    double S = 0.0, SS = 0.0;
+    for (int c = 0; c < a.n_chunks; ++c) {
+        const double2 v = p[static_cast<int64_t>(c) * a.D];
+        S = S + v.x;
+        SS = SS + v.y;
+    }
+    const double mean = S / static_cast<double>(a.T);
+    const double sm = S * mean;
+    double var = (SS - sm) / static_cast<double>(a.T - a.ddof);
+    if (var < 0.0) var = 0.0;
+    a.stats[(static_cast<int64_t>(b) * 2) * a.D + j] = mean;
+    a.stats[(static_cast<int64_t>(b) * 2 + 1) * a.D + j] = sqrt(var);
+}
+
+// Samples: one thread per (sample i, feature quad jq); grid (ceil(P*D/4 / 256), B).
+__global__ void __launch_bounds__(256) hidden_proxies_kernel(HiddenArgs a) {
+    const int b = blockIdx.y;
+    const int quads = a.D / 4;
+    const int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (item >= static_cast<int64_t>(a.P) * quads) return;
+    const int i = static_cast<int>(item / quads), jq = static_cast<int>(item % quads);
+    const double* mu = a.stats + (static_cast<int64_t>(b) * 2) * a.D;
+    const double* sg = a.stats + (static_cast<int64_t>(b) * 2 + 1) * a.D;
+    double z[4];
+    normal_quad(a.key0, a.key1, b, a.layer, -1, i, jq, z);
+    uint16_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int j = 4 * jq + e;
+        const double gs = a.gamma * sg[j];
+        const double t = gs * z[e];
+        const double x = mu[j] + t;
+        o[e] = static_cast<uint16_t>(f32_to_bf16_bits(static_cast<float>(x)));
+    }
+    uint2 pk;
+    pk.x = o[0] | (static_cast<uint32_t>(o[1]) << 16);
+    pk.y = o[2] | (static_cast<uint32_t>(o[3]) << 16);
+    *reinterpret_cast<uint2*>(a.hp + (static_cast<int64_t>(b) * a.P + i) * a.D + 4 * jq) = pk;
+}
+
+// ------------------------------------------------------------ projection GEMM
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kGemmThreads = 256;
+constexpr int kRowChunks = kBK / 8;            // 16-byte chunks per tile row
+constexpr int kRowSlots = kRowChunks + 1;      // padded row (one spare chunk)
+constexpr int kTileSlots = kBM * kRowSlots;    // per operand tile
+constexpr int kLoads = kBM * kRowChunks / kGemmThreads;   // chunks per thread per operand
+
+__device__ __forceinline__ floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Rows r of A (M x K) and of W (N x K) in 16-byte chunks; rows past the
+// matrix and k past D read as zero.
+struct GemmStage {
+    u32x4 a[kLoads], w[kLoads];
+};
+
+__device__ __forceinline__ void gemm_fetch(const ProjectArgs& p, int m0, int n0, int k0, GemmStage& st) {
+#pragma unroll
+    for (int q = 0; q < kLoads; ++q) {
+        const int c = static_cast<int>(threadIdx.x) + q * kGemmThreads;
+        const int r = c / kRowChunks, kc = c % kRowChunks;
+        const int k = k0 + 8 * kc;
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+        st.a[q] = (m0 + r < p.M && k < p.K)
+                      ? *reinterpret_cast<const u32x4*>(p.a + static_cast<int64_t>(m0 + r) * p.K + k) : zero;
+        st.w[q] = (n0 + r < p.N && k < p.K)
+                      ? *reinterpret_cast<const u32x4*>(p.w + static_cast<int64_t>(n0 + r) * p.K + k) : zero;
+    }
+}
+
+__device__ __forceinline__ void gemm_store(const GemmStage& st, u32x4* la, u32x4* lw) {
+#pragma unroll
+    for (int q = 0; q < kLoads; ++q) {
+        const int c = static_cast<int>(threadIdx.x) + q * kGemmThreads;
+        const int r = c / kRowChunks, kc = c % kRowChunks;
+        la[r * kRowSlots + kc] = st.a[q];
+        lw[r * kRowSlots + kc] = st.w[q];
+    }
+}
+
+__global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
+    // two stages of (A tile, W tile); the fp32 output tile reuses the space
+    __shared__ u32x4 lds[2 * 2 * kTileSlots];
+    const int m0 = static_cast<int>(blockIdx.x) * kBM, n0 = static_cast<int>(blockIdx.y) * kBN;
+    const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
+    const int wm = wave >> 1, wn = wave & 1;           // 64 x 64 quadrant of the wave
+    const int n_k = (p.K + kBK - 1) / kBK;
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
+
+    GemmStage st;
+    gemm_fetch(p, m0, n0, 0, st);
+    gemm_store(st, lds, lds + kTileSlots);
+    __syncthreads();
+    for (int ks = 0; ks < n_k; ++ks) {
+        const int cur = ks & 1;
+        const u32x4* la = lds + cur * 2 * kTileSlots;
+        const u32x4* lw = la + kTileSlots;
+        if (ks + 1 < n_k) gemm_fetch(p, m0, n0, (ks + 1) * kBK, st);
+#pragma unroll
+        for (int kc = 0; kc < kBK / 16; ++kc) {
+            bf16x8 fa[2], fw[2];
+            const int chunk = 2 * kc + (lane >> 5);
+#pragma unroll
+            for (int x = 0; x < 2; ++x) {
+                fa[x] = __builtin_bit_cast(bf16x8, la[(wm * 64 + 32 * x + (lane & 31)) * kRowSlots + chunk]);
+                fw[x] = __builtin_bit_cast(bf16x8, lw[(wn * 64 + 32 * x + (lane & 31)) * kRowSlots + chunk]);
+            }
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(fa[x], fw[y], acc[x][y]);
+        }
+        if (ks + 1 < n_k) {
+            u32x4* na = lds + (cur ^ 1) * 2 * kTileSlots;
+            gemm_store(st, na, na + kTileSlots);
+        }
+        __syncthreads();
+    }
+
+    // epilogue: fp32 tile [kBM][kBN + 4] in LDS, then rotary pairs and bf16
+    constexpr int kLd = kBN + 4;
+    float* tile = reinterpret_cast<float*>(lds);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int r = wm * 64 + 32 * x + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+                const int cc = wn * 64 + 32 * y + (lane & 31);
+                tile[r * kLd + cc] = acc[x][y][i];
+            }
+    __syncthreads();
+    const int d = p.d, half = d / 2;
+    const bool rope = p.cos != nullptr;
+    // each thread: one row, 8 consecutive output columns (one head's
+    // lower half when rotary pairs are formed)
+    const int groups = rope ? kBN / 16 : kBN / 8;     // 8-column groups per row
+    for (int g = static_cast<int>(threadIdx.x); g < kBM * groups; g += kGemmThreads) {
+        const int r = g / groups, cg = g % groups;
+        const int m = m0 + r;
+        if (m >= p.M) continue;
+        const int bb = m / p.P, i = m % p.P;
+        int col;
+        if (rope) {
+            const int c8 = cg * 8;                     // lower-half column index inside the tile's heads
+            col = (c8 / half) * d + (c8 % half);
+        } else {
+            col = cg * 8;
+        }
+        const int n = n0 + col;
+        if (n >= p.N) continue;
+        const int h = n / d, e = n % d;
+        uint16_t* out = p.out + ((static_cast<int64_t>(bb) * p.Hq + h) * p.P + i) * d;
+        u32x4 lo, hi;
+        if (!rope) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                lo[q] = f32_to_bf16_bits(tile[r * kLd + col + 2 * q]) |
+                        (f32_to_bf16_bits(tile[r * kLd + col + 2 * q + 1]) << 16);
+            *reinterpret_cast<u32x4*>(out + e) = lo;
+        } else {
+            uint32_t l16[8], h16[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const float x0 = tile[r * kLd + col + q], x1 = tile[r * kLd + col + half + q];
+                const float c = p.cos[e + q], s = p.sin[e + q];
+                const float a0 = x0 * c, a1 = x1 * s, b0 = x1 * c, b1 = x0 * s;
+                l16[q] = f32_to_bf16_bits(a0 - a1);
+                h16[q] = f32_to_bf16_bits(b0 + b1);
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                lo[q] = l16[2 * q] | (l16[2 * q + 1] << 16);
+                hi[q] = h16[2 * q] | (h16[2 * q + 1] << 16);
+            }
+            *reinterpret_cast<u32x4*>(out + e) = lo;
+            *reinterpret_cast<u32x4*>(out + e + half) = hi;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_hidden_stats(const HiddenArgs& a, hipStream_t s) {
+    dim3 g1(a.n_chunks, (a.D + kStatThreads * kStatVec - 1) / (kStatThreads * kStatVec), a.B);
+    hipLaunchKernelGGL(hidden_stats_partial_kernel, g1, dim3(kStatThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 g2((a.D + 255) / 256, a.B);
+    hipLaunchKernelGGL(hidden_stats_final_kernel, g2, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s) {
+    const int64_t items = static_cast<int64_t>(a.P) * (a.D / 4);
+    dim3 g(static_cast<unsigned>((items + 255) / 256), a.B);
+    hipLaunchKernelGGL(hidden_proxies_kernel, g, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_project(const ProjectArgs& p, hipStream_t s) {
+    dim3 g((p.M + kBM - 1) / kBM, (p.N + kBN - 1) / kBN);
+    hipLaunchKernelGGL(project_kernel, g, dim3(kGemmThreads), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace mmskv

@@ -68,10 +68,34 @@ struct GatherArgs {
     void* k_out; void* v_out;
 };
 
+struct HiddenArgs {
+    const void* hidden;   // [B, T, D], D contiguous
+    int dtype;            // 0 fp32, 1 bf16
+    int64_t sb, st;       // element strides of batch row and token
+    int B, T, D, chunk, n_chunks, ddof;
+    double2* partial;     // [B, n_chunks, D] per-chunk (sum, sum of squares)
+    double* stats;        // [B, 2, D] mean then std
+    uint16_t* hp;         // [B, P, D] hidden-space samples (bf16)
+    int P, layer;
+    double gamma;
+    uint32_t key0, key1;
+};
+
+struct ProjectArgs {
+    const uint16_t* a;    // [M, K] hidden-space samples, M = B * P
+    const uint16_t* w;    // [N, K] query weights, N = Hq * d
+    const float* cos; const float* sin;   // [d/2] or null
+    uint16_t* out;        // [B, Hq, P, d]
+    int M, N, K, P, Hq, d;
+};
+
 hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s);
 hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s);
 hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+hipError_t launch_hidden_stats(const HiddenArgs& a, hipStream_t s);
+hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s);
+hipError_t launch_project(const ProjectArgs& p, hipStream_t s);
 
 }  // namespace mmskv

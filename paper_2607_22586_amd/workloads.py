@@ -23,6 +23,15 @@ Five named workloads (sizes per layer):
                 W=64, C=1024.  Each query head's window is N(0,1.5) plus the
                 mean shift of one randomly chosen block of its KV head.
 
+Hidden-state inputs (``make_hidden``, for the hidden-state form of the
+proxies): per layer, prefill hidden states [B, T, D] with D = Hq*d (3584 for
+the 7B shapes, as in a Qwen2-style 7B backbone whose query projection is
+square) and a query weight W_Q [Hq*d, D] ~ N(0, 1/D).  Hidden rows are the
+normalised inputs of the query projection: per-feature scale s_j =
+exp(0.5 n_j), visual rows s * (sqrt(1-eps^2) (A M)/sqrt(r) + eps E) (rank 64,
+eps 0.1), text rows s * N(0, 1.5), and 4 outlier features whose values are
+scaled by 10 (the few large-magnitude channels of LLM hidden states).
+
 Tensors are drawn in fp32 with a seeded ``torch.Generator`` on the requested
 device and rounded to bf16 (round to nearest even) where the workload is bf16.
 The CPU stream is reproducible bit for bit; a device stream follows the same
@@ -173,6 +182,71 @@ def make_layer(w: Workload | str, layer: int = 0, device="cpu"):
         if w.dtype == "bf16":
             q, k, v = (x.to(torch.bfloat16) for x in (q, k, v))
     return dict(q_win=q.contiguous(), k=k.contiguous(), v=v.contiguous(), planted=planted)
+
+
+HIDDEN_OUTLIERS = 4
+HIDDEN_OUTLIER_SCALE = 10.0
+
+
+def make_hidden(w: Workload | str, layer: int = 0, device="cpu", T: int | None = None):
+    """Hidden-state inputs of one layer: dict(hidden [B, T, D] bf16 (fp32 for
+    ``tiny``), wq [Hq*d, D] bf16, q_last [B, Hq, d] bf16) with D = Hq*d;
+    q_last is the model's last query (W_Q times the last hidden row, fp32,
+    rounded to bf16).  ``T`` overrides the token count (the visual/text
+    split keeps the workload's text share)."""
+    if isinstance(w, str):
+        w = WORKLOADS[w]
+    dev = torch.device(device)
+    T = w.T if T is None else int(T)
+    D = w.Hq * w.d
+    n_text = min(T, w.n_text * T // w.T) if w.n_text else 0
+    n_vis = T - n_text
+    g = _gen(dev, w.wid, layer, 7)
+    with torch.no_grad():
+        scale = torch.exp(0.5 * _randn((w.B, 1, D), g, dev))
+        m = _randn((w.B, LOWRANK_R, D), g, dev)
+        parts = []
+        if n_vis:
+            parts.append(_lowrank_rows((w.B,), n_vis, LOWRANK_R, LOWRANK_EPS, m, g, dev))
+        if n_text:
+            parts.append(math.sqrt(TEXT_VAR) * _randn((w.B, n_text, D), g, dev))
+        out = torch.cat(parts, dim=1) * scale
+        cols = torch.randperm(D, generator=g, device=dev)[:HIDDEN_OUTLIERS]
+        out[:, :, cols] *= HIDDEN_OUTLIER_SCALE
+        wq = _randn((w.Hq * w.d, D), g, dev) / math.sqrt(D)
+        dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+        hidden = out.to(dt).contiguous()
+        wq = wq.to(torch.bfloat16).contiguous()
+        # the model's own last query (the anchor's input), W_Q h_{T-1} in fp32
+        q_last = (hidden[:, -1].float() @ wq.float().t()).reshape(w.B, w.Hq, w.d)
+        return dict(hidden=hidden, wq=wq, q_last=q_last.to(torch.bfloat16).contiguous())
+
+
+def custom_hidden(B, T, D, Hq, d, dtype="bf16", seed=0, device="cpu", wq_kind="dense"):
+    """Free-shape hidden-state inputs: hidden [B, T, D] ~ per-feature scaled
+    N(0, 1) plus a per-feature mean, W_Q [Hq*d, D] bf16 and the last query
+    q_last [B, Hq, d] bf16.  wq_kind "dense": N(0, 1/D); "select": one
+    nonzero per row, +-1 or +-2 at a random feature (its products are exact
+    in every precision)."""
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) & 0x7FFFFFFF)
+    dev = torch.device(device)
+    with torch.no_grad():
+        scale = torch.exp(0.5 * _randn((B, 1, D), g, dev))
+        hidden = (_randn((B, T, D), g, dev) + _randn((B, 1, D), g, dev)) * scale
+        if wq_kind == "dense":
+            wq = _randn((Hq * d, D), g, dev) / math.sqrt(D)
+        else:
+            wq = torch.zeros((Hq * d, D), device=dev)
+            cols = torch.randint(0, D, (Hq * d,), generator=g, device=dev)
+            vals = torch.tensor([-2.0, -1.0, 1.0, 2.0], device=dev)[
+                torch.randint(0, 4, (Hq * d,), generator=g, device=dev)]
+            wq[torch.arange(Hq * d, device=dev), cols] = vals
+        dt = torch.float32 if dtype == "f32" else torch.bfloat16
+        hidden = hidden.to(dt).contiguous()
+        wq = wq.to(torch.bfloat16).contiguous()
+        q_last = (hidden[:, -1].float() @ wq.float().t()).reshape(B, Hq, d)
+        return dict(hidden=hidden, wq=wq, q_last=q_last.to(torch.bfloat16).contiguous())
 
 
 def custom_layer(B, Hq, Hkv, T, W, d, dtype="bf16", seed=0, device="cpu", key_scale=1.0,

@@ -188,3 +188,31 @@ def test_binding_refuses_host_tensors():
     q = torch.zeros((1, 4, 16, 64))
     with pytest.raises(ValueError):
         bd.build_proxies(q, bd.SelectionConfig(), T=1024, Hkv=1)
+
+
+def test_hidden_form_rejects(lib):
+    """Host validation of the hidden-state proxy calls (Sec. 3.2.1 Eqs. 4-6)."""
+    hs = bd.HShape(2, 300, 64)
+    need = lib.mmshiftkv_hidden_stats_workspace(ctypes.byref(hs))
+    assert need >= 2 * 2 * 64 * 16                  # two chunks of 256 tokens, (sum, sum sq) fp64
+    assert lib.mmshiftkv_hidden_stats_workspace(ctypes.byref(bd.HShape(1, 10, 12))) == 0   # D % 8
+    stats = lambda shape=hs, ddof=0, h=FAKE, dtype=1, sb=300 * 64, st=64, ws=FAKE, nbytes=need: \
+        lib.mmshiftkv_hidden_stats(ctypes.byref(shape), ddof, h, dtype, sb, st, FAKE, ws, nbytes, None)  # noqa: E731
+    assert stats(shape=bd.HShape(0, 300, 64)) == bd.MMSKV_EINVAL
+    assert stats(shape=bd.HShape(1, 1, 64), ddof=1) == bd.MMSKV_EINVAL     # T - ddof < 1
+    assert stats(ddof=2) == bd.MMSKV_EINVAL
+    assert stats(h=None) == bd.MMSKV_EINVAL
+    assert stats(dtype=5) == bd.MMSKV_EINVAL
+    assert stats(st=63) == bd.MMSKV_EINVAL                                 # rows not 16-byte aligned
+    assert stats(nbytes=need - 1) == bd.MMSKV_EWORKSPACE
+    assert stats(ws=ctypes.c_void_p(0x10010)) == bd.MMSKV_EWORKSPACE
+    prox = lambda prm, hp=FAKE: lib.mmshiftkv_hidden_proxies(ctypes.byref(hs), ctypes.byref(prm), FAKE, hp, None)  # noqa: E731
+    assert prox(_params(gamma=-1.0)) == bd.MMSKV_EINVAL
+    assert prox(_params(layer=-1)) == bd.MMSKV_EINVAL
+    assert prox(_params(), hp=None) == bd.MMSKV_EINVAL
+    proj = lambda P=512, Hq=4, d=64, out=FAKE, rope=(None, None): lib.mmshiftkv_project_proxies(  # noqa: E731
+        ctypes.byref(hs), P, Hq, d, FAKE, FAKE, rope[0], rope[1], out, None)
+    assert proj(d=96) == bd.MMSKV_EUNSUPPORTED
+    assert proj(P=0) == bd.MMSKV_EINVAL
+    assert proj(out=ctypes.c_void_p(0x10008)) == bd.MMSKV_EINVAL
+    assert proj(rope=(FAKE, None)) == bd.MMSKV_EINVAL
