@@ -304,13 +304,13 @@ int mmshiftkv_select_topk(const mmskv_shape* shape, const mmskv_params* params, 
     a.c_max = c_max;
     a.tau = params->tau;
     a.lambda = params->lambda;
-    // fixed-point scale 2^S with S = 62 - bitlen(rows per group), so a
+    // fixed-point unit 2^-S with S = 62 - bitlen(rows per group), so a
     // group's total (<= rows per group, plus rounding) stays below 2^63
     {
         const int rows_per_group = (params->P / params->G) * (shape->Hq / shape->Hkv);
         int bits = 0;
         while ((1 << bits) <= rows_per_group) ++bits;
-        a.fix_scale = ldexp(1.0, 62 - bits);
+        a.fix_shift = 62 - bits;
     }
     char* w = static_cast<char*>(workspace);
     a.theta = reinterpret_cast<uint32_t*>(w + l.theta_off);

@@ -50,7 +50,7 @@ struct SelectArgs {
     const int32_t* budgets;    // [B, Hkv] or null
     int B, Hkv, T, G, mode, keep_last, budget, c_max;
     double tau, lambda;
-    double fix_scale;          // 2^S: fixed-point scale of the tau sums
+    int fix_shift;             // S: tau sums count masses in units of 2^-S
     uint32_t* theta;           // [B, Hkv, G] cut mass (fp32 bits)
     int32_t* tcut;             // [B, Hkv, G] last admitted index among equals
     uint64_t* keys;            // [B, Hkv, T] score bits (fp64, non-negative)

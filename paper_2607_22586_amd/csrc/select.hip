@@ -3,19 +3,21 @@
 //
 // tau_cut   one workgroup per (b, c, group): a mass-weighted radix select on
 //           the fp32 bit patterns of the group masses (non-negative floats
-//           order like their bits; 11/11/10-bit digits) finds the cut mass
-//           theta and, among keys whose mass equals theta, the last admitted
-//           index, such that {mass > theta} u {mass == theta, index <= tcut}
-//           is the shortest (mass desc, index asc) prefix whose mass reaches
-//           tau * total.  Masses are summed as 2^S fixed-point integers, so
-//           every decision is independent of summation order.
-// vote      one thread per key: vote = #groups whose set holds the key;
+//           order like their bits; 11/11/9-bit digits below the sign bit)
+//           finds the cut mass theta and, among keys whose mass equals theta,
+//           the last admitted index, such that
+//           {mass > theta} u {mass == theta, index <= tcut} is the shortest
+//           (mass desc, index asc) prefix whose mass reaches tau * total.
+//           Masses are summed as integers in units of 2^-S (converted from
+//           the float bits exactly), so every decision is independent of
+//           summation order.
+// vote      one thread per 4 keys: vote = #groups whose set holds the key;
 //           score = vote + lambda*anchor (fp64) or the total mass.
 // topk      one workgroup per (b, c): radix select (11-bit digits, stopping
 //           early once a bucket is taken whole) of the (C-1)-th largest score
-//           key over [0, T-1) (or the C-th over [0, T)), then an index-ordered
-//           compaction writes the kept tokens in ascending order and appends
-//           token T-1.
+//           key over [0, T-1) (or the C-th over [0, T)), then an
+//           index-ordered compaction writes the kept tokens in ascending
+//           order and appends token T-1.
 #include <math.h>
 
 #include "common.hpp"
@@ -26,9 +28,20 @@ namespace {
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
+constexpr int kTauThreads = 512;                 // register-resident tau cut
+constexpr int kTauWaves = kTauThreads / kWave;
 
-__device__ __forceinline__ uint64_t to_fixed(float m, double scale) {
-    return static_cast<uint64_t>(static_cast<double>(m) * scale);
+// floor(m * 2^S) for the finite, non-negative float with bit pattern `bits`,
+// computed exactly from the significand and exponent (the product m * 2^S
+// stays below 2^63 for every mass the score pass can produce).
+__device__ __forceinline__ uint64_t fixed_of(uint32_t bits, int S) {
+    const uint32_t e = (bits >> 23) & 0xFFu;
+    const uint64_t man = static_cast<uint64_t>((bits & 0x7FFFFFu) | (e != 0 ? 0x800000u : 0u));
+    // value = man * 2^(e - 150) (normal) or man * 2^-149 (subnormal)
+    const int sh = (e != 0 ? static_cast<int>(e) : 1) - 150 + S;
+    if (sh >= 0) return man << sh;
+    if (sh <= -24) return 0ull;
+    return man >> (-sh);
 }
 
 // Adds (count 1, value f) of every active lane to bucket `digit`, combining
@@ -60,16 +73,18 @@ __device__ __forceinline__ void hist_add(bool active, uint32_t digit, uint64_t f
     }
 }
 
-// Block-wide exclusive prefix count of `flag` over the 1024 threads in
-// thread order; returns the prefix and writes the block total.
+// Block-wide exclusive prefix count of `flag` over the NT threads in thread
+// order; returns the prefix and writes the block total.
+template <int NT = kSelThreads>
 __device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* wtot, uint32_t& total) {
+    constexpr int kW = NT / kWave;
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     const uint64_t m = __ballot(flag);
     const uint32_t below = static_cast<uint32_t>(__popcll(m & ((1ull << lane) - 1ull)));
     if (lane == 0) wtot[wave] = static_cast<uint32_t>(__popcll(m));
     __syncthreads();
     uint32_t before = 0, tot = 0;
-    for (int w = 0; w < kSelWaves; ++w) {
+    for (int w = 0; w < kW; ++w) {
         const uint32_t x = wtot[w];
         before += (w < wave) ? x : 0u;
         tot += x;
@@ -79,10 +94,11 @@ __device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* wtot, 
     return before + below;
 }
 
-// Block-wide exclusive prefix sum of `v` over the 1024 threads in thread
+// Block-wide exclusive prefix sum of `v` over the NT threads in thread
 // order; also returns the block total.
-template <typename U>
+template <typename U, int NT = kSelThreads>
 __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
+    constexpr int kW = NT / kWave;
     const int lane = lane_id(), wave = static_cast<int>(threadIdx.x) / kWave;
     U x = v;
 #pragma unroll
@@ -98,7 +114,7 @@ __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
     __syncthreads();
     U before = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < kSelWaves; ++w) {
+    for (int w = 0; w < kW; ++w) {
         const U t = wtot[w];
         before += (w < wave) ? t : U(0);
         tot += t;
@@ -108,42 +124,57 @@ __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
     return before + x - v;
 }
 
-// Digits [0, 2048) visited in descending order, thread i covering digits
-// 2047-2i and 2046-2i: finds the digit whose bucket takes the running total
-// (from the top) to `need` (need >= 1, need <= total).  Returns, through
-// shared memory, the digit, `need` minus the total of higher buckets, and the
-// bucket's count.
-template <typename U>
+// Digits [0, 2048) visited in descending order, thread i of NT covering the
+// 2048/NT digits below 2048 - (2048/NT)*i: finds the digit whose bucket
+// takes the running total (from the top) to `need` (need >= 1, need <=
+// total).  Returns, through shared memory, the digit, `need` minus the total
+// of higher buckets, and the bucket's count.
+template <typename U, int NT = kSelThreads>
 __device__ __forceinline__ void descending_crossing(const U* val, const uint32_t* cnt, U need, U* wtot,
                                                     uint32_t* s_digit, U* s_rem, uint32_t* s_cnt) {
-    const int i = static_cast<int>(threadIdx.x);
-    const int d_hi = 2047 - 2 * i, d_lo = 2046 - 2 * i;
-    const U v_hi = val[d_hi], v_lo = val[d_lo];
+    constexpr int kPer = 2048 / NT;
+    const int top = 2047 - kPer * static_cast<int>(threadIdx.x);
+    U v[kPer];
+    U mine = 0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        v[k] = val[top - k];
+        mine += v[k];
+    }
     U total;
-    const U excl = block_excl_scan<U>(v_hi + v_lo, wtot, total);
-    if (excl < need && need <= excl + v_hi + v_lo) {
-        if (excl + v_hi >= need) {
-            *s_digit = d_hi;
-            *s_rem = need - excl;
-            *s_cnt = cnt[d_hi];
-        } else {
-            *s_digit = d_lo;
-            *s_rem = need - excl - v_hi;
-            *s_cnt = cnt[d_lo];
+    U excl = block_excl_scan<U, NT>(mine, wtot, total);
+    if (excl < need && need <= excl + mine) {
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            if (excl < need && need <= excl + v[k]) {
+                *s_digit = top - k;
+                *s_rem = need - excl;
+                *s_cnt = cnt[top - k];
+            }
+            excl += v[k];
         }
     }
     __syncthreads();
 }
 
+template <int NT = kSelThreads>
 __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long* scratch) {
+    constexpr int kW = NT / kWave;
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     v = wave_sum_u64(v);
     if (lane == 0) scratch[wave] = v;
     __syncthreads();
     uint64_t t = 0;
-    for (int w = 0; w < kSelWaves; ++w) t += scratch[w];
+    for (int w = 0; w < kW; ++w) t += scratch[w];
     __syncthreads();
     return t;
+}
+
+// tau-cut digits: bits 30..20, 19..9, 8..0 of the (sign-free) mass bits.
+__device__ __forceinline__ int tau_shift(int pass) { return pass == 0 ? 20 : pass == 1 ? 9 : 0; }
+__device__ __forceinline__ uint32_t tau_mask(int pass) { return pass == 0 ? 0u : pass == 1 ? 0xFFF00000u : 0xFFFFFE00u; }
+__device__ __forceinline__ uint32_t tau_digit(uint32_t bits, int pass) {
+    return (bits >> tau_shift(pass)) & (pass == 2 ? 0x1FFu : 0x7FFu);
 }
 
 // ---------------------------------------------------------------- tau cut
@@ -158,11 +189,12 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
 
     const int g = blockIdx.x, c = blockIdx.y, b = blockIdx.z;
     const int64_t hcg = (static_cast<int64_t>(b) * a.Hkv + c) * a.G + g;
-    const float* m = a.group_mass + hcg * a.T;
+    const uint32_t* m = reinterpret_cast<const uint32_t*>(a.group_mass) + hcg * a.T;
     const int tid = threadIdx.x;
+    const int S = a.fix_shift;
 
     uint64_t local = 0;
-    for (int t = tid; t < a.T; t += kSelThreads) local += to_fixed(m[t], a.fix_scale);
+    for (int t = tid; t < a.T; t += kSelThreads) local += fixed_of(m[t], S);
     const uint64_t total = block_sum_u64(local, wtot64);
     if (total == 0) {
         // every mass is below the fixed-point resolution: empty set
@@ -173,32 +205,26 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
     if (need < 1) need = 1;
     if (need > total) need = total;
 
-    // digits: bits 31..21, 20..10, 9..0 (the sign bit is 0)
-    const int shifts[3] = {21, 10, 0};
-    const uint32_t masks[3] = {0u, 0xFFE00000u, 0xFFFFFC00u};
     uint32_t prefix = 0;
     for (int pass = 0; pass < 3; ++pass) {
-        const int shift = shifts[pass];
-        const uint32_t mask = masks[pass];
+        const uint32_t mask = tau_mask(pass);
         for (int i = tid; i < 2048; i += kSelThreads) { cnt[i] = 0; sum[i] = 0; }
         __syncthreads();
-        for (int t = tid; t < a.T; t += kSelThreads) {
-            const float mv = m[t];
-            const uint32_t bits = __float_as_uint(mv);
-            if ((bits & mask) == prefix) {
-                const uint32_t dg = (bits >> shift) & 2047u;
-                atomicAdd(&cnt[dg], 1u);
-                atomicAdd(&sum[dg], static_cast<unsigned long long>(to_fixed(mv, a.fix_scale)));
-            }
+        // uniform trip count: hist_add needs every lane of the wave
+        for (int base = 0; base < a.T; base += kSelThreads) {
+            const int t = base + tid;
+            const uint32_t bits = t < a.T ? m[t] : 0u;
+            const bool in = t < a.T && (bits & mask) == prefix;
+            hist_add(in, tau_digit(bits, pass), in ? fixed_of(bits, S) : 0ull, cnt, sum);
         }
         __syncthreads();
         descending_crossing<unsigned long long>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
-        prefix |= s_digit << shift;
+        prefix |= s_digit << tau_shift(pass);
         need = s_rem;
     }
     // keys with mass == theta each carry f_theta; the first k_eq by index
     // enter the set (all of them when k_eq covers the bucket)
-    const uint64_t f_theta = to_fixed(__uint_as_float(prefix), a.fix_scale);
+    const uint64_t f_theta = fixed_of(prefix, S);
     const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
     if (k_eq >= s_cnt) {
         if (tid == 0) { a.theta[hcg] = prefix; a.tcut[hcg] = a.T; }
@@ -209,7 +235,7 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
     uint64_t seen = 0;
     for (int base = 0; base < a.T; base += kSelThreads) {
         const int t = base + tid;
-        const bool eq = t < a.T && __float_as_uint(m[t]) == prefix;
+        const bool eq = t < a.T && m[t] == prefix;
         uint32_t tot;
         const uint32_t before = block_excl_count(eq, wtot, tot);
         if (eq && seen + before + 1 == k_eq) s_tcut = t;
@@ -224,6 +250,12 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
 }
 
 // ---------------------------------------------------------------- vote + score
+// VEC consecutive keys per thread (VEC = 4 needs T % 4 == 0, so every group
+// row starts on a 16-byte boundary); the G group masses of a key are fetched
+// kVoteBatch groups at a time so their latencies overlap.
+constexpr int kVoteBatch = 8;
+
+template <int VEC>
 __global__ void __launch_bounds__(256) vote_score_kernel(SelectArgs a) {
     __shared__ uint32_t th[256];
     __shared__ int32_t tc[256];
@@ -237,29 +269,106 @@ __global__ void __launch_bounds__(256) vote_score_kernel(SelectArgs a) {
         }
     }
     __syncthreads();
-    const int t = blockIdx.x * 256 + threadIdx.x;
-    if (t >= a.T) return;
-    double score;
+    const int t0 = (static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x)) * VEC;
+    if (t0 >= a.T) return;
+    double score[VEC];
     if (vote_mode) {
-        int vote = 0;
-        const float* gm = a.group_mass + hc * a.G * static_cast<int64_t>(a.T) + t;
-        for (int g = 0; g < a.G; ++g) {
-            const uint32_t bits = __float_as_uint(gm[static_cast<int64_t>(g) * a.T]);
-            vote += (bits > th[g] || (bits == th[g] && t <= tc[g])) ? 1 : 0;
+        int vote[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) vote[e] = 0;
+        const uint32_t* gm = reinterpret_cast<const uint32_t*>(a.group_mass) + hc * a.G * static_cast<int64_t>(a.T) + t0;
+        for (int g0 = 0; g0 < a.G; g0 += kVoteBatch) {
+            uint32_t v[kVoteBatch][VEC];
+#pragma unroll
+            for (int j = 0; j < kVoteBatch; ++j) {
+                const int g = g0 + j;
+                if (VEC == 4) {
+                    u32x4 x = {0u, 0u, 0u, 0u};
+                    if (g < a.G) x = *reinterpret_cast<const u32x4*>(gm + static_cast<int64_t>(g) * a.T);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) v[j][e] = x[e];
+                } else {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e)
+                        v[j][e] = (g < a.G && t0 + e < a.T) ? gm[static_cast<int64_t>(g) * a.T + e] : 0u;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kVoteBatch; ++j) {
+                const int g = g0 + j;
+                if (g < a.G) {
+                    const uint32_t tg = th[g];
+                    const int cg = tc[g];
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e)
+                        vote[e] += (v[j][e] > tg || (v[j][e] == tg && t0 + e <= cg)) ? 1 : 0;
+                }
+            }
         }
-        score = static_cast<double>(vote) + a.lambda * static_cast<double>(a.anchor[hc * a.T + t]);
-        if (a.votes != nullptr) a.votes[hc * a.T + t] = static_cast<uint8_t>(vote);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            if (t0 + e < a.T) {
+                score[e] = static_cast<double>(vote[e]) + a.lambda * static_cast<double>(a.anchor[hc * a.T + t0 + e]);
+                if (a.votes != nullptr) a.votes[hc * a.T + t0 + e] = static_cast<uint8_t>(vote[e]);
+            }
+        }
     } else {
-        score = static_cast<double>(a.mass[hc * a.T + t]);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            if (t0 + e < a.T) score[e] = static_cast<double>(a.mass[hc * a.T + t0 + e]);
     }
-    a.keys[hc * a.T + t] = static_cast<uint64_t>(__double_as_longlong(score));
+#pragma unroll
+    for (int e = 0; e < VEC; ++e)
+        if (t0 + e < a.T) a.keys[hc * a.T + t0 + e] = static_cast<uint64_t>(__double_as_longlong(score[e]));
 }
 
 // ---------------------------------------------------------------- top-k
+// Radix search for the selection threshold over the 64-bit score keys of
+// the pool: 11-bit digits from the top (bits 63..53, ..., 9..0), stopping
+// once the crossing bucket is taken whole.  `each(f)` calls f(key, ok) with
+// the same trip count on every thread, ok marking the pool keys this thread
+// owns.  On return, the selected keys are {key > theta} plus the first k_eq
+// keys (by index) with key == theta.  Requires 1 <= want < pool size.
+struct TopkShared {
+    uint32_t cnt[2048];
+    uint32_t wtot[kSelWaves];
+    uint32_t s_digit, s_cnt, s_rem;
+};
+
+template <typename Each>
+__device__ __forceinline__ void topk_threshold(uint32_t want, Each each, TopkShared& sh, uint64_t& theta,
+                                               uint32_t& k_eq) {
+    const int tid = threadIdx.x;
+    uint64_t prefix = 0, mask = 0;
+    uint32_t need = want;
+    for (int pass = 0; pass < 6; ++pass) {
+        const int shift = pass == 5 ? 0 : 53 - 11 * pass;
+        for (int i = tid; i < 2048; i += kSelThreads) sh.cnt[i] = 0;
+        __syncthreads();
+        // plain LDS atomics: same-digit lanes of a wave serialise in the LDS
+        // unit, which is cheaper than combining them with wave operations
+        each([&](uint64_t kv, bool ok) {
+            if (ok && (kv & mask) == prefix) atomicAdd(&sh.cnt[static_cast<uint32_t>(kv >> shift) & 2047u], 1u);
+        });
+        __syncthreads();
+        descending_crossing<uint32_t>(sh.cnt, sh.cnt, need, sh.wtot, &sh.s_digit, &sh.s_rem, &sh.s_cnt);
+        prefix |= static_cast<uint64_t>(sh.s_digit) << shift;
+        mask |= (shift == 0 ? 0x1FFull : 0x7FFull) << shift;
+        need = sh.s_rem;
+        if (sh.s_cnt == need) {
+            // the whole bucket is taken: every key >= its lower bound (> 0,
+            // since the pool holds more keys than are wanted)
+            theta = prefix - 1;
+            k_eq = 0;
+            return;
+        }
+    }
+    theta = prefix;
+    k_eq = need;
+}
+
 __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
-    __shared__ uint32_t cnt[2048];
-    __shared__ uint32_t wtot[kSelWaves];
-    __shared__ uint32_t s_digit, s_cnt, s_rem;
+    __shared__ TopkShared sh;
 
     const int c = blockIdx.x, b = blockIdx.y;
     const int64_t hc = static_cast<int64_t>(b) * a.Hkv + c;
@@ -277,42 +386,15 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
     const uint32_t want = static_cast<uint32_t>(a.keep_last ? budget - 1 : budget);
     const uint64_t* key = a.keys + hc * a.T;
 
-    // selected: key > theta, or key == theta among the first k_eq by index
     uint64_t theta = 0;
     uint32_t k_eq = 0;
     if (want > 0) {
-        const int shifts[6] = {53, 42, 31, 20, 9, 0};
-        uint64_t prefix = 0, mask = 0;
-        uint32_t need = want;
-        bool settled = false;
-        for (int pass = 0; pass < 6 && !settled; ++pass) {
-            const int shift = shifts[pass];
-            for (int i = tid; i < 2048; i += kSelThreads) cnt[i] = 0;
-            __syncthreads();
+        topk_threshold(want, [&](auto&& f) {
             for (int base = 0; base < pool; base += kSelThreads) {
                 const int t = base + tid;
-                const bool in = t < pool;
-                const uint64_t kv = in ? key[t] : 0ull;
-                const bool cand = in && (kv & mask) == prefix;
-                hist_add(cand, static_cast<uint32_t>(kv >> shift) & 2047u, 0ull, cnt, nullptr);
+                f(t < pool ? key[t] : 0ull, t < pool);
             }
-            __syncthreads();
-            descending_crossing<uint32_t>(cnt, cnt, need, wtot, &s_digit, &s_rem, &s_cnt);
-            prefix |= static_cast<uint64_t>(s_digit) << shift;
-            mask |= (shift == 0 ? 0x1FFull : 0x7FFull) << shift;
-            need = s_rem;
-            if (s_cnt == need) {
-                // the whole bucket is taken: every key >= its lower bound
-                // (> 0, since the pool holds more keys than are wanted)
-                theta = prefix - 1;
-                k_eq = 0;
-                settled = true;
-            }
-        }
-        if (!settled) {
-            theta = prefix;
-            k_eq = need;
-        }
+        }, sh, theta, k_eq);
     }
     uint32_t eq_seen = 0, written = 0;
     for (int base = 0; base < pool; base += kSelThreads) {
@@ -322,10 +404,10 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
         const bool gt = in && want > 0 && kv > theta;
         const bool eq = in && want > 0 && k_eq > 0 && kv == theta;
         uint32_t eq_tot;
-        const uint32_t eq_before = block_excl_count(eq, wtot, eq_tot);
+        const uint32_t eq_before = block_excl_count(eq, sh.wtot, eq_tot);
         const bool sel = gt || (eq && eq_seen + eq_before < k_eq);
         uint32_t sel_tot;
-        const uint32_t pos = block_excl_count(sel, wtot, sel_tot);
+        const uint32_t pos = block_excl_count(sel, sh.wtot, sel_tot);
         if (sel && written + pos < want) out[written + pos] = t;
         eq_seen += eq_tot;
         written = min(written + sel_tot, want);
@@ -344,31 +426,43 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
 // is read from memory once and every index-ordered step (ties, compaction)
 // needs one block scan instead of a sweep.
 
-// tau cut of one (b, c, group); same result as tau_cut_kernel.
+// tau cut of one (b, c, group); same result as tau_cut_kernel.  512 threads
+// of at most 128 VGPRs, so two workgroups share a CU and a whole launch of
+// 512 workgroups is resident at once.
 template <int KPT>
-__global__ void __launch_bounds__(kSelThreads) tau_cut_reg_kernel(SelectArgs a) {
+__global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) {
     __shared__ uint32_t cnt[2048];
     __shared__ unsigned long long sum[2048];
-    __shared__ unsigned long long wtot64[kSelWaves];
-    __shared__ uint32_t wtot[kSelWaves];
+    __shared__ unsigned long long wtot64[kTauWaves];
+    __shared__ uint32_t wtot[kTauWaves];
     __shared__ uint32_t s_digit, s_cnt;
     __shared__ unsigned long long s_rem;
     __shared__ int32_t s_tcut;
 
     const int g = blockIdx.x, c = blockIdx.y, b = blockIdx.z;
     const int64_t hcg = (static_cast<int64_t>(b) * a.Hkv + c) * a.G + g;
-    const float* m = a.group_mass + hcg * a.T;
+    const uint32_t* m = reinterpret_cast<const uint32_t*>(a.group_mass) + hcg * a.T;
     const int tid = threadIdx.x;
     const int t0 = tid * KPT;
+    const int S = a.fix_shift;
 
-    float mv[KPT];
+    // masses (bits), held for all passes (their fixed-point values are
+    // recomputed where needed); keys past T read as mass 0
+    uint32_t mb[KPT];
+    if (t0 + KPT <= a.T && (reinterpret_cast<uintptr_t>(m + t0) & 15u) == 0) {
+#pragma unroll
+        for (int j = 0; j < KPT; j += 4) {
+            const u32x4 x = *reinterpret_cast<const u32x4*>(m + t0 + j);
+            mb[j] = x[0]; mb[j + 1] = x[1]; mb[j + 2] = x[2]; mb[j + 3] = x[3];
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) mb[j] = (t0 + j < a.T) ? m[t0 + j] : 0u;
+    }
     uint64_t local = 0;
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-        mv[j] = (t0 + j < a.T) ? m[t0 + j] : 0.f;
-        local += to_fixed(mv[j], a.fix_scale);
-    }
-    const uint64_t total = block_sum_u64(local, wtot64);
+    for (int j = 0; j < KPT; ++j) local += fixed_of(mb[j], S);
+    const uint64_t total = block_sum_u64<kTauThreads>(local, wtot64);
     if (total == 0) {
         if (tid == 0) { a.theta[hcg] = 0xFFFFFFFFu; a.tcut[hcg] = -1; }
         return;
@@ -377,29 +471,29 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_reg_kernel(SelectArgs a) 
     if (need < 1) need = 1;
     if (need > total) need = total;
 
-    const int shifts[3] = {21, 10, 0};
-    const uint32_t masks[3] = {0u, 0xFFE00000u, 0xFFFFFC00u};
     uint32_t prefix = 0;
+#pragma nounroll
     for (int pass = 0; pass < 3; ++pass) {
-        const int shift = shifts[pass];
-        const uint32_t mask = masks[pass];
-        for (int i = tid; i < 2048; i += kSelThreads) { cnt[i] = 0; sum[i] = 0; }
+        const uint32_t mask = tau_mask(pass);
+        for (int i = tid; i < 2048; i += kTauThreads) { cnt[i] = 0; sum[i] = 0; }
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
-            const uint32_t bits = __float_as_uint(mv[j]);
-            if (t0 + j < a.T && (bits & mask) == prefix) {
-                const uint32_t dg = (bits >> shift) & 2047u;
+            // opaque inside the pass loop, so the fixed-point values are not
+            // hoisted out of it and kept live
+            asm volatile("" : "+v"(mb[j]));
+            if (t0 + j < a.T && (mb[j] & mask) == prefix) {
+                const uint32_t dg = tau_digit(mb[j], pass);
                 atomicAdd(&cnt[dg], 1u);
-                atomicAdd(&sum[dg], static_cast<unsigned long long>(to_fixed(mv[j], a.fix_scale)));
+                atomicAdd(&sum[dg], static_cast<unsigned long long>(fixed_of(mb[j], S)));
             }
         }
         __syncthreads();
-        descending_crossing<unsigned long long>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
-        prefix |= s_digit << shift;
+        descending_crossing<unsigned long long, kTauThreads>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
+        prefix |= s_digit << tau_shift(pass);
         need = s_rem;
     }
-    const uint64_t f_theta = to_fixed(__uint_as_float(prefix), a.fix_scale);
+    const uint64_t f_theta = fixed_of(prefix, S);
     const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
     if (k_eq >= s_cnt) {
         if (tid == 0) { a.theta[hcg] = prefix; a.tcut[hcg] = a.T; }
@@ -408,14 +502,14 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_reg_kernel(SelectArgs a) 
     // the k_eq-th key (by index) whose mass equals theta
     uint32_t n_eq = 0;
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) n_eq += (t0 + j < a.T && __float_as_uint(mv[j]) == prefix) ? 1u : 0u;
+    for (int j = 0; j < KPT; ++j) n_eq += (t0 + j < a.T && mb[j] == prefix) ? 1u : 0u;
     uint32_t eq_total;
-    const uint32_t eq_before = block_excl_scan<uint32_t>(n_eq, wtot, eq_total);
+    const uint32_t eq_before = block_excl_scan<uint32_t, kTauThreads>(n_eq, wtot, eq_total);
     if (eq_before < k_eq && k_eq <= eq_before + n_eq) {
         uint32_t seen = eq_before;
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
-            if (t0 + j < a.T && __float_as_uint(mv[j]) == prefix) {
+            if (t0 + j < a.T && mb[j] == prefix) {
                 if (++seen == k_eq) s_tcut = t0 + j;
             }
         }
@@ -430,9 +524,7 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_reg_kernel(SelectArgs a) 
 // Budgeted selection of one (b, c); same result as topk_kernel.
 template <int KPT>
 __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
-    __shared__ uint32_t cnt[2048];
-    __shared__ uint32_t wtot[kSelWaves];
-    __shared__ uint32_t s_digit, s_cnt, s_rem;
+    __shared__ TopkShared sh;
 
     const int c = blockIdx.x, b = blockIdx.y;
     const int64_t hc = static_cast<int64_t>(b) * a.Hkv + c;
@@ -457,41 +549,17 @@ __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
     uint64_t theta = 0;
     uint32_t k_eq = 0;
     if (want > 0) {
-        const int shifts[6] = {53, 42, 31, 20, 9, 0};
-        uint64_t prefix = 0, mask = 0;
-        uint32_t need = want;
-        bool settled = false;
-        for (int pass = 0; pass < 6 && !settled; ++pass) {
-            const int shift = shifts[pass];
-            for (int i = tid; i < 2048; i += kSelThreads) cnt[i] = 0;
-            __syncthreads();
+        topk_threshold(want, [&](auto&& f) {
 #pragma unroll
-            for (int j = 0; j < KPT; ++j) {
-                const bool cand = t0 + j < pool && (kv[j] & mask) == prefix;
-                hist_add(cand, static_cast<uint32_t>(kv[j] >> shift) & 2047u, 0ull, cnt, nullptr);
-            }
-            __syncthreads();
-            descending_crossing<uint32_t>(cnt, cnt, need, wtot, &s_digit, &s_rem, &s_cnt);
-            prefix |= static_cast<uint64_t>(s_digit) << shift;
-            mask |= (shift == 0 ? 0x1FFull : 0x7FFull) << shift;
-            need = s_rem;
-            if (s_cnt == need) {
-                theta = prefix - 1;
-                k_eq = 0;
-                settled = true;
-            }
-        }
-        if (!settled) {
-            theta = prefix;
-            k_eq = need;
-        }
+            for (int j = 0; j < KPT; ++j) f(kv[j], t0 + j < pool);
+        }, sh, theta, k_eq);
     }
     // index-ordered compaction: keys > theta, then the first k_eq equal keys
     uint32_t n_eq = 0;
 #pragma unroll
     for (int j = 0; j < KPT; ++j) n_eq += (want > 0 && k_eq > 0 && t0 + j < pool && kv[j] == theta) ? 1u : 0u;
     uint32_t eq_total;
-    uint32_t eq_seen = block_excl_scan<uint32_t>(n_eq, wtot, eq_total);
+    uint32_t eq_seen = block_excl_scan<uint32_t>(n_eq, sh.wtot, eq_total);
     uint32_t sel_mask = 0, n_sel = 0;
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
@@ -505,7 +573,7 @@ __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
         }
     }
     uint32_t sel_total;
-    uint32_t pos = block_excl_scan<uint32_t>(n_sel, wtot, sel_total);
+    uint32_t pos = block_excl_scan<uint32_t>(n_sel, sh.wtot, sel_total);
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
         if ((sel_mask >> j) & 1u) {
@@ -525,23 +593,30 @@ __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-    // register-resident kernels while a row fits in 16 (tau cut) or 32
-    // (top-k) elements per thread
+    // register-resident kernels while a row fits in 32 elements per thread
+    // (512 threads for the tau cut, 1024 for the top-k)
     const int per = (a.T + kSelThreads - 1) / kSelThreads;
     const int kpt = per <= 4 ? 4 : per <= 8 ? 8 : per <= 16 ? 16 : per <= 32 ? 32 : 0;
     if (a.mode == 0) {
         dim3 g1(a.G, a.Hkv, a.B);
-        switch (kpt) {
-            case 4: hipLaunchKernelGGL(tau_cut_reg_kernel<4>, g1, dim3(kSelThreads), 0, s, a); break;
-            case 8: hipLaunchKernelGGL(tau_cut_reg_kernel<8>, g1, dim3(kSelThreads), 0, s, a); break;
-            case 16: hipLaunchKernelGGL(tau_cut_reg_kernel<16>, g1, dim3(kSelThreads), 0, s, a); break;
+        const int tper = (a.T + kTauThreads - 1) / kTauThreads;
+        const int tkpt = tper <= 8 ? 8 : tper <= 16 ? 16 : tper <= 32 ? 32 : 0;
+        switch (tkpt) {
+            case 8: hipLaunchKernelGGL(tau_cut_reg_kernel<8>, g1, dim3(kTauThreads), 0, s, a); break;
+            case 16: hipLaunchKernelGGL(tau_cut_reg_kernel<16>, g1, dim3(kTauThreads), 0, s, a); break;
+            case 32: hipLaunchKernelGGL(tau_cut_reg_kernel<32>, g1, dim3(kTauThreads), 0, s, a); break;
             default: hipLaunchKernelGGL(tau_cut_kernel, g1, dim3(kSelThreads), 0, s, a); break;
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    dim3 g2((a.T + 255) / 256, a.Hkv, a.B);
-    hipLaunchKernelGGL(vote_score_kernel, g2, dim3(256), 0, s, a);
+    if ((a.T & 3) == 0 && (reinterpret_cast<uintptr_t>(a.group_mass) & 15u) == 0) {
+        dim3 g2((a.T / 4 + 255) / 256, a.Hkv, a.B);
+        hipLaunchKernelGGL(vote_score_kernel<4>, g2, dim3(256), 0, s, a);
+    } else {
+        dim3 g2((a.T + 255) / 256, a.Hkv, a.B);
+        hipLaunchKernelGGL(vote_score_kernel<1>, g2, dim3(256), 0, s, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g3(a.Hkv, a.B);
