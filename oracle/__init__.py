@@ -84,6 +84,8 @@ def _load():
     lib.oracle_hidden_proxies.argtypes = [i32, i32, i32, f64, u64, i32, i32, P, P]
     lib.oracle_hidden_proxies.restype = i32
     lib.oracle_project_proxies.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, P, P]
+    lib.oracle_query_scale.argtypes = [i32]
+    lib.oracle_query_scale.restype = f64
     lib.oracle_project_proxies.restype = i32
     _lib = lib
     return lib
@@ -127,6 +129,11 @@ def normal4(seed: int, b: int, layer: int, h: int, i: int, jq: int) -> np.ndarra
     z = np.zeros(4, dtype=np.float64)
     _load().oracle_normal4(int(seed), b, layer, h, i, jq, _ptr(z))
     return z
+
+
+def query_scale(d: int) -> float:
+    """log2(e)/sqrt(d): the softmax scale the proxies and anchor queries carry."""
+    return float(_load().oracle_query_scale(int(d)))
 
 
 def f32_to_bf16(x: np.ndarray) -> np.ndarray:

@@ -22,11 +22,18 @@
  *   - Noise z is independent per (batch, layer, query head, proxy, dim).
  *   - Optional rotary embedding uses caller tables (rotate-half pairing j,
  *     j+d/2) for one synthetic future position (Sec. 3.2.1, last paragraph).
- *   - Proxies are rounded fp64 -> fp32 -> bf16 (round to nearest even);
- *     scoring keys are rounded fp32 -> bf16 the same way; the logits are then
- *     computed in fp64 on those bf16 values (mixed-precision inference,
- *     Sec. 4.1 "Implementation and Hyperparameters").
- *   - Softmax over all T prompt keys, scale 1/sqrt(head_dim) (Sec. 3.2.2 Eq. 7).
+ *   - The softmax scale of Sec. 3.2.2 Eq. 7, 1/sqrt(head_dim), is carried by
+ *     the queries: proxies are multiplied by c = log2(e)/sqrt(head_dim) in
+ *     fp64 and then rounded fp64 -> fp32 -> bf16 (round to nearest even), as
+ *     attention implementations scale queries before the low-precision
+ *     product; the anchor query is scaled the same way (fp64 product of its
+ *     bf16 value and c, then fp32, then bf16).  Scoring keys are rounded
+ *     fp32 -> bf16 the same way.  The logits q~ . k are then computed in fp64
+ *     on those bf16 values (mixed-precision inference, Sec. 4.1
+ *     "Implementation and Hyperparameters") and are base-2 logits: the
+ *     softmax is 2^(s - L) with L = log2 sum_t 2^(s_t), which equals
+ *     exp(q.k/sqrt(d) - lse) up to the bf16 rounding of the scaled queries.
+ *   - Softmax over all T prompt keys (Sec. 3.2.2 Eq. 7).
  *   - Groups are contiguous proxy blocks I_g = {g*P/G .. (g+1)*P/G - 1}
  *     (Sec. 3.2.2 Eq. 8 leaves the partition open).
  *   - GQA: the masses of the query heads that share a KV head are summed
@@ -221,6 +228,12 @@ static double load_key_bf16(const void *base, int dtype, int64_t off)
     return oracle_bf16_to_f64(((const uint16_t *)base)[off]);
 }
 
+/* Softmax scale carried by the queries: log2(e) / sqrt(d), fp64. */
+double oracle_query_scale(int d)
+{
+    return 1.4426950408889634074 / sqrt((double)d);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Step 1 -- proxies (Sec. 3.2.1 Eqs. 4-5, Appendix A.4 Eq. 15).             */
 /* ------------------------------------------------------------------------ */
@@ -230,7 +243,8 @@ static double load_key_bf16(const void *base, int dtype, int64_t off)
  *            position, or NULL (no rotary embedding)
  * rope_cos_l / rope_sin_l: [d/2] fp32 tables for the last query's position
  *            (used for the anchor query), or NULL
- * proxies    [B, Hq, P, d] bf16 out;  q_last [B, Hq, d] bf16 out
+ * proxies    [B, Hq, P, d] bf16 out (x times log2(e)/sqrt(d), rounded)
+ * q_last     [B, Hq, d] bf16 out (the last window query, not scaled)
  * stats      [B, Hq, 2, d] fp64 out (mu, sigma), may be NULL
  * returns 0, or -1 on invalid arguments
  */
@@ -249,6 +263,7 @@ int oracle_build_proxies_at(int B, int Hq, int W, int d, int P, double gamma, in
     int use_rope = (rope_cos_f != NULL && rope_sin_f != NULL);
     int use_rope_last = (rope_cos_l != NULL && rope_sin_l != NULL);
     int half = d / 2;
+    double qs = oracle_query_scale(d);
 
 #pragma omp parallel for collapse(2) schedule(static)
     for (int b = 0; b < B; ++b) {
@@ -299,12 +314,15 @@ int oracle_build_proxies_at(int B, int Hq, int W, int d, int P, double gamma, in
                         double a0 = x[j] * c, a1 = x[j + half] * s;
                         double b0 = x[j + half] * c, b1 = x[j] * s;
                         double lo = a0 - a1, hi = b0 + b1;
-                        out[j] = oracle_f32_to_bf16((float)lo);
-                        out[j + half] = oracle_f32_to_bf16((float)hi);
+                        double slo = lo * qs, shi = hi * qs;
+                        out[j] = oracle_f32_to_bf16((float)slo);
+                        out[j + half] = oracle_f32_to_bf16((float)shi);
                     }
                 } else {
-                    for (int j = 0; j < d; ++j)
-                        out[j] = oracle_f32_to_bf16((float)x[j]);
+                    for (int j = 0; j < d; ++j) {
+                        double sx = x[j] * qs;
+                        out[j] = oracle_f32_to_bf16((float)sx);
+                    }
                 }
             }
             /* anchor query: the last window query of this head */
@@ -420,9 +438,10 @@ int oracle_hidden_proxies(int B, int D, int P, double gamma, uint64_t seed, int 
  * Query proxies (Eq. 6): q[b, h, i, e] = sum_k H~[b, i, k] * W_Q[h*d + e, k]
  * over the bf16 values, summed in k order in fp64, then the optional rotary
  * placement (rotate-half pairs e, e + d/2, caller tables for one future
- * position), fp64 -> fp32 -> bf16.  hp [B, P, D]; wq [Hq*d, D] bf16;
+ * position), times the query scale log2(e)/sqrt(d) in fp64, then
+ * fp64 -> fp32 -> bf16.  hp [B, P, D]; wq [Hq*d, D] bf16;
  * proxies [B, Hq, P, d] bf16; pre [B, Hq, P, d] fp64 values before the
- * rounding, or NULL.
+ * rounding (scaled), or NULL.
  */
 int oracle_project_proxies(int B, int P, int D, int Hq, int d, const uint16_t *hp, const uint16_t *wq,
                            const float *rope_cos, const float *rope_sin, uint16_t *proxies, double *pre)
@@ -431,6 +450,7 @@ int oracle_project_proxies(int B, int P, int D, int Hq, int d, const uint16_t *h
         return -1;
     int use_rope = (rope_cos != NULL && rope_sin != NULL);
     int half = d / 2;
+    double qs = oracle_query_scale(d);
 #pragma omp parallel for collapse(3) schedule(static)
     for (int b = 0; b < B; ++b) {
         for (int h = 0; h < Hq; ++h) {
@@ -453,16 +473,18 @@ int oracle_project_proxies(int B, int P, int D, int Hq, int d, const uint16_t *h
                         double a0 = x[e] * c, a1 = x[e + half] * s;
                         double b0 = x[e + half] * c, b1 = x[e] * s;
                         double lo = a0 - a1, hi = b0 + b1;
-                        proxies[o + e] = oracle_f32_to_bf16((float)lo);
-                        proxies[o + e + half] = oracle_f32_to_bf16((float)hi);
+                        double slo = lo * qs, shi = hi * qs;
+                        proxies[o + e] = oracle_f32_to_bf16((float)slo);
+                        proxies[o + e + half] = oracle_f32_to_bf16((float)shi);
                         if (pre) {
-                            pre[o + e] = lo;
-                            pre[o + e + half] = hi;
+                            pre[o + e] = slo;
+                            pre[o + e + half] = shi;
                         }
                     } else {
-                        proxies[o + e] = oracle_f32_to_bf16((float)x[e]);
+                        double sx = x[e] * qs;
+                        proxies[o + e] = oracle_f32_to_bf16((float)sx);
                         if (pre)
-                            pre[o + e] = x[e];
+                            pre[o + e] = sx;
                     }
                 }
                 free(x);
@@ -488,11 +510,12 @@ int oracle_build_proxies(int B, int Hq, int W, int d, int P, double gamma, int d
 /* Eq. 11 for the anchor; Appendix B for the GQA aggregation).               */
 /* ------------------------------------------------------------------------ */
 
-/* softmax over t of q . k_t / sqrt(d) for one bf16 query row; writes p[T]. */
+/* softmax over t for one scaled bf16 query row q~: base-2 logits
+ * s_t = q~ . k_t (fp64 on the bf16 values), p_t = 2^(s_t - L) with
+ * L = log2 sum_t 2^(s_t); writes p[T]. */
 static void softmax_row(const uint16_t *q, const void *k, int kdtype, int64_t kbase, int T,
                         int d, double *logit, double *p)
 {
-    double sqrt_d = sqrt((double)d);
     double mx = -INFINITY;
     for (int t = 0; t < T; ++t) {
         double dot = 0.0;
@@ -500,20 +523,32 @@ static void softmax_row(const uint16_t *q, const void *k, int kdtype, int64_t kb
             double prod = oracle_bf16_to_f64(q[j]) * load_key_bf16(k, kdtype, kbase + (int64_t)t * d + j);
             dot = dot + prod;
         }
-        logit[t] = dot / sqrt_d;
+        logit[t] = dot;
         if (logit[t] > mx)
             mx = logit[t];
     }
     double sum = 0.0;
     for (int t = 0; t < T; ++t)
-        sum = sum + exp(logit[t] - mx);
-    double lse = mx + log(sum);
+        sum = sum + exp2(logit[t] - mx);
+    double lse2 = mx + log2(sum);
     for (int t = 0; t < T; ++t)
-        p[t] = exp(logit[t] - lse);
+        p[t] = exp2(logit[t] - lse2);
+}
+
+/* The anchor query scaled like the proxies: fp64 product of its bf16 value
+ * and log2(e)/sqrt(d), then fp32, then bf16. */
+static void scale_query(const uint16_t *q, int d, uint16_t *out)
+{
+    double qs = oracle_query_scale(d);
+    for (int j = 0; j < d; ++j) {
+        double v = oracle_bf16_to_f64(q[j]) * qs;
+        out[j] = oracle_f32_to_bf16((float)v);
+    }
 }
 
 /*
- * proxies  [B, Hq, P, d] bf16;  q_last [B, Hq, d] bf16
+ * proxies  [B, Hq, P, d] bf16, scaled by log2(e)/sqrt(d) (as step 1 makes them)
+ * q_last   [B, Hq, d] bf16, not scaled (the anchor queries)
  * k        [B, Hkv, T, d] contiguous, dtype 0 (fp32, rounded to bf16) / 1
  * group_mass [B, Hkv, G, T] fp64 out (may be NULL)
  * mass       [B, Hkv, T] fp64 out;  anchor [B, Hkv, T] fp64 out
@@ -566,6 +601,7 @@ int oracle_score(int B, int Hq, int Hkv, int T, int d, int P, int G,
         for (int c = 0; c < Hkv; ++c) {
             double *logit = (double *)malloc(sizeof(double) * (size_t)T);
             double *p = (double *)malloc(sizeof(double) * (size_t)T);
+            uint16_t *qa = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)d);
             int64_t kbase = ((int64_t)b * Hkv + c) * (int64_t)T * d;
             double *ms = mass + ((int64_t)b * Hkv + c) * T;
             double *an = anchor + ((int64_t)b * Hkv + c) * T;
@@ -578,8 +614,8 @@ int oracle_score(int B, int Hq, int Hkv, int T, int d, int P, int G,
             }
             for (int hl = 0; hl < Gh; ++hl) {
                 int h = c * Gh + hl;
-                const uint16_t *q = q_last + ((int64_t)b * Hq + h) * d;
-                softmax_row(q, k, kdtype, kbase, T, d, logit, p);
+                scale_query(q_last + ((int64_t)b * Hq + h) * d, d, qa);
+                softmax_row(qa, k, kdtype, kbase, T, d, logit, p);
                 for (int t = 0; t < T; ++t)
                     an[t] = an[t] + p[t];
             }
@@ -587,6 +623,7 @@ int oracle_score(int B, int Hq, int Hkv, int T, int d, int P, int G,
                 an[t] = an[t] / (double)Gh;
             free(logit);
             free(p);
+            free(qa);
         }
     }
     free(gm_own);

@@ -109,15 +109,16 @@ def test_projection_matches_float64_matmul(oracle_lib):
     out, pre = oracle_lib.project_proxies(hp, wq, Hq, with_pre=True)
     x = brute.bits_to_f64(hp)
     w = brute.bits_to_f64(wq).reshape(Hq, d, D)
-    ref = np.einsum("bpk,hek->bhpe", x, w)
+    ref = np.einsum("bpk,hek->bhpe", x, w) * brute.qscale(d)
     np.testing.assert_allclose(pre, ref, rtol=1e-12, atol=1e-14)
     assert np.array_equal(out, bf16_bits(pre.astype(np.float32)))
 
 
 def test_projection_selection_matrix_and_rope(oracle_lib):
-    """A one-hot W_Q copies hidden features into the heads exactly; identity
-    rotary tables change nothing and general tables rotate (e, e + d/2) as
-    the complex product (x_e + i x_{e+d/2}) (cos + i sin)."""
+    """A one-hot W_Q copies hidden features into the heads (times the query
+    scale log2(e)/sqrt(d)); identity rotary tables change nothing and
+    general tables rotate (e, e + d/2) as the complex product
+    (x_e + i x_{e+d/2}) (cos + i sin)."""
     rng = np.random.default_rng(6)
     B, P, D, Hq, d = 1, 4, 16, 2, 8
     hp = bf16_bits(rng.standard_normal((B, P, D)))
@@ -126,22 +127,24 @@ def test_projection_selection_matrix_and_rope(oracle_lib):
     w[np.arange(Hq * d), sel] = 1.0
     wq = bf16_bits(w)
     out = oracle_lib.project_proxies(hp, wq, Hq)
-    assert np.array_equal(out, hp[:, None, :, sel].reshape(B, P, Hq, d).transpose(0, 2, 1, 3))
+    copied = brute.bits_to_f64(hp[:, None, :, sel].reshape(B, P, Hq, d).transpose(0, 2, 1, 3))
+    assert np.array_equal(out, bf16_bits((copied * brute.qscale(d)).astype(np.float32)))
     ident = (np.ones(d // 2, np.float32), np.zeros(d // 2, np.float32))
     assert np.array_equal(oracle_lib.project_proxies(hp, wq, Hq, rope=ident), out)
     ang = rng.uniform(-3, 3, d // 2).astype(np.float32)
     rope = (np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32))
     _, pre = oracle_lib.project_proxies(hp, wq, Hq, rope=rope, with_pre=True)
-    x = brute.bits_to_f64(out)
+    x = copied * brute.qscale(d)
     zc = (x[..., : d // 2] + 1j * x[..., d // 2:]) * (rope[0].astype(np.float64) + 1j * rope[1].astype(np.float64))
     np.testing.assert_allclose(pre[..., : d // 2], zc.real, rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(pre[..., d // 2:], zc.imag, rtol=1e-12, atol=1e-14)
 
 
 def test_hidden_gamma_zero_path_is_single_query_attention(oracle_lib):
-    """gamma = 0: every proxy of head h is W_Q^(h) bf16(mu); the group mass of
-    every group is then g * sum_h softmax(q_h k / sqrt(d)) (Eq. 7-8 closed
-    form), checked against scipy's softmax."""
+    """gamma = 0: every proxy of head h is W_Q^(h) bf16(mu) (scaled by
+    log2(e)/sqrt(d)); the group mass of every group is then
+    g * sum_h softmax(ln(2) q~_h k) (Eq. 7-8 closed form), checked against
+    scipy's softmax."""
     from scipy.special import softmax
     rng = np.random.default_rng(8)
     B, T, D, Hq, Hkv, d, P, G = 1, 50, 32, 2, 1, 8, 16, 1
@@ -157,5 +160,5 @@ def test_hidden_gamma_zero_path_is_single_query_attention(oracle_lib):
     expect = np.zeros(T)
     for hh in range(Hq):
         qv = brute.bits_to_f64(prox[0, hh, 0])
-        expect += softmax(kq @ qv / math.sqrt(d))
+        expect += softmax(kq @ qv * math.log(2.0))
     np.testing.assert_allclose(gm[0, 0, 0], P * expect, rtol=1e-12)

@@ -50,14 +50,24 @@ def test_bf16_rounding_matches_torch(oracle_lib):
     assert np.array_equal(oracle_lib.f32_to_bf16(x), bf16_bits(x))
 
 
+def test_query_scale_constant(oracle_lib):
+    """The softmax scale carried by the queries is log2(e)/sqrt(d): squared,
+    times d ln(2)^2, it is one; it matches an independent evaluation."""
+    for d in (8, 16, 64, 128, 256):
+        c = oracle_lib.query_scale(d)
+        assert abs(c * c * d * math.log(2.0) ** 2 - 1.0) < 1e-15
+        assert abs(c - brute.qscale(d)) <= 2.0 ** -52 * c
+
+
 def test_proxy_law_mean_and_gamma_scaling(oracle_lib):
     """Eq. 5: proxies ~ N(mu, diag((gamma sigma)^2)); gamma multiplies sigma.
     A centring mistake (0 instead of mu) or gamma applied to the variance
-    (sqrt(gamma) in std) would move these moments far outside the bands."""
+    (sqrt(gamma) in std) would move these moments far outside the bands.
+    (The stored proxies carry the softmax scale log2(e)/sqrt(d).)"""
     q, _ = rand_inputs(1, 2, 1, 4, 32, 16, 5, qscale=3.0)
     P, gamma = 4096, 2.5
     prox, _, st = oracle_lib.build_proxies(q, P, gamma, seed=11)
-    x = brute.bits_to_f64(prox)                            # [1, 2, P, d]
+    x = brute.bits_to_f64(prox) / brute.qscale(16)         # [1, 2, P, d]
     mu, sg = st[:, :, 0][:, :, None, :], st[:, :, 1][:, :, None, :]
     zhat = (x - mu) / (gamma * sg)
     n = P
@@ -66,15 +76,16 @@ def test_proxy_law_mean_and_gamma_scaling(oracle_lib):
 
 
 def test_proxy_composition_rounding(oracle_lib):
-    """Eq. 5 with the generator's z: proxy = bf16(fp32(mu + (gamma*sigma)*z)),
-    the two roundings done by numpy/torch library conversions."""
+    """Eq. 5 with the generator's z: proxy = bf16(fp32((mu + (gamma*sigma)*z) * c)),
+    c = log2(e)/sqrt(d), the two roundings done by numpy/torch library
+    conversions."""
     q, _ = rand_inputs(1, 2, 1, 4, 8, 8, 9)
     P, gamma, seed, layer = 6, 10.0, 77, 3
     prox, _, st = oracle_lib.build_proxies(q, P, gamma, seed=seed, layer=layer)
     for h in range(2):
         for i in range(P):
             z = np.concatenate([oracle_lib.normal4(seed, 0, layer, h, i, jq) for jq in range(2)])
-            x = st[0, h, 0] + (gamma * st[0, h, 1]) * z
+            x = (st[0, h, 0] + (gamma * st[0, h, 1]) * z) * brute.qscale(8)
             assert np.array_equal(prox[0, h, i], bf16_bits(x.astype(np.float32)))
 
 
@@ -82,16 +93,18 @@ def test_gamma_zero_proxies_are_the_mean(oracle_lib):
     q, _ = rand_inputs(1, 3, 1, 4, 9, 16, 2)
     prox, _, st = oracle_lib.build_proxies(q, 5, 0.0, seed=3)
     for h in range(3):
-        want = bf16_bits(st[0, h, 0].astype(np.float32))
+        want = bf16_bits((st[0, h, 0] * brute.qscale(16)).astype(np.float32))
         assert all(np.array_equal(prox[0, h, i], want) for i in range(5))
 
 
 def test_single_window_query_collapses_to_last_query(oracle_lib):
-    """W=1 gives sigma=0 (ddof=0): every proxy equals the last query."""
+    """W=1 gives sigma=0 (ddof=0): every proxy equals the (scaled) last
+    query; the anchor query itself is returned unscaled."""
     q, _ = rand_inputs(2, 2, 1, 4, 1, 16, 4)
     prox, ql, st = oracle_lib.build_proxies(q, 7, 10.0, seed=5)
     assert np.all(st[:, :, 1] == 0.0)
-    assert np.array_equal(prox, np.broadcast_to(ql[:, :, None, :], prox.shape))
+    want = bf16_bits((q[:, :, 0, :].astype(np.float64) * brute.qscale(16)).astype(np.float32))
+    assert np.array_equal(prox, np.broadcast_to(want[:, :, None, :], prox.shape))
     assert np.array_equal(ql, bf16_bits(q[:, :, 0, :]))
 
 
@@ -112,7 +125,7 @@ def test_rope_identity_and_complex_rotation(oracle_lib):
     for h in range(2):
         mu = st[0, h, 0]
         zc = (mu[: d // 2] + 1j * mu[d // 2:]) * (cos.astype(np.float64) + 1j * sin.astype(np.float64))
-        want = bf16_bits(np.concatenate([zc.real, zc.imag]).astype(np.float32))
+        want = bf16_bits((np.concatenate([zc.real, zc.imag]) * brute.qscale(d)).astype(np.float32))
         got = prox[0, h, 0]
         # identical except possibly a one-ulp bf16 flip where the complex
         # product rounds differently from the two-product form
@@ -144,7 +157,9 @@ def test_normalisation_invariants(oracle_lib):
 def test_gamma_zero_is_single_query_attention(oracle_lib):
     """gamma = 0: every proxy is the window mean, so each group's mass is g times
     the sum over the GQA group of softmax(mu_h . k / sqrt(d)) -- textbook
-    single-query attention (scipy softmax on the same bf16 values)."""
+    single-query attention (scipy softmax on the same bf16 values, the
+    queries scaled by log2(e)/sqrt(d) before their bf16 rounding, so the
+    softmax argument is ln(2) times their product with the keys)."""
     B, Hq, Hkv, T, W, d, P, G = 1, 4, 2, 40, 6, 64, 16, 4
     q, k = rand_inputs(B, Hq, Hkv, T, W, d, 12)
     prox, ql, st = oracle_lib.build_proxies(q, P, 0.0, seed=1)
@@ -156,9 +171,9 @@ def test_gamma_zero_is_single_query_attention(oracle_lib):
         acc_l = np.zeros(T)
         for hl in range(Gh):
             h = c * Gh + hl
-            mu = brute.bits_to_f64(bf16_bits(st[0, h, 0].astype(np.float32)))
-            acc += softmax(kb[0, c] @ mu / math.sqrt(d))
-            acc_l += softmax(kb[0, c] @ brute.bits_to_f64(ql[0, h]) / math.sqrt(d))
+            mu = brute.scale_to_bf16(st[0, h, 0], d)
+            acc += softmax(kb[0, c] @ mu * math.log(2.0))
+            acc_l += softmax(kb[0, c] @ brute.scale_to_bf16(brute.bits_to_f64(ql[0, h]), d) * math.log(2.0))
         np.testing.assert_allclose(gm[0, c], np.broadcast_to((P // G) * acc, (G, T)), rtol=1e-11)
         np.testing.assert_allclose(mass[0, c], P * acc, rtol=1e-11)
         np.testing.assert_allclose(an[0, c], acc_l / Gh, rtol=1e-11)
