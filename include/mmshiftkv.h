@@ -98,14 +98,17 @@ typedef struct {
  * z from Philox4x32-10 (counter (j/4, i, h, (b<<16)|layer), key = seed) and
  * Box-Muller on series-evaluated ln/sin/cos in fp64, each product and sum
  * rounded separately; optional rotate-half rotary embedding (pairs j, j+d/2)
- * from the caller's cos/sin tables; then fp64 -> fp32 -> bf16, both round to
- * nearest even.  q_last[b,h] is window query W-1 (rotated by the *_l tables
- * when given), rounded the same way; it is the anchor query of Eq. 11.
+ * from the caller's cos/sin tables; then multiplied by the softmax scale
+ * c = log2(e)/sqrt(d) (fp64; the proxies carry Eq. 7's 1/sqrt(d), so their
+ * products with the keys are base-2 logits) and rounded fp64 -> fp32 ->
+ * bf16, both round to nearest even.  q_last[b,h] is window query W-1
+ * (rotated by the *_l tables when given), rounded the same way but NOT
+ * scaled; it is the anchor query of Eq. 11.
  *   q_win     [B, Hq, W, d] q_dtype, strides q_strides (elements)
  *   rope_*_f  [d/2] fp32 cos/sin at the proxies' future position, or both NULL
  *   rope_*_l  [d/2] fp32 cos/sin at the last query's position, or both NULL
- *   proxies   [B, Hq, P, d] bf16 out, contiguous
- *   q_last    [B, Hq, d] bf16 out, contiguous
+ *   proxies   [B, Hq, P, d] bf16 out, contiguous (scaled by c)
+ *   q_last    [B, Hq, d] bf16 out, contiguous (not scaled)
  *   stats     [B, Hq, 2, d] fp64 out (mu then sigma) or NULL */
 int mmshiftkv_build_proxies(const mmskv_shape *shape, const mmskv_params *params,
                             const void *q_win, int32_t q_dtype, const mmskv_strides *q_strides,
@@ -116,8 +119,12 @@ int mmshiftkv_build_proxies(const mmskv_shape *shape, const mmskv_params *params
 /* Step 2 -- proxy attention and masses (Sec. 3.2.2 Eqs. 7-8; Sec. 3.2.3
  * Eq. 11; Appendix B GQA aggregation).  For KV head c of batch row b, every
  * proxy row of the Gh query heads that share c gets its softmax over all T
- * keys (scale 1/sqrt(d); bf16 operands, fp32 accumulation; fp32 keys are
- * rounded to bf16 for scoring).  Outputs, fp32, contiguous:
+ * keys: the proxies arrive scaled by c = log2(e)/sqrt(d) (as the proxy calls
+ * make them), so p_t = 2^(s_t - L) with s_t = q~ . k_t and
+ * L = log2 sum_t 2^(s_t) (bf16 operands, fp32 accumulation; fp32 keys are
+ * rounded to bf16 for scoring).  The anchor queries q_last arrive unscaled
+ * and are scaled the same way here (fp64 product with c, then fp32, then
+ * bf16).  Outputs, fp32, contiguous:
  *   group_mass [B, Hkv, G, T]  sum over the group's proxies and heads
  *                              (may be NULL in MMSKV_MASS mode)
  *   mass       [B, Hkv, T]     sum over all groups
@@ -221,7 +228,8 @@ int mmshiftkv_hidden_proxies(const mmskv_hshape *shape, const mmskv_params *para
 /* Eq. 6: proxies[b, h, i, :] = W_Q^(h) hp[b, i, :] (bf16 operands, fp32
  * accumulation on the matrix cores), then, when rope_cos / rope_sin are
  * given, the rotate-half rotary embedding at the future position (pairs
- * e, e + d/2, fp32), rounded to bf16.
+ * e, e + d/2, fp32), then the softmax scale log2(e)/sqrt(d) (fp64 product,
+ * rounded to fp32), rounded to bf16.
  *   hp        [B, P, D] bf16, contiguous
  *   wq        [Hq * d, D] bf16, contiguous (row h*d + e is output feature e
  *             of head h; no bias)

@@ -10,6 +10,13 @@ using namespace mmskv;
 
 namespace {
 
+// Softmax scale carried by the queries (Sec. 3.2.2 Eq. 7's 1/sqrt(d), with
+// log2(e) so that the products are base-2 logits), in fp64: the proxies are
+// multiplied by it before their bf16 rounding and the score passes apply it
+// to the anchor rows the same way.
+double query_scale(int d) { return 1.4426950408889634074 / sqrt(static_cast<double>(d)); }
+
+
 constexpr size_t kAlign = 256;
 constexpr size_t kMaxRowLds = 96 * 1024;   // Gh * P + 32 rows of fp32 in LDS
 
@@ -129,7 +136,7 @@ int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const ui
     a->n_kb = l.n_kb;
     a->rows = l.rows;
     a->rows_pad = l.rows_pad;
-    a->kappa = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(shape->d)));
+    a->anchor_scale = query_scale(shape->d);
     a->part = static_cast<float2*>(ws);
     a->lse = reinterpret_cast<float*>(static_cast<char*>(ws) + l.lse_off);
     a->group_mass = nullptr;
@@ -211,6 +218,7 @@ int mmshiftkv_build_proxies(const mmskv_shape* shape, const mmskv_params* params
     a.ddof = params->std_ddof;
     a.layer = params->layer;
     a.gamma = params->gamma;
+    a.scale = query_scale(shape->d);
     a.key0 = static_cast<uint32_t>(params->seed & 0xFFFFFFFFull);
     a.key1 = static_cast<uint32_t>(params->seed >> 32);
     return status_of(launch_build_proxies(a, static_cast<hipStream_t>(stream)));
@@ -439,6 +447,7 @@ int mmshiftkv_project_proxies(const mmskv_hshape* shape, int32_t P, int32_t Hq, 
     a.P = P;
     a.Hq = Hq;
     a.d = d;
+    a.scale = query_scale(d);
     return status_of(launch_project(a, static_cast<hipStream_t>(stream)));
 }
 

@@ -18,7 +18,8 @@
 //                output tiles, 64-wide k steps double buffered in LDS through
 //                registers, four waves of 64x64; the epilogue goes through
 //                LDS so that the rotary pairs (e, e + d/2) of a head meet in
-//                one thread, then rounds to bf16.
+//                one thread, then multiplies by the query scale
+//                log2(e)/sqrt(d) in fp64 and rounds to bf16.
 #pragma clang fp contract(off)
 
 #include <math.h>
@@ -31,6 +32,12 @@ namespace mmskv {
 namespace {
 
 constexpr int kStatThreads = 256;
+
+// fp32 value times the query scale, in fp64, rounded back to fp32.
+__device__ __forceinline__ float scaled(float v, double scale) {
+    const double y = static_cast<double>(v) * scale;
+    return static_cast<float>(y);
+}
 constexpr int kStatVec = 8;                 // features per thread (one 16-byte bf16 load)
 
 // 8 consecutive features of one token as fp64.
@@ -264,8 +271,8 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
         if (!rope) {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                lo[q] = f32_to_bf16_bits(tile[r * kLd + col + 2 * q]) |
-                        (f32_to_bf16_bits(tile[r * kLd + col + 2 * q + 1]) << 16);
+                lo[q] = f32_to_bf16_bits(scaled(tile[r * kLd + col + 2 * q], p.scale)) |
+                        (f32_to_bf16_bits(scaled(tile[r * kLd + col + 2 * q + 1], p.scale)) << 16);
             *reinterpret_cast<u32x4*>(out + e) = lo;
         } else {
             uint32_t l16[8], h16[8];
@@ -274,8 +281,8 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
                 const float x0 = tile[r * kLd + col + q], x1 = tile[r * kLd + col + half + q];
                 const float c = p.cos[e + q], s = p.sin[e + q];
                 const float a0 = x0 * c, a1 = x1 * s, b0 = x1 * c, b1 = x0 * s;
-                l16[q] = f32_to_bf16_bits(a0 - a1);
-                h16[q] = f32_to_bf16_bits(b0 + b1);
+                l16[q] = f32_to_bf16_bits(scaled(a0 - a1, p.scale));
+                h16[q] = f32_to_bf16_bits(scaled(b0 + b1, p.scale));
             }
 #pragma unroll
             for (int q = 0; q < 4; ++q) {

@@ -21,6 +21,7 @@ struct ProxyArgs {
     double* stats;        // [B, Hq, 2, d] or null
     int B, Hq, W, d, P, ddof, layer;
     double gamma;
+    double scale;         // log2(e) / sqrt(d), applied before the rounding
     uint32_t key0, key1;
 };
 
@@ -35,8 +36,8 @@ struct ScoreArgs {
     int n_kb;                  // key blocks of block_keys
     int rows;                  // Gh * P proxy rows per KV head
     int rows_pad;              // rows + 32 * ceil(Gh / 32) (anchor rows, padded)
-    float kappa;               // log2(e) / sqrt(d)
-    float2* part;              // [B, Hkv, n_kb, rows_pad]  (max*kappa, sum)
+    double anchor_scale;       // log2(e) / sqrt(d), applied to the anchor rows
+    float2* part;              // [B, Hkv, n_kb, rows_pad]  (max, sum), base 2
     float* lse;                // [B, Hkv, rows_pad]        log2-domain
     float* group_mass;         // [B, Hkv, G, T] or null
     float* mass;               // [B, Hkv, T]
@@ -86,6 +87,7 @@ struct ProjectArgs {
     const uint16_t* w;    // [N, K] query weights, N = Hq * d
     const float* cos; const float* sin;   // [d/2] or null
     uint16_t* out;        // [B, Hq, P, d]
+    double scale;         // log2(e) / sqrt(d), applied before the rounding
     int M, N, K, P, Hq, d;
 };
 

@@ -4,7 +4,10 @@
 // Every floating-point step here is an fp64 operation rounded on its own
 // (no fused multiply-add), so the proxies are a fixed function of the
 // inputs: window statistics summed in window order, Philox4x32-10 words,
-// Box-Muller with series-evaluated ln / sin / cos, fp64 -> fp32 -> bf16.
+// Box-Muller with series-evaluated ln / sin / cos, the softmax scale
+// log2(e)/sqrt(d) that the queries carry (Sec. 3.2.2 Eq. 7, so the score
+// products are base-2 logits), fp64 -> fp32 -> bf16.  The anchor query is
+// returned unscaled.
 #pragma clang fp contract(off)
 
 #include "common.hpp"
@@ -129,9 +132,12 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
             x[e] = mu[j] + t;
         }
         if (!rope) {
+            double sx[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sx[e] = x[e] * a.scale;
             uint2 pk;
-            pk.x = static_cast<uint32_t>(to_bf16(x[0])) | (static_cast<uint32_t>(to_bf16(x[1])) << 16);
-            pk.y = static_cast<uint32_t>(to_bf16(x[2])) | (static_cast<uint32_t>(to_bf16(x[3])) << 16);
+            pk.x = static_cast<uint32_t>(to_bf16(sx[0])) | (static_cast<uint32_t>(to_bf16(sx[1])) << 16);
+            pk.y = static_cast<uint32_t>(to_bf16(sx[2])) | (static_cast<uint32_t>(to_bf16(sx[3])) << 16);
             *reinterpret_cast<uint2*>(row + 4 * jq) = pk;
         } else {
             // partner dims j + d/2 come from quad jq + d/8
@@ -151,8 +157,9 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
                 const double c = static_cast<double>(a.cos_f[j]), s = static_cast<double>(a.sin_f[j]);
                 const double a0 = x[e] * c, a1 = y[e] * s;
                 const double b0 = y[e] * c, b1 = x[e] * s;
-                lo[e] = to_bf16(a0 - a1);
-                hi[e] = to_bf16(b0 + b1);
+                const double rl = a0 - a1, rh = b0 + b1;
+                lo[e] = to_bf16(rl * a.scale);
+                hi[e] = to_bf16(rh * a.scale);
             }
             uint2 pl, ph;
             pl.x = lo[0] | (static_cast<uint32_t>(lo[1]) << 16);

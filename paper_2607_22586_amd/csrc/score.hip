@@ -15,17 +15,20 @@
 // An exact column mass needs every row's full normaliser, so the keys are
 // scored twice:
 //   score_lse:  D = K * P^T (keys as rows).  Per proxy row: max and
-//               sum 2^(s*kappa - max) over the wave's keys (in-lane, then one
+//               sum 2^(s - max) over the wave's keys (in-lane, then one
 //               cross-lane step), merged over the waves through LDS into one
 //               partial per (row, key block); lse_combine folds the partials
-//               into L_row = log2 sum_t 2^(s_t*kappa).
-//   score_mass: D = P * K^T (proxies as rows).  p = 2^(s*kappa - L_row);
+//               into L_row = log2 sum_t 2^(s_t).
+//   score_mass: D = P * K^T (proxies as rows).  p = 2^(s - L_row);
 //               column sums over the 16-row halves of each tile, accumulated
 //               over the Gh heads into per-group masses, then over groups
 //               into the total mass, and over the anchor rows.  Each key
 //               column belongs to one wave, so there are no atomics and the
 //               result is deterministic.
-// kappa = log2(e)/sqrt(d), so 2^(s*kappa) = e^(s/sqrt(d)).
+// The query rows carry the softmax scale log2(e)/sqrt(d) (the proxies from
+// their construction, the anchor rows from their staging here, both in fp64
+// before the bf16 rounding), so s = q~ . k is a base-2 logit and
+// 2^s = e^(q.k/sqrt(d)).
 //
 // Workgroups are numbered so that all key blocks of one (b, c) land on the
 // same XCD (workgroup i runs on XCD i mod 8), keeping that head's proxies in
@@ -130,7 +133,9 @@ struct Stager {
         for (int k = 0; k < kPer; ++k)
             if (active(k)) v[k] = *reinterpret_cast<const u32x4*>(base + off[k]);
     }
-    // any tile of the padded row space (anchor rows)
+    // any tile of the padded row space; anchor rows (the raw last window
+    // queries) are scaled by log2(e)/sqrt(d) in fp64 and rounded back to
+    // bf16 (fp64 -> fp32 -> bf16), like the proxies
     __device__ __forceinline__ void load_rows(const ScoreArgs& a, int b, int c, int row0) {
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
@@ -139,6 +144,15 @@ struct Stager {
                 const int r = q / TileLds<D>::kChunks;
                 const int cs = q - r * TileLds<D>::kChunks;
                 v[k] = *reinterpret_cast<const u32x4*>(row_ptr<D>(a, b, c, row0 + r) + 8 * cs);
+                if (row0 + r >= a.rows) {
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const double lo = static_cast<double>(__uint_as_float(v[k][w] << 16)) * a.anchor_scale;
+                        const double hi = static_cast<double>(__uint_as_float(v[k][w] & 0xFFFF0000u)) * a.anchor_scale;
+                        v[k][w] = f32_to_bf16_bits(static_cast<float>(lo)) |
+                                  (f32_to_bf16_bits(static_cast<float>(hi)) << 16);
+                    }
+                }
             }
         }
     }
@@ -183,8 +197,8 @@ __device__ __forceinline__ void read_frags(const u32x4* sp, bf16x8 (&A)[D / 16],
 }
 
 // Accumulator start for a P * K^T tile whose rows begin at `rowv`: each
-// lane's 16 rows (8*m + 4*(lane/32) + j) get -L_row/kappa, so the MFMA result
-// is s - L/kappa and the probability is 2^(kappa * acc).
+// lane's 16 rows (8*m + 4*(lane/32) + j) get -L_row, so the MFMA result is
+// s - L and the probability is 2^acc.
 __device__ __forceinline__ floatx16 row_offsets(const float* rowv, int lane) {
     floatx16 c;
 #pragma unroll
@@ -231,7 +245,7 @@ constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batc
 // Pass 1 in the K * P^T layout: lane l holds proxy column l % 32 of a tile and
 // keys key0 + 32*s + 8*(i/4) + 4*(l/32) + i%4 of sub-tile s (value 16*s + i of
 // the lane).  Per tile and column, m = max over the wave's 64 keys and
-// l = sum 2^(s*kappa - m*kappa); the pair (m*kappa, l) goes to LDS and the
+// l = sum 2^(s - m); the pair (m, l) goes to LDS and the
 // waves' pairs are merged every kMergeTiles tiles into one partial per
 // (row, key block).  FULL: every key of the block is < T.
 template <int D, int WAVES, bool FULL>
@@ -241,7 +255,6 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     using St = Stager<D, WAVES>;
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
     const int key0 = kb * 64 * WAVES + wave * kWaveKeys;
-    const float kappa = a.kappa;
 
     bf16x8 kf[kSub][D / 16];
     load_keys<D>(a, b, c, key0, kf);
@@ -320,7 +333,7 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         constexpr int cur = T4 & 1, prev = cur ^ 1;
         const u32x4* next = stage[(T4 + 1) % kRing];
         const bool mfma_on = FAST || t < n_tiles;
-        float m = -INFINITY, nmk = 0.f, l0 = 0.f, l1 = 0.f;
+        float m = -INFINITY, nm = 0.f, l0 = 0.f, l1 = 0.f;
 #pragma unroll
         for (int kc = 0; kc < D / 16; ++kc) {
 #pragma unroll
@@ -338,13 +351,13 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
                         }
                     } else if (slot == kMaxSlots) {
                         m = pair_max(m);
-                        nmk = (FULL || m != -INFINITY) ? -m * kappa : 0.f;
+                        nm = (FULL || m != -INFINITY) ? -m : 0.f;
                     } else {
 #pragma unroll
                         for (int q = 0; q < kExpPer; ++q) {
                             const int idx = (slot - kMaxSlots - 1) * kExpPer + q;
                             if (idx < 32) {
-                                const float e = fast_exp2(fmaf(value(acc[prev], idx), kappa, nmk));
+                                const float e = fast_exp2(value(acc[prev], idx) + nm);
                                 const float ev = ok(idx) ? e : 0.f;
                                 if (q & 1) l1 += ev; else l0 += ev;
                             }
@@ -366,7 +379,7 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         if (STATS) {
             const int tp = t - 1;
             const float l = pair_total(l0 + l1);
-            if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(-nmk, l);
+            if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(-nm, l);
             if (T4 == 1 && tp >= kMergeTiles && (tp - kMergeTiles) % kMergeTiles == 0)
                 merge_chunk((tp - kMergeTiles) / kMergeTiles);
         }
@@ -464,7 +477,6 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     const int b = head / a.Hkv, c = head - b * a.Hkv;
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
     const int key0 = kb * 64 * WAVES + wave * kWaveKeys;
-    const float kappa = a.kappa;
     const float* L = a.lse + static_cast<int64_t>(head) * a.rows_pad;
 
     bf16x8 kf[kSub][D / 16];
@@ -501,7 +513,6 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     St pre[3], st[2];
     TileCursor ld{0, 0, 0};                  // next tile to fetch
     constexpr int kLBatch = 8;               // row offsets fetched per thread at once
-    const float inv_kappa = 1.0f / kappa;
     auto l_batch = [&](int i0, auto&& between) {
         float lv[kLBatch];
 #pragma unroll
@@ -513,7 +524,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
 #pragma unroll
         for (int j = 0; j < kLBatch; ++j) {
             const int i = i0 + j * 64 * WAVES;
-            if (i < a.rows_pad) Llds[i] = -lv[j] * inv_kappa;
+            if (i < a.rows_pad) Llds[i] = -lv[j];
         }
     };
     l_batch(static_cast<int>(threadIdx.x), [&]() {
@@ -578,12 +589,12 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     // One pipeline iteration; PROBS: tile t-1 exists (t > 0).  FAST: tile t
     // exists, tile t+3 is staged and tile t+5 fetched, so nothing branches.
     // The issue order is fixed by hand: after MFMA slot j of tile t come the
-    // sums of value group j-2, the exps of group j-1 and the kappa products of
-    // group j of tile t-1 (kPer32 of its 32 accumulator values per group), so
-    // no VALU step waits on the one before it and the matrix pipe and the
-    // VALU work side by side; the fragment refill follows the second MFMA of
-    // each k-chunk, the accumulator start of tile t+1 is read halfway and the
-    // staging sits at the end.
+    // sums of value group j-1 and the exps of group j of tile t-1 (kPer32 of
+    // its 32 accumulator values per group; the accumulator already holds the
+    // base-2 exponent s - L), so no VALU step waits on the one before it and
+    // the matrix pipe and the VALU work side by side; the fragment refill
+    // follows the second MFMA of each k-chunk, the accumulator start of tile
+    // t+1 is read halfway and the staging sits at the end.
     constexpr int kMfmas = kSub * (D / 16);
     constexpr int kPer32 = 32 / kMfmas;
     auto iter = [&](auto t4, auto probs, auto fast, int t) {
@@ -593,7 +604,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
         const u32x4* next = stage[(T4 + 1) % kRing];
         const bool mfma_on = FAST || t < n_prox;
         floatx16 Cnext;
-        float mv[kPer32], ev[kPer32];
+        float ev[kPer32];
         auto add_group = [&](int g) {
 #pragma unroll
             for (int v = 0; v < kPer32; ++v) {
@@ -601,15 +612,11 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
                 if (i < 8) runA[s2][v & 1] += ev[v]; else runB[s2][v & 1] += ev[v];
             }
         };
-        auto exp_group = [&]() {
-#pragma unroll
-            for (int v = 0; v < kPer32; ++v) ev[v] = fast_exp2(mv[v]);
-        };
-        auto mul_group = [&](int g) {
+        auto exp_group = [&](int g) {
 #pragma unroll
             for (int v = 0; v < kPer32; ++v) {
                 const int idx = g * kPer32 + v;
-                mv[v] = acc[prev][idx / 16][idx % 16] * kappa;
+                ev[v] = fast_exp2(acc[prev][idx / 16][idx % 16]);
             }
         };
 #pragma unroll
@@ -619,9 +626,8 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
                 const int slot = kSub * kc + s;
                 if (mfma_on) acc[cur][s] = mfma32(A[kc], kf[s][kc], kc == 0 ? Cn : acc[cur][s]);
                 if (PROBS) {
-                    if (slot >= 2) add_group(slot - 2);
-                    if (slot >= 1) exp_group();
-                    mul_group(slot);
+                    if (slot >= 1) add_group(slot - 1);
+                    exp_group(slot);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -634,8 +640,6 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
             __builtin_amdgcn_sched_barrier(0);
         }
         if (PROBS) {
-            add_group(kMfmas - 2);
-            exp_group();
             add_group(kMfmas - 1);
 #pragma unroll
             for (int s = 0; s < kSub; ++s)
@@ -700,7 +704,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
             for (int s = 0; s < kSub; ++s)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const float e = fast_exp2(ac[s][4 * m4 + j] * kappa);
+                    const float e = fast_exp2(ac[s][4 * m4 + j]);
                     aacc[s] += (h0 + 8 * m4 + j < a.Gh) ? e : 0.f;
                 }
     }

@@ -44,9 +44,11 @@ def bf16_ulp(x):
 
 
 def check_projection(gpu_bits, hp_bits, wq_bits, Hq, rope=None, min_exact=0.99):
-    """GPU proxies vs the oracle's fp64 projection: |gpu - pre| <= ulp/2 +
-    acc, acc = (D + 16) 2^-24 sum_k |x_k w_k| (fp32 accumulation), widened
-    through the rotation when there is one."""
+    """GPU proxies vs the oracle's fp64 projection (times the query scale
+    c = log2(e)/sqrt(d)): |gpu - pre| <= ulp/2 + acc, acc = c (D + 16)
+    2^-24 sum_k |x_k w_k| (fp32 accumulation), widened through the rotation
+    when there is one, plus 2^-23 |pre| for the fp32 rounding of the scaled
+    value."""
     out, pre = oracle.project_proxies(hp_bits, wq_bits, Hq, rope=rope, with_pre=True)
     B, P, D = hp_bits.shape
     d = wq_bits.shape[0] // Hq
@@ -56,12 +58,14 @@ def check_projection(gpu_bits, hp_bits, wq_bits, Hq, rope=None, min_exact=0.99):
     acc = (D + 16) * 2.0 ** -24 * absdot
     if rope is not None:
         _, raw = oracle.project_proxies(hp_bits, wq_bits, Hq, with_pre=True)
+        raw = raw / brute.qscale(d)              # the unscaled projection the rotation acts on
         h = d // 2
         c = np.abs(rope[0].astype(np.float64))
         s = np.abs(rope[1].astype(np.float64))
         lo = acc[..., :h] * c + acc[..., h:] * s + 2.0 ** -22 * (np.abs(raw[..., :h]) * c + np.abs(raw[..., h:]) * s)
         hi = acc[..., h:] * c + acc[..., :h] * s + 2.0 ** -22 * (np.abs(raw[..., h:]) * c + np.abs(raw[..., :h]) * s)
         acc = np.concatenate([lo, hi], axis=-1)
+    acc = acc * brute.qscale(d) + 2.0 ** -23 * np.abs(pre)
     g = brute.bits_to_f64(gpu_bits)
     err = np.abs(g - pre)
     bound = 0.5 * bf16_ulp(np.abs(pre) + acc) + acc
