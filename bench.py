@@ -8,7 +8,13 @@ keys (16128 visual + 256 text), W=64 window queries, budget 256 per KV
 head, the paper's method settings (P=512, G=32, gamma=10, tau=0.95,
 lambda=1, vote mode).
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--streams N]
+
+The layers of a step are independent, so the throughput steps spread them
+over N HIP streams (layer l on stream l % N, default 3): the latency-bound
+selection kernels and the tails of one layer's score passes then overlap
+another layer's work.  The score-pass durations for the roofline come from
+K further steps on one stream, where no other kernel shares the GPU.
 
 Prints one JSON line: keys scored+selected per second (B*L*T / step time),
 the roofline of the dominant kernel (algorithmic MFMA flops per launch /
@@ -100,6 +106,9 @@ def main():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--mode", choices=["vote", "mass"], default="vote")
     ap.add_argument("--cpu-heads", type=int, default=12)
+    ap.add_argument("--streams", type=int, default=3,
+                    help="HIP streams the layers are spread over in the throughput steps "
+                         "(layer l on stream l %% n); the kernel-timing steps use one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
@@ -136,56 +145,79 @@ def main():
     torch.cuda.synchronize()
     log("inputs ready: %.2f GiB" % (sum(x["k"].numel() * 2 * x["k"].element_size() for x in layers) / 2**30))
 
-    # preallocated outputs and workspaces (reused by every layer)
-    prox = torch.empty((B, Hq, cfg.P, d), dtype=torch.bfloat16, device=dev)
-    qlast = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
-    sc = bd.ScoreOut(torch.empty((B, Hkv, cfg.G, T), dtype=torch.float32, device=dev) if mode == 0 else None,
-                     torch.empty((B, Hkv, T), dtype=torch.float32, device=dev),
-                     torch.empty((B, Hkv, T), dtype=torch.float32, device=dev))
-    ws_score = torch.empty(bd.score_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev)
-    ws_sel = torch.empty(bd.select_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev)
-    sel = bd.Selected(torch.empty((B, Hkv, w.budget), dtype=torch.int32, device=dev),
-                      torch.empty((B, Hkv), dtype=torch.int32, device=dev), None)
+    # preallocated outputs and workspaces, one set per stream (reused by the
+    # layers of that stream)
+    def buffers():
+        return dict(
+            prox=torch.empty((B, Hq, cfg.P, d), dtype=torch.bfloat16, device=dev),
+            qlast=torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev),
+            sc=bd.ScoreOut(torch.empty((B, Hkv, cfg.G, T), dtype=torch.float32, device=dev) if mode == 0 else None,
+                           torch.empty((B, Hkv, T), dtype=torch.float32, device=dev),
+                           torch.empty((B, Hkv, T), dtype=torch.float32, device=dev)),
+            ws_score=torch.empty(bd.score_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev),
+            ws_sel=torch.empty(bd.select_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev),
+            sel=bd.Selected(torch.empty((B, Hkv, w.budget), dtype=torch.int32, device=dev),
+                            torch.empty((B, Hkv), dtype=torch.int32, device=dev), None))
+    n_streams = max(1, args.streams)
+    bufs = [buffers() for _ in range(n_streams)]
     kv_out = [(torch.empty((B, Hkv, w.budget, d), dtype=layers[0]["k"].dtype, device=dev),
                torch.empty((B, Hkv, w.budget, d), dtype=layers[0]["k"].dtype, device=dev)) for _ in range(L)]
     stream = torch.cuda.current_stream(dev)
+    # extra streams at the default priority
+    streams = [stream] + [torch.cuda.Stream(dev) for _ in range(n_streams - 1)]
 
-    def step(events=None):
+    def step(events=None, n=n_streams):
+        for s in streams[1:n]:
+            s.wait_stream(stream)
         for l in range(L):
             x = layers[l]
             c = cfgs[l]
-            bd.build_proxies(x["q_win"], c, T, Hkv, out=(prox, qlast))
-            if events is not None:
-                events[l][0].record(stream)
-            bd.score_lse(prox, qlast, x["k"], c, ws_score, W)
-            if events is not None:
-                events[l][1].record(stream)
-            bd.score_mass(prox, qlast, x["k"], c, ws_score, W, out=sc)
-            if events is not None:
-                events[l][2].record(stream)
-            bd.select_topk(sc, c, w.budget, w.budget, None, Hq, W, out=sel, workspace=ws_sel)
-            bd.gather_kv(x["k"], x["v"], sel, out=kv_out[l])
+            s = streams[l % n]
+            bf = bufs[l % n]
+            with torch.cuda.stream(s):
+                bd.build_proxies(x["q_win"], c, T, Hkv, out=(bf["prox"], bf["qlast"]))
+                if events is not None:
+                    events[l][0].record(s)
+                bd.score_lse(bf["prox"], bf["qlast"], x["k"], c, bf["ws_score"], W)
+                if events is not None:
+                    events[l][1].record(s)
+                bd.score_mass(bf["prox"], bf["qlast"], x["k"], c, bf["ws_score"], W, out=bf["sc"])
+                if events is not None:
+                    events[l][2].record(s)
+                bd.select_topk(bf["sc"], c, w.budget, w.budget, None, Hq, W, out=bf["sel"], workspace=bf["ws_sel"])
+                bd.gather_kv(x["k"], x["v"], bf["sel"], out=kv_out[l])
+        for s in streams[1:n]:
+            stream.wait_stream(s)
 
     for i in range(args.warmup):
         step()
         torch.cuda.synchronize()
         log("warmup step %d done" % (i + 1))
 
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(L)] for _ in range(args.steps)]
+    # throughput: K whole steps, layers spread over the streams
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
     for s in range(args.steps):
-        step(ev[s])
+        step()
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
+    log("timed %d steps on %d stream(s): %.3f ms/step" % (args.steps, n_streams, ms_step))
+
+    # kernel timing: one more warmup and K steps on one stream, with events
+    # around the two score passes of every layer (un-overlapped durations)
+    step(n=1)
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(L)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for s in range(args.steps):
+        step(ev[s], n=1)
+    torch.cuda.synchronize()
     lse_ms = sum(ev[s][l][0].elapsed_time(ev[s][l][1]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
     mass_ms = sum(ev[s][l][1].elapsed_time(ev[s][l][2]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
-    log("timed %d steps: %.3f ms/step, score_lse %.1f us, score_mass %.1f us per layer"
-        % (args.steps, ms_step, lse_ms * 1e3, mass_ms * 1e3))
+    log("kernel timing on one stream: score_lse %.1f us, score_mass %.1f us per layer" % (lse_ms * 1e3, mass_ms * 1e3))
 
     # algorithmic MFMA work of one scoring launch: 2*Gh*P*d flops per prompt
     # key per KV head (one proxy-by-key contraction), times B*Hkv*T keys
@@ -210,11 +242,12 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "layers": L, "batch": B, "T": T, "Hq": Hq, "Hkv": Hkv, "d": d, "W": W,
                    "budget": w.budget, "P": cfg.P, "G": cfg.G, "gamma": cfg.gamma, "tau": cfg.tau,
-                   "lambda": cfg.lam, "mode": args.mode},
+                   "lambda": cfg.lam, "mode": args.mode, "streams": n_streams},
         "stages_us_per_layer": {"score_lse": lse_ms * 1e3, "score_mass": mass_ms * 1e3},
         "roofline": {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": measured_traffic(w.name, dom)},
+                     "traffic": measured_traffic(w.name, dom),
+                     "timing": "%d steps on one stream after the throughput steps" % args.steps},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on %d head(s)" % args.cpu_heads)
