@@ -87,6 +87,8 @@ def _load():
     lib.oracle_query_scale.argtypes = [i32]
     lib.oracle_query_scale.restype = f64
     lib.oracle_project_proxies.restype = i32
+    lib.oracle_decode_check.argtypes = [i32, i32, i32, i32, i32, i32, P, P, i32, P, P, i32, P, P, i32, P, P]
+    lib.oracle_decode_check.restype = i32
     _lib = lib
     return lib
 
@@ -339,3 +341,33 @@ def project_proxies(hp: np.ndarray, wq: np.ndarray, Hq: int, rope=None, with_pre
     if rc != 0:
         raise ValueError("oracle_project_proxies: invalid arguments")
     return (out, pre) if with_pre else out
+
+
+def decode_check(q_dec: np.ndarray, k: np.ndarray, idx: np.ndarray, counts: np.ndarray,
+                 k_out: np.ndarray, v_out: np.ndarray):
+    """Decode-time check (Fig. 1b's attention-mass coverage; decode attention
+    over the fixed compacted cache, Sec. 3.1 / Sec. 3.2.3).
+
+    q_dec [B, Hq, n_dec, d] bf16 bits (unscaled); k [B, Hkv, T, d];
+    idx [B, Hkv, c_max], counts [B, Hkv]; k_out, v_out [B, Hkv, c_max, d].
+    Returns (coverage [B, Hq, n_dec], out [B, Hq, n_dec, d]), fp64.
+    """
+    q_dec = np.ascontiguousarray(q_dec, dtype=np.uint16)
+    k = np.ascontiguousarray(k)
+    k_out = np.ascontiguousarray(k_out)
+    v_out = np.ascontiguousarray(v_out)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    B, Hq, n_dec, d = q_dec.shape
+    Hkv, T = k.shape[1], k.shape[2]
+    c_max = idx.shape[2]
+    assert k.shape == (B, Hkv, T, d) and k_out.shape == (B, Hkv, c_max, d) and v_out.shape == k_out.shape
+    assert k_out.dtype == v_out.dtype
+    cov = np.zeros((B, Hq, n_dec), dtype=np.float64)
+    out = np.zeros((B, Hq, n_dec, d), dtype=np.float64)
+    rc = _load().oracle_decode_check(B, Hq, Hkv, T, d, n_dec, _ptr(q_dec), _ptr(k), _dtype_code(k),
+                                     _ptr(idx), _ptr(counts), c_max, _ptr(k_out), _ptr(v_out),
+                                     _dtype_code(k_out), _ptr(cov), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_decode_check rejected its arguments")
+    return cov, out

@@ -777,6 +777,93 @@ int oracle_gather(int B, int H, int T, int64_t row_bytes, int c_max, const void 
     return 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Decode-time check: the attention-mass coverage of Fig. 1b (the fraction  */
+/* of a decoding query's attention mass that falls on the prompt keys kept  */
+/* after prefilling) and decode attention over the compacted cache, which   */
+/* stays fixed while decoding under the prefill-only protocol (Sec. 3.1,    */
+/* Sec. 3.2.3).  For decode query j of query head h (KV head c = h / Gh) of */
+/* batch row b, with q~ the query scaled like the anchor query above and    */
+/* p its softmax over all T prompt keys (Eq. 7, base-2 logits):             */
+/*   coverage[b,h,j] = sum of p_t over the kept keys t (index order);       */
+/*   out[b,h,j,:]    = sum_i p'_i v'_i, p' the softmax of q~ over the       */
+/*                     counts[b,c] rows k'_i of the compacted cache.        */
+/* q_dec [B, Hq, n_dec, d] bf16, not scaled; k [B, Hkv, T, d] contiguous,   */
+/* kdtype; idx [B, Hkv, c_max] (ascending, -1 padded), counts [B, Hkv];     */
+/* k_out, v_out [B, Hkv, c_max, d] kvdtype; coverage [B, Hq, n_dec] fp64    */
+/* out; out [B, Hq, n_dec, d] fp64 out.                                     */
+/* ------------------------------------------------------------------------ */
+int oracle_decode_check(int B, int Hq, int Hkv, int T, int d, int n_dec,
+                        const uint16_t *q_dec, const void *k, int kdtype,
+                        const int32_t *idx, const int32_t *counts, int c_max,
+                        const void *k_out, const void *v_out, int kvdtype,
+                        double *coverage, double *out)
+{
+    if (B < 1 || Hq < 1 || Hkv < 1 || (Hq % Hkv) != 0 || T < 1 || d < 1 || n_dec < 1 || c_max < 1)
+        return -1;
+    for (int64_t bc = 0; bc < (int64_t)B * Hkv; ++bc) {
+        if (counts[bc] < 0 || counts[bc] > c_max)
+            return -1;
+        for (int i = 0; i < counts[bc]; ++i) {
+            int t = idx[bc * c_max + i];
+            if (t < 0 || t >= T)
+                return -1;
+        }
+    }
+    const int Gh = Hq / Hkv;
+    const int64_t rows = (int64_t)B * Hq * n_dec;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+    for (int64_t r = 0; r < rows; ++r) {
+        const int b = (int)(r / ((int64_t)Hq * n_dec));
+        const int h = (int)((r / n_dec) % Hq);
+        const int64_t bc = (int64_t)b * Hkv + h / Gh;
+        uint16_t *qs = malloc(sizeof(uint16_t) * (size_t)d);
+        double *logit = malloc(sizeof(double) * (size_t)T);
+        double *p = malloc(sizeof(double) * (size_t)T);
+        const int n = counts[bc];
+        double *lc = malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+        if (!qs || !logit || !p || !lc) {
+            bad = 1;
+        } else {
+            scale_query(q_dec + r * d, d, qs);
+            softmax_row(qs, k, kdtype, bc * T * d, T, d, logit, p);
+            double cov = 0.0;
+            for (int i = 0; i < n; ++i)
+                cov = cov + p[idx[bc * c_max + i]];
+            coverage[r] = cov;
+            /* softmax over the compacted rows, then the weighted sum of V' */
+            double mx = -INFINITY;
+            for (int i = 0; i < n; ++i) {
+                double dot = 0.0;
+                for (int j = 0; j < d; ++j) {
+                    double prod = oracle_bf16_to_f64(qs[j]) * load_key_bf16(k_out, kvdtype, (bc * c_max + i) * d + j);
+                    dot = dot + prod;
+                }
+                lc[i] = dot;
+                if (dot > mx)
+                    mx = dot;
+            }
+            double sum = 0.0;
+            for (int i = 0; i < n; ++i)
+                sum = sum + exp2(lc[i] - mx);
+            const double lse2 = mx + log2(sum);
+            for (int j = 0; j < d; ++j)
+                out[r * d + j] = 0.0;
+            for (int i = 0; i < n; ++i) {
+                const double w = exp2(lc[i] - lse2);
+                for (int j = 0; j < d; ++j)
+                    out[r * d + j] = out[r * d + j] + w * load_elem(v_out, kvdtype, (bc * c_max + i) * d + j);
+            }
+        }
+        free(qs);
+        free(logit);
+        free(p);
+        free(lc);
+    }
+    return bad ? -1 : 0;
+}
+
 int oracle_num_threads(void)
 {
 #ifdef _OPENMP

@@ -32,6 +32,14 @@ exp(0.5 n_j), visual rows s * (sqrt(1-eps^2) (A M)/sqrt(r) + eps E) (rank 64,
 eps 0.1), text rows s * N(0, 1.5), and 4 outlier features whose values are
 scaled by 10 (the few large-magnitude channels of LLM hidden states).
 
+Decode queries (``make_layer(..., n_dec=n)``, for the decode-time coverage
+check): n per query head, drawn after all other tensors of the layer from the
+same law as that head's window queries but with the noise variance scaled by
+DECODE_VAR_SCALE = 16 -- the paper reports hidden-state variance growing by
+13x to 22x from prefill to decoding (Appendix, global vs. layer-wise
+expansion), so decode queries spread wider than the window the proxies are
+built from.
+
 Tensors are drawn in fp32 with a seeded ``torch.Generator`` on the requested
 device and rounded to bf16 (round to nearest even) where the workload is bf16.
 The CPU stream is reproducible bit for bit; a device stream follows the same
@@ -87,6 +95,7 @@ LOWRANK_R = 64
 LOWRANK_EPS = 0.1
 TEXT_VAR = 1.5
 BLOCK_SHIFT_VAR = 0.5
+DECODE_VAR_SCALE = 16.0
 
 
 def _seed(wid: int, layer: int, stream: int) -> int:
@@ -103,7 +112,7 @@ def _randn(shape, gen, device):
     return torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
 
 
-def _planted(w: Workload, layer: int, device):
+def _planted(w: Workload, layer: int, device, n_dec: int = 0):
     g = _gen(device, w.wid, layer, 0)
     d, T = w.d, w.T
     u = _randn((w.B, w.Hkv, 1, d), g, device)
@@ -119,7 +128,10 @@ def _planted(w: Workload, layer: int, device):
     k = k + bump * (3.0 * math.sqrt(d)) * u
     u_q = u.repeat_interleave(w.Gh, dim=1)
     q = _randn((w.B, w.Hq, w.W, d), g, device) + math.sqrt(d) * u_q
-    return q, k, v, planted
+    q_dec = None
+    if n_dec > 0:
+        q_dec = math.sqrt(DECODE_VAR_SCALE) * _randn((w.B, w.Hq, n_dec, d), g, device) + math.sqrt(d) * u_q
+    return q, k, v, planted, q_dec
 
 
 def _lowrank_rows(shape_bc, n, r, eps, m, g, device):
@@ -128,7 +140,7 @@ def _lowrank_rows(shape_bc, n, r, eps, m, g, device):
     return math.sqrt(1.0 - eps * eps) * torch.matmul(a, m) / math.sqrt(r) + eps * e
 
 
-def _lowrank(w: Workload, layer: int, device):
+def _lowrank(w: Workload, layer: int, device, n_dec: int = 0):
     g = _gen(device, w.wid, layer, 1)
     d, T, r = w.d, w.T, LOWRANK_R
     n_vis = T - w.n_text
@@ -142,10 +154,13 @@ def _lowrank(w: Workload, layer: int, device):
     a_h = _randn((w.B, w.Hq, 1, r), g, device)
     m_h = 0.5 * torch.matmul(a_h, m_k.repeat_interleave(w.Gh, dim=1)) / math.sqrt(r)
     q = math.sqrt(TEXT_VAR) * _randn((w.B, w.Hq, w.W, d), g, device) + m_h
-    return q, k.contiguous(), v.contiguous(), None
+    q_dec = None
+    if n_dec > 0:
+        q_dec = math.sqrt(DECODE_VAR_SCALE * TEXT_VAR) * _randn((w.B, w.Hq, n_dec, d), g, device) + m_h
+    return q, k.contiguous(), v.contiguous(), None, q_dec
 
 
-def _blocks(w: Workload, layer: int, device):
+def _blocks(w: Workload, layer: int, device, n_dec: int = 0):
     g = _gen(device, w.wid, layer, 2)
     d, T, nb = w.d, w.T, w.n_blocks
     n_blk = (T - w.n_text) // nb
@@ -165,23 +180,32 @@ def _blocks(w: Workload, layer: int, device):
     s_q = s_k.repeat_interleave(w.Gh, dim=1)                    # [B, Hq, nb, d]
     shift_q = torch.gather(s_q, 2, pick[:, :, None, None].expand(w.B, w.Hq, 1, d))
     q = math.sqrt(TEXT_VAR) * _randn((w.B, w.Hq, w.W, d), g, device) + shift_q
-    return q, k, v, None
+    q_dec = None
+    if n_dec > 0:
+        q_dec = math.sqrt(DECODE_VAR_SCALE * TEXT_VAR) * _randn((w.B, w.Hq, n_dec, d), g, device) + shift_q
+    return q, k, v, None, q_dec
 
 
-def make_layer(w: Workload | str, layer: int = 0, device="cpu"):
-    """Inputs of one layer: dict(q_win [B,Hq,W,d], k, v [B,Hkv,T,d], planted).
+def make_layer(w: Workload | str, layer: int = 0, device="cpu", n_dec: int = 0):
+    """Inputs of one layer: dict(q_win [B,Hq,W,d], k, v [B,Hkv,T,d], planted,
+    q_dec).
 
     ``planted`` holds the planted key indices for the ``tiny`` workload
-    (None otherwise).  Tensors are fp32 for ``tiny`` and bf16 otherwise.
+    (None otherwise).  ``q_dec`` [B,Hq,n_dec,d] bf16 holds n_dec decode
+    queries per head (None when n_dec = 0); drawing them does not change the
+    other tensors.  Tensors are fp32 for ``tiny`` and bf16 otherwise (decode
+    queries are bf16 always).
     """
     if isinstance(w, str):
         w = WORKLOADS[w]
     fn = {"planted": _planted, "lowrank": _lowrank, "blocks": _blocks}[w.kind]
     with torch.no_grad():
-        q, k, v, planted = fn(w, layer, torch.device(device))
+        q, k, v, planted, q_dec = fn(w, layer, torch.device(device), n_dec)
         if w.dtype == "bf16":
             q, k, v = (x.to(torch.bfloat16) for x in (q, k, v))
-    return dict(q_win=q.contiguous(), k=k.contiguous(), v=v.contiguous(), planted=planted)
+        if q_dec is not None:
+            q_dec = q_dec.to(torch.bfloat16).contiguous()
+    return dict(q_win=q.contiguous(), k=k.contiguous(), v=v.contiguous(), planted=planted, q_dec=q_dec)
 
 
 HIDDEN_OUTLIERS = 4
