@@ -241,6 +241,34 @@ int mmshiftkv_project_proxies(const mmskv_hshape *shape, int32_t P, int32_t Hq, 
                               const float *rope_cos, const float *rope_sin,
                               uint16_t *proxies, void *stream);
 
+/* ---- Decode-time check (not part of the selection; it measures it).  The
+ * attention-mass coverage of Fig. 1b -- the share of a decoding query's
+ * softmax mass over all T prompt keys that falls on the keys kept after
+ * prefilling -- and decode attention over the compacted cache, which stays
+ * fixed while decoding under the prefill-only protocol (Sec. 3.1,
+ * Sec. 3.2.3).  For decode query j of query head h (KV head c = h / Gh) of
+ * batch row b, with q~ = bf16(fp32(q * log2(e)/sqrt(d))) (fp64 product, as
+ * for the anchor query) and base-2 logits s_t = q~ . k_t (bf16 operands,
+ * fp32 accumulation; fp32 keys rounded to bf16):
+ *   coverage[b,h,j] = sum over kept t of 2^(s_t - L),  L = log2 sum_t 2^(s_t),
+ * with kept = idx[b,c,0..counts[b,c]) (entries outside [0, T) ignored), and
+ *   out[b,h,j,:]    = sum_{i < counts[b,c]} 2^(s'_i - L') v'_i,
+ * s'_i = q~ . k'_i over the compacted rows, L' = log2 sum_i 2^(s'_i) (fp32);
+ * out is zero when counts[b,c] is 0.  counts are clamped to [0, c_max].
+ *   q_dec        [B, Hq, n_dec, d] bf16, contiguous, not scaled
+ *   k            [B, Hkv, T, d] dtype, strides k_strides (the prompt cache)
+ *   idx, counts  as returned by mmshiftkv_select_topk (c_max columns)
+ *   k_out, v_out [B, Hkv, c_max, d] dtype, contiguous (mmshiftkv_gather_kv)
+ *   coverage     [B, Hq, n_dec] fp32 out;  out [B, Hq, n_dec, d] fp32 out
+ * (Hq/Hkv) * n_dec <= 256 and c_max <= 2048 (else MMSKV_EUNSUPPORTED).
+ * Workspace: mmshiftkv_decode_workspace bytes (0 for an invalid shape). */
+size_t mmshiftkv_decode_workspace(const mmskv_shape *shape, int32_t n_dec);
+int mmshiftkv_decode_check(const mmskv_shape *shape, int32_t n_dec, const uint16_t *q_dec,
+                           const void *k, int32_t dtype, const mmskv_strides *k_strides,
+                           const int32_t *idx, const int32_t *counts, int32_t c_max,
+                           const void *k_out, const void *v_out, float *coverage, float *out,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
 /* Human-readable text for an mmskv_status value (static storage). */
 const char *mmshiftkv_status_string(int status);
 

@@ -24,7 +24,8 @@ EXPORTED = ("mmshiftkv_build_proxies", "mmshiftkv_score_workspace", "mmshiftkv_s
             "mmshiftkv_score_lse", "mmshiftkv_score_mass", "mmshiftkv_select_workspace",
             "mmshiftkv_select_topk", "mmshiftkv_gather_kv", "mmshiftkv_status_string",
             "mmshiftkv_version", "mmshiftkv_hidden_stats_workspace", "mmshiftkv_hidden_stats",
-            "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies")
+            "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies", "mmshiftkv_decode_workspace",
+            "mmshiftkv_decode_check")
 
 
 class Shape(ctypes.Structure):
@@ -84,12 +85,16 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_hidden_stats.argtypes = [PH, I32, V, I32, I64, I64, V, V, SZ, V]
     lib.mmshiftkv_hidden_proxies.argtypes = [PH, PP, V, V, V]
     lib.mmshiftkv_project_proxies.argtypes = [PH, I32, I32, I32, V, V, V, V, V, V]
+    lib.mmshiftkv_decode_workspace.argtypes = [PS, I32]
+    lib.mmshiftkv_decode_workspace.restype = SZ
+    lib.mmshiftkv_decode_check.argtypes = [PS, I32, V, V, I32, PT, V, V, I32, V, V, V, V, V, SZ, V]
     lib.mmshiftkv_status_string.argtypes = [ctypes.c_int]
     lib.mmshiftkv_status_string.restype = ctypes.c_char_p
     lib.mmshiftkv_version.restype = ctypes.c_int
     for name in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_score_lse",
                  "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_gather_kv",
-                 "mmshiftkv_hidden_stats", "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies"):
+                 "mmshiftkv_hidden_stats", "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies",
+                 "mmshiftkv_decode_check"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -370,6 +375,39 @@ def select_topk(s: ScoreOut, cfg: SelectionConfig, budget: int, c_max: int | Non
                                        _p(out.counts), _p(out.votes), _p(ws),
                                        ws.numel() * ws.element_size(), _stream(dev))
     _check("mmshiftkv_select_topk", rc)
+    return out
+
+
+def decode_workspace(B, Hq, Hkv, T, d, n_dec) -> int:
+    return int(load_library().mmshiftkv_decode_workspace(ctypes.byref(_shape(B, Hq, Hkv, T, 1, d)), int(n_dec)))
+
+
+def decode_check(q_dec: torch.Tensor, k: torch.Tensor, sel: Selected, k_out: torch.Tensor, v_out: torch.Tensor,
+                 workspace: torch.Tensor | None = None, out=None):
+    """mmshiftkv_decode_check: (coverage [B, Hq, n_dec] fp32, out [B, Hq, n_dec, d] fp32) of the
+    decode queries q_dec [B, Hq, n_dec, d] bf16 against the full cache k and the compacted
+    cache (k_out, v_out) of the selection `sel`."""
+    dev = _dev(k)
+    B, Hq, n_dec, d = q_dec.shape
+    Hkv, T = k.shape[1], k.shape[2]
+    if q_dec.dtype != torch.bfloat16 or not q_dec.is_contiguous():
+        raise ValueError("q_dec must be a contiguous bf16 tensor")
+    if k_out.dtype != k.dtype or v_out.dtype != k.dtype or not k_out.is_contiguous() or not v_out.is_contiguous():
+        raise ValueError("k_out and v_out must be contiguous and of k's dtype")
+    c_max = sel.idx.shape[2]
+    shape = _shape(B, Hq, Hkv, T, 1, d)
+    lib = load_library()
+    need = int(lib.mmshiftkv_decode_workspace(ctypes.byref(shape), int(n_dec)))
+    ws = workspace if workspace is not None else _ws(need, dev)
+    if out is None:
+        out = (torch.empty((B, Hq, n_dec), dtype=torch.float32, device=dev),
+               torch.empty((B, Hq, n_dec, d), dtype=torch.float32, device=dev))
+    with torch.cuda.device(dev):
+        rc = lib.mmshiftkv_decode_check(ctypes.byref(shape), int(n_dec), _p(q_dec), _p(k), _dtype_code(k),
+                                        ctypes.byref(_strides4(k)), _p(sel.idx), _p(sel.counts), c_max,
+                                        _p(k_out), _p(v_out), _p(out[0]), _p(out[1]), _p(ws),
+                                        ws.numel() * ws.element_size(), _stream(dev))
+    _check("mmshiftkv_decode_check", rc)
     return out
 
 

@@ -369,6 +369,79 @@ int mmshiftkv_gather_kv(const mmskv_shape* shape, const void* k, const void* v, 
     return status_of(launch_gather(a, static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+
+int check_decode(const mmskv_shape* shape, int32_t n_dec) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    if (n_dec < 1) return MMSKV_EINVAL;
+    const int64_t rows = static_cast<int64_t>(shape->Hq / shape->Hkv) * n_dec;
+    if (rows > decode_max_rows()) return MMSKV_EUNSUPPORTED;
+    return MMSKV_OK;
+}
+
+size_t decode_ws(const mmskv_shape* shape, int32_t n_dec) {
+    const int64_t Gh = shape->Hq / shape->Hkv;
+    return align_up(static_cast<size_t>(shape->B) * shape->Hkv * decode_key_blocks(shape->T) *
+                    decode_rows_pad(static_cast<int>(Gh), n_dec) * sizeof(float4));
+}
+
+}  // namespace
+
+size_t mmshiftkv_decode_workspace(const mmskv_shape* shape, int32_t n_dec) {
+    if (check_decode(shape, n_dec) != MMSKV_OK) return 0;
+    return decode_ws(shape, n_dec);
+}
+
+int mmshiftkv_decode_check(const mmskv_shape* shape, int32_t n_dec, const uint16_t* q_dec, const void* k,
+                           int32_t dtype, const mmskv_strides* k_strides, const int32_t* idx,
+                           const int32_t* counts, int32_t c_max, const void* k_out, const void* v_out,
+                           float* coverage, float* out, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+    int rc = check_decode(shape, n_dec);
+    if (rc) return rc;
+    const int eb = elem_bytes(dtype);
+    if (eb == 0 || q_dec == nullptr || k == nullptr || idx == nullptr || counts == nullptr ||
+        k_out == nullptr || v_out == nullptr || coverage == nullptr || out == nullptr)
+        return MMSKV_EINVAL;
+    if (c_max < 1) return MMSKV_EINVAL;
+    if (c_max > decode_max_compact()) return MMSKV_EUNSUPPORTED;
+    rc = check_rows(k, k_strides, eb, true);
+    if (rc) return rc;
+    if (!aligned(q_dec, 16) || !aligned(k_out, 16) || !aligned(v_out, 16) || !aligned(idx, 4) ||
+        !aligned(counts, 4) || !aligned(coverage, 4) || !aligned(out, 4))
+        return MMSKV_EINVAL;
+    if (workspace == nullptr || !aligned(workspace, kAlign) || workspace_bytes < decode_ws(shape, n_dec))
+        return MMSKV_EWORKSPACE;
+    DecodeArgs a = {};
+    a.q_dec = q_dec;
+    a.k = k;
+    a.k_dtype = dtype;
+    a.ksb = k_strides->sb;
+    a.ksh = k_strides->sh;
+    a.kst = k_strides->st;
+    a.idx = idx;
+    a.counts = counts;
+    a.k_out = k_out;
+    a.v_out = v_out;
+    a.B = shape->B;
+    a.Hq = shape->Hq;
+    a.Hkv = shape->Hkv;
+    a.T = shape->T;
+    a.d = shape->d;
+    a.Gh = shape->Hq / shape->Hkv;
+    a.n_dec = n_dec;
+    a.c_max = c_max;
+    a.rows = a.Gh * n_dec;
+    a.rows_pad = decode_rows_pad(a.Gh, n_dec);
+    a.n_kb = decode_key_blocks(shape->T);
+    a.scale = query_scale(shape->d);
+    a.part = static_cast<float4*>(workspace);
+    a.coverage = coverage;
+    a.out = out;
+    return status_of(launch_decode_check(a, static_cast<hipStream_t>(stream)));
+}
+
 size_t mmshiftkv_hidden_stats_workspace(const mmskv_hshape* shape) {
     if (check_hshape(shape)) return 0;
     return hidden_stats_ws(shape);

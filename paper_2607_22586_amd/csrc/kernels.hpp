@@ -92,6 +92,30 @@ struct ProjectArgs {
     int M, N, K, P, Hq, d;
 };
 
+struct DecodeArgs {
+    const uint16_t* q_dec;     // [B, Hq, n_dec, d] bf16, unscaled
+    const void* k;             // [B, Hkv, T, d] full prompt cache
+    int k_dtype;               // dtype of k, k_out and v_out
+    int64_t ksb, ksh, kst;
+    const int32_t* idx;        // [B, Hkv, c_max]
+    const int32_t* counts;     // [B, Hkv]
+    const void* k_out;         // [B, Hkv, c_max, d] compacted cache
+    const void* v_out;
+    int B, Hq, Hkv, T, d, Gh, n_dec, c_max;
+    int rows;                  // Gh * n_dec decode queries per KV head
+    int rows_pad;              // rows rounded up to 32
+    int n_kb;                  // key blocks
+    double scale;              // log2(e) / sqrt(d), applied to the queries
+    float4* part;              // [B, Hkv, n_kb, rows_pad] (max, sum all, sum kept), base 2
+    float* coverage;           // [B, Hq, n_dec]
+    float* out;                // [B, Hq, n_dec, d]
+};
+
+int decode_rows_pad(int Gh, int n_dec);
+int decode_key_blocks(int T);
+int decode_max_rows();
+int decode_max_compact();
+
 hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s);
 hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s);
 hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s);
@@ -100,5 +124,6 @@ hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 hipError_t launch_hidden_stats(const HiddenArgs& a, hipStream_t s);
 hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s);
 hipError_t launch_project(const ProjectArgs& p, hipStream_t s);
+hipError_t launch_decode_check(const DecodeArgs& a, hipStream_t s);
 
 }  // namespace mmskv

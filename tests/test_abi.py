@@ -216,3 +216,29 @@ def test_hidden_form_rejects(lib):
     assert proj(P=0) == bd.MMSKV_EINVAL
     assert proj(out=ctypes.c_void_p(0x10008)) == bd.MMSKV_EINVAL
     assert proj(rope=(FAKE, None)) == bd.MMSKV_EINVAL
+
+
+def test_decode_check_rejects(lib):
+    """Host validation of the decode-time check."""
+    s = _shape(B=1, Hq=4, Hkv=1, T=1024, W=16, d=64)
+    st = bd.Strides(1024 * 64, 1024 * 64, 64)
+    need = lib.mmshiftkv_decode_workspace(ctypes.byref(s), 8)
+    # (max, all, kept, pad) fp32 per (head, block of 256 keys, row padded to 32)
+    assert need >= 1 * 4 * 32 * 16 and need % 256 == 0
+    assert lib.mmshiftkv_decode_workspace(ctypes.byref(s), 0) == 0
+    assert lib.mmshiftkv_decode_workspace(ctypes.byref(s), 65) == 0            # Gh * n_dec > 256
+    call = lambda n_dec=8, q=FAKE, k=FAKE, dtype=1, c_max=64, ws=FAKE, nbytes=need, cov=FAKE, strides=st: \
+        lib.mmshiftkv_decode_check(ctypes.byref(s), n_dec, q, k, dtype, ctypes.byref(strides), FAKE, FAKE, c_max,  # noqa: E731
+                                   FAKE, FAKE, cov, FAKE, ws, nbytes, None)
+    assert call(n_dec=0) == bd.MMSKV_EINVAL
+    assert call(n_dec=65) == bd.MMSKV_EUNSUPPORTED
+    assert call(c_max=0) == bd.MMSKV_EINVAL
+    assert call(c_max=4096) == bd.MMSKV_EUNSUPPORTED
+    assert call(q=None) == bd.MMSKV_EINVAL
+    assert call(cov=None) == bd.MMSKV_EINVAL
+    assert call(q=ctypes.c_void_p(0x10008)) == bd.MMSKV_EINVAL              # q rows not 16-byte aligned
+    assert call(k=ctypes.c_void_p(0x10002)) == bd.MMSKV_EINVAL
+    assert call(strides=bd.Strides(0, 0, 3)) == bd.MMSKV_EINVAL
+    assert call(dtype=5) == bd.MMSKV_EINVAL
+    assert call(nbytes=need - 1) == bd.MMSKV_EWORKSPACE
+    assert call(ws=None) == bd.MMSKV_EWORKSPACE
