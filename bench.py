@@ -102,6 +102,78 @@ def cpu_baseline(w, cfg, layer_inputs, heads=1):
                       % (heads, w.T, dt)}
 
 
+def decode_check_bench(args):
+    """The decode-time check (Fig. 1b's attention-mass coverage of decode
+    queries on the kept prompt keys, and decode attention over the compacted
+    cache): the selection path runs once per layer, then K steps time the
+    check over all layers on one stream.  One JSON line."""
+    import torch
+    from paper_2607_22586_amd import binding as bd
+    from paper_2607_22586_amd import workloads as wl
+    bd.load_library()
+    dev = torch.device("cuda:0")
+    w = wl.WORKLOADS[args.workload]
+    L = args.layers or w.L
+    n = args.decode_check
+    B, Hq, Hkv, T, W, d = w.B, w.Hq, w.Hkv, w.T, w.W, w.d
+    log("generating %d layers of %s with %d decode queries per head" % (L, w.name, n))
+    layers = [wl.make_layer(w, l, device=dev, n_dec=n) for l in range(L)]
+    sels = []
+    for l, x in enumerate(layers):
+        cfg = bd.SelectionConfig(seed=w.wid, layer=l)
+        out = bd.select_layer(x["q_win"], x["k"], x["v"], w.budget, cfg)
+        sels.append(out)
+    ws = torch.empty(bd.decode_workspace(B, Hq, Hkv, T, d, n), dtype=torch.uint8, device=dev)
+    res = [(torch.empty((B, Hq, n), dtype=torch.float32, device=dev),
+            torch.empty((B, Hq, n, d), dtype=torch.float32, device=dev)) for _ in range(L)]
+
+    def step(ev=None):
+        for l in range(L):
+            if ev is not None:
+                ev[l][0].record()
+            bd.decode_check(layers[l]["q_dec"], layers[l]["k"], sels[l].sel, sels[l].k_out, sels[l].v_out,
+                            workspace=ws, out=res[l])
+            if ev is not None:
+                ev[l][1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(L)] for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for s_ in range(args.steps):
+        step(ev[s_])
+    t1.record()
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    call_ms = sum(ev[s_][l][0].elapsed_time(ev[s_][l][1]) for s_ in range(args.steps) for l in range(L)) / (args.steps * L)
+    eb = layers[0]["k"].element_size()
+    c_max = sels[0].sel.idx.shape[2]
+    # algorithmic bytes of one call: K once, the decode queries, the compacted
+    # K'/V' and indices, the outputs
+    nbytes = (B * Hkv * T * d * eb + B * Hq * n * d * 2 + 2 * B * Hkv * c_max * d * eb + B * Hkv * c_max * 4
+              + B * Hq * n * (d + 1) * 4)
+    achieved = nbytes / (call_ms * 1e-3) / 1e9
+    cov = torch.stack([r[0] for r in res]).double()
+    out = {
+        "metric": "decode queries checked/sec",
+        "value": B * Hq * n * L / (ms_step * 1e-3),
+        "unit": "queries/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "us_per_layer": ms_step * 1e3 / L, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "batch": B, "T": T, "Hq": Hq, "Hkv": Hkv, "d": d,
+                   "budget": w.budget, "n_dec": n, "decode_var_scale": wl.DECODE_VAR_SCALE},
+        "coverage": {"mean": float(cov.mean()), "min": float(cov.min()), "max": float(cov.max())},
+        "roofline": {"kernel": "decode check call (decode_cover_kernel + combine + decode_attend_kernel)",
+                     "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "bytes_per_call": nbytes, "us_per_call": call_ms * 1e3},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +187,8 @@ def main():
                     help="HIP streams the layers are spread over in the throughput steps "
                          "(layer l on stream l %% n); the kernel-timing steps use one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-check", type=int, default=0, metavar="N_DEC",
+                    help="time the decode-time coverage check with N_DEC decode queries per head instead")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -125,6 +199,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.decode_check > 0:
+        decode_check_bench(args)
         return
 
     import torch

@@ -223,8 +223,10 @@ def test_decode_check_rejects(lib):
     s = _shape(B=1, Hq=4, Hkv=1, T=1024, W=16, d=64)
     st = bd.Strides(1024 * 64, 1024 * 64, 64)
     need = lib.mmshiftkv_decode_workspace(ctypes.byref(s), 8)
-    # (max, all, kept, pad) fp32 per (head, block of 256 keys, row padded to 32)
-    assert need >= 1 * 4 * 32 * 16 and need % 256 == 0
+    # (max, all, kept, pad) fp32 per (head, block of 512 keys, row padded to 32)
+    assert need >= 1 * 1 * 32 * 16 and need % 256 == 0
+    s2 = _shape(B=2, Hq=4, Hkv=2, T=3000, W=16, d=128)
+    assert lib.mmshiftkv_decode_workspace(ctypes.byref(s2), 20) >= 2 * 2 * 6 * 64 * 16
     assert lib.mmshiftkv_decode_workspace(ctypes.byref(s), 0) == 0
     assert lib.mmshiftkv_decode_workspace(ctypes.byref(s), 65) == 0            # Gh * n_dec > 256
     call = lambda n_dec=8, q=FAKE, k=FAKE, dtype=1, c_max=64, ws=FAKE, nbytes=need, cov=FAKE, strides=st: \
