@@ -87,6 +87,10 @@ def _load():
     lib.oracle_query_scale.argtypes = [i32]
     lib.oracle_query_scale.restype = f64
     lib.oracle_project_proxies.restype = i32
+    lib.oracle_window_rows.argtypes = [i32, i32, i32, i32, i32, P, i32, P]
+    lib.oracle_window_rows.restype = i32
+    lib.oracle_shape_scores.argtypes = [i32, i32, i32, i32, i32, i32, i32, P, P]
+    lib.oracle_shape_scores.restype = i32
     lib.oracle_decode_check.argtypes = [i32, i32, i32, i32, i32, i32, P, P, i32, P, P, i32, P, P, i32, P, P]
     lib.oracle_decode_check.restype = i32
     _lib = lib
@@ -371,3 +375,55 @@ def decode_check(q_dec: np.ndarray, k: np.ndarray, idx: np.ndarray, counts: np.n
     if rc != 0:
         raise ValueError("oracle_decode_check rejected its arguments")
     return cov, out
+
+
+SHAPE_SNAPKV, SHAPE_STREAMING, SHAPE_SINKS = 0, 1, 2
+KEEP_SCORE = 2.0 ** 100
+
+
+def window_rows(q_win: np.ndarray, n: int) -> np.ndarray:
+    """The last n window queries of each head, scaled like the proxies (bf16 bits)."""
+    q_win = np.ascontiguousarray(q_win)
+    B, Hq, W, d = q_win.shape
+    rows = np.zeros((B, Hq, n, d), dtype=np.uint16)
+    if _load().oracle_window_rows(B, Hq, W, d, n, _ptr(q_win), _dtype_code(q_win), _ptr(rows)) != 0:
+        raise ValueError("oracle_window_rows rejected its arguments")
+    return rows
+
+
+def shape_scores(mass: np.ndarray, kind: int, window: int = 0, pool: int = 1, sinks: int = 0) -> np.ndarray:
+    """Per-key scores of the baseline selectors from a mass [B, Hkv, T] (fp64)."""
+    mass = np.ascontiguousarray(mass, dtype=np.float64)
+    B, Hkv, T = mass.shape
+    out = np.zeros_like(mass)
+    if _load().oracle_shape_scores(B, Hkv, T, int(kind), int(window), int(pool), int(sinks), _ptr(mass), _ptr(out)) != 0:
+        raise ValueError("oracle_shape_scores rejected its arguments")
+    return out
+
+
+def baseline_select(name: str, q_win, k, v, Hkv: int, budget: int, seed: int = 0, layer: int = 0,
+                    window: int = 32, pool: int = 5, sinks: int = 4, P: int = 512, c_max=None):
+    """The baseline selectors end to end (Sec. 4.1 baselines as configured in the
+    paper's appendix on them; LastAttn is the tau = 1 setting of select_layer).
+    Returns (selection, score [B, Hkv, T], mass [B, Hkv, T])."""
+    q_win = np.ascontiguousarray(q_win)
+    k = np.ascontiguousarray(k)
+    B, Hq, W, d = q_win.shape
+    T = k.shape[2]
+    if name == "snapkv":
+        rows = window_rows(q_win, window)
+        prox, ql, _ = build_proxies(q_win, 32, 0.0, seed, layer)   # q_last only (the anchor query)
+        _, mass, anchor = score(rows, ql, k, Hkv, 1)
+        sc = shape_scores(mass, SHAPE_SNAPKV, window=window, pool=pool)
+    elif name == "streaming":
+        mass = np.zeros((B, Hkv, T))
+        anchor = np.zeros((B, Hkv, T))
+        sc = shape_scores(mass, SHAPE_STREAMING, sinks=sinks)
+    elif name == "expected":
+        prox, ql, _ = build_proxies(q_win, P, 1.0, seed, layer)
+        _, mass, anchor = score(prox, ql, k, Hkv, 32)
+        sc = shape_scores(mass, SHAPE_SINKS, sinks=sinks)
+    else:
+        raise ValueError(name)
+    sel = select(None, sc, anchor, budget, 1.0, 0.0, MODE_MASS, keep_last=False, c_max=c_max)
+    return sel, sc, mass

@@ -864,6 +864,75 @@ int oracle_decode_check(int B, int Hq, int Hkv, int T, int d, int n_dec,
     return bad ? -1 : 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Baseline selectors on the same scoring and selection (the comparison     */
+/* methods of Sec. 4.1 as the paper configures them in its appendix on the  */
+/* baselines).  Each one becomes a per-key score that the MASS-mode top-C   */
+/* of oracle_select (keep_last = 0) turns into the kept set:                */
+/*   SnapKV: the attention of the last `window` prompt queries (rows from   */
+/*     oracle_window_rows, scored by oracle_score), summed over the GQA     */
+/*     group, average-pooled over the prompt keys before the window         */
+/*     (kernel `pool`, zero padding counted); the window itself is kept;    */
+/*   StreamingLLM: the first `sinks` keys and then the most recent ones;    */
+/*   ExpectedAttn: the proxy mass of N samples drawn without variance       */
+/*     expansion (gamma = 1), the first `sinks` keys kept.                  */
+/* A kept key gets score KEEP = 2^100, above any mass.                      */
+/* ------------------------------------------------------------------------ */
+
+/* the last n window queries of each head, scaled like the proxies
+ * (times log2(e)/sqrt(d) in fp64, then fp32, then bf16):
+ * q_win [B, Hq, W, d] dtype 0/1; rows [B, Hq, n, d] bf16 out */
+int oracle_window_rows(int B, int Hq, int W, int d, int n, const void *q_win, int dtype, uint16_t *rows)
+{
+    if (B < 1 || Hq < 1 || W < 1 || d < 1 || n < 1 || n > W)
+        return -1;
+    const double qs = oracle_query_scale(d);
+    for (int64_t bh = 0; bh < (int64_t)B * Hq; ++bh)
+        for (int i = 0; i < n; ++i)
+            for (int j = 0; j < d; ++j) {
+                /* window queries enter as bf16 values (fp32 inputs rounded first) */
+                double x = oracle_bf16_to_f64(oracle_f32_to_bf16((float)load_elem(q_win, dtype, (bh * W + (W - n + i)) * d + j)));
+                rows[(bh * n + i) * d + j] = oracle_f32_to_bf16((float)(x * qs));
+            }
+    return 0;
+}
+
+enum { ORACLE_SHAPE_SNAPKV = 0, ORACLE_SHAPE_STREAMING = 1, ORACLE_SHAPE_SINKS = 2 };
+
+/* mass [B, Hkv, T] fp64 in; score [B, Hkv, T] fp64 out */
+int oracle_shape_scores(int B, int Hkv, int T, int kind, int window, int pool, int sinks,
+                        const double *mass, double *score)
+{
+    const double keep = ldexp(1.0, 100);
+    if (B < 1 || Hkv < 1 || T < 1 || window < 0 || sinks < 0 || pool < 1 || (pool % 2) == 0)
+        return -1;
+    for (int64_t bc = 0; bc < (int64_t)B * Hkv; ++bc) {
+        const double *m = mass + bc * T;
+        double *o = score + bc * T;
+        for (int t = 0; t < T; ++t) {
+            if (kind == ORACLE_SHAPE_SNAPKV) {
+                const int prefix = T - window;
+                if (t >= prefix) {
+                    o[t] = keep;
+                } else {
+                    double s = 0.0;
+                    for (int u = t - pool / 2; u <= t + pool / 2; ++u)
+                        if (u >= 0 && u < prefix)
+                            s = s + m[u];
+                    o[t] = s / pool;
+                }
+            } else if (kind == ORACLE_SHAPE_STREAMING) {
+                o[t] = t < sinks ? keep : (double)t;
+            } else if (kind == ORACLE_SHAPE_SINKS) {
+                o[t] = t < sinks ? keep : m[t];
+            } else {
+                return -1;
+            }
+        }
+    }
+    return 0;
+}
+
 int oracle_num_threads(void)
 {
 #ifdef _OPENMP
