@@ -269,6 +269,43 @@ int mmshiftkv_decode_check(const mmskv_shape *shape, int32_t n_dec, const uint16
                            const void *k_out, const void *v_out, float *coverage, float *out,
                            void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---- Baseline selectors on the same kernels: the comparison methods of
+ * Sec. 4.1 with the settings of the paper's appendix on the baselines.  Each
+ * one is a per-key score for mmshiftkv_select_topk in MMSKV_MASS mode with
+ * keep_last = 0 (score = mass; a kept key scores 2^100, above any mass):
+ *   SnapKV        rows of mmshiftkv_window_rows (window 32) scored by
+ *                 mmshiftkv_score (P = 32, G = 1, MASS), then
+ *                 MMSKV_SHAPE_SNAPKV (pooling 5);
+ *   StreamingLLM  MMSKV_SHAPE_STREAMING (4 sinks, recency), no scoring;
+ *   ExpectedAttn  proxies with gamma = 1 (512 samples, no variance
+ *                 expansion) scored in MASS mode, then MMSKV_SHAPE_SINKS (4);
+ *   LastAttn      the method itself with tau = 1 (Table 5's first row).
+ *
+ * The last n window queries of each head in the form of proxies: window
+ * query w = W-n+i as a bf16 value (fp32 inputs rounded to nearest even),
+ * times log2(e)/sqrt(d) in fp64, rounded to fp32 then bf16, and q_last[b,h]
+ * = window query W-1 as a bf16 value (not scaled), as mmshiftkv_build_proxies
+ * gives it.  1 <= n <= W.
+ *   q_win  [B, Hq, W, d] q_dtype, strides q_strides (elements)
+ *   rows   [B, Hq, n, d] bf16 out, contiguous;  q_last [B, Hq, d] bf16 out */
+int mmshiftkv_window_rows(const mmskv_shape *shape, int32_t n, const void *q_win, int32_t q_dtype,
+                          const mmskv_strides *q_strides, uint16_t *rows, uint16_t *q_last, void *stream);
+
+typedef enum {
+    MMSKV_SHAPE_SNAPKV = 0,    /* keys t < T-window: average of mass[u] over
+                                  |u-t| <= pool/2, u < T-window, divided by
+                                  pool (zeros outside); t >= T-window kept */
+    MMSKV_SHAPE_STREAMING = 1, /* t < sinks kept, else score t (recency) */
+    MMSKV_SHAPE_SINKS = 2      /* t < sinks kept, else mass[t] */
+} mmskv_shape_kind;
+
+/* Per-key baseline score from a mass (fp32 sums in ascending u):
+ *   mass   [B, Hkv, T] fp32 (may be NULL for MMSKV_SHAPE_STREAMING)
+ *   score  [B, Hkv, T] fp32 out
+ * 0 <= window <= T, sinks >= 0, pool odd >= 1, T <= 2^24. */
+int mmshiftkv_shape_scores(const mmskv_shape *shape, int32_t kind, int32_t window, int32_t pool, int32_t sinks,
+                           const float *mass, float *score, void *stream);
+
 /* Human-readable text for an mmskv_status value (static storage). */
 const char *mmshiftkv_status_string(int status);
 

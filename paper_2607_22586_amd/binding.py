@@ -25,7 +25,7 @@ EXPORTED = ("mmshiftkv_build_proxies", "mmshiftkv_score_workspace", "mmshiftkv_s
             "mmshiftkv_select_topk", "mmshiftkv_gather_kv", "mmshiftkv_status_string",
             "mmshiftkv_version", "mmshiftkv_hidden_stats_workspace", "mmshiftkv_hidden_stats",
             "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies", "mmshiftkv_decode_workspace",
-            "mmshiftkv_decode_check")
+            "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores")
 
 
 class Shape(ctypes.Structure):
@@ -88,13 +88,15 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_decode_workspace.argtypes = [PS, I32]
     lib.mmshiftkv_decode_workspace.restype = SZ
     lib.mmshiftkv_decode_check.argtypes = [PS, I32, V, V, I32, PT, V, V, I32, V, V, V, V, V, SZ, V]
+    lib.mmshiftkv_window_rows.argtypes = [PS, I32, V, I32, PT, V, V, V]
+    lib.mmshiftkv_shape_scores.argtypes = [PS, I32, I32, I32, I32, V, V, V]
     lib.mmshiftkv_status_string.argtypes = [ctypes.c_int]
     lib.mmshiftkv_status_string.restype = ctypes.c_char_p
     lib.mmshiftkv_version.restype = ctypes.c_int
     for name in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_score_lse",
                  "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_gather_kv",
                  "mmshiftkv_hidden_stats", "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies",
-                 "mmshiftkv_decode_check"):
+                 "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -409,6 +411,71 @@ def decode_check(q_dec: torch.Tensor, k: torch.Tensor, sel: Selected, k_out: tor
                                         ws.numel() * ws.element_size(), _stream(dev))
     _check("mmshiftkv_decode_check", rc)
     return out
+
+
+MMSKV_SHAPE_SNAPKV, MMSKV_SHAPE_STREAMING, MMSKV_SHAPE_SINKS = 0, 1, 2
+
+
+def window_rows(q_win: torch.Tensor, n: int, T: int, Hkv: int):
+    """mmshiftkv_window_rows: (rows [B, Hq, n, d] bf16 scaled like proxies, q_last [B, Hq, d] bf16)."""
+    dev = _dev(q_win)
+    B, Hq, W, d = q_win.shape
+    rows = torch.empty((B, Hq, n, d), dtype=torch.bfloat16, device=dev)
+    ql = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    shape = _shape(B, Hq, Hkv, T, W, d)
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_window_rows(ctypes.byref(shape), int(n), _p(q_win), _dtype_code(q_win),
+                                                  ctypes.byref(_strides4(q_win)), _p(rows), _p(ql), _stream(dev))
+    _check("mmshiftkv_window_rows", rc)
+    return rows, ql
+
+
+def shape_scores(mass: torch.Tensor | None, kind: int, B: int, Hkv: int, T: int, window: int = 0, pool: int = 1,
+                 sinks: int = 0, out: torch.Tensor | None = None, device=None) -> torch.Tensor:
+    """mmshiftkv_shape_scores: per-key baseline scores [B, Hkv, T] fp32."""
+    dev = _dev(mass) if mass is not None else torch.device(device if device is not None else "cuda:0")
+    score = out if out is not None else torch.empty((B, Hkv, T), dtype=torch.float32, device=dev)
+    shape = _shape(B, Hkv, Hkv, T, 1, 64)
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_shape_scores(ctypes.byref(shape), int(kind), int(window), int(pool), int(sinks),
+                                                   _p(mass), _p(score), _stream(dev))
+    _check("mmshiftkv_shape_scores", rc)
+    return score
+
+
+BASELINES = ("snapkv", "streaming", "expected")
+
+
+def baseline_select(name: str, q_win, k, v, budget: int, seed: int = 0, layer: int = 0, window: int = 32,
+                    pool: int = 5, sinks: int = 4, P: int = 512, c_max=None):
+    """A baseline selector end to end on the library's kernels: (Selected, score, mass, k_out, v_out).
+    snapkv: window rows -> mass pass -> pooled scores; streaming: sinks + recency;
+    expected: gamma = 1 proxies -> mass pass -> sinks; then the MASS-mode top-C and the gather."""
+    B, Hkv, T, d = k.shape
+    Hq, W = q_win.shape[1], q_win.shape[2]
+    dev = _dev(k)
+    sel_cfg = SelectionConfig(mode=MMSKV_MASS, keep_last=False, seed=seed, layer=layer)
+    mass = None
+    anchor = torch.zeros((B, Hkv, T), dtype=torch.float32, device=dev)
+    if name == "snapkv":
+        rows, ql = window_rows(q_win, window, T, Hkv)
+        cfg = SelectionConfig(P=window, G=1, mode=MMSKV_MASS, seed=seed, layer=layer)
+        sc = score(rows, ql, k, cfg, W)
+        mass, anchor = sc.mass, sc.anchor
+        scores = shape_scores(mass, MMSKV_SHAPE_SNAPKV, B, Hkv, T, window=window, pool=pool)
+    elif name == "streaming":
+        scores = shape_scores(None, MMSKV_SHAPE_STREAMING, B, Hkv, T, sinks=sinks, device=dev)
+    elif name == "expected":
+        cfg = SelectionConfig(P=P, gamma=1.0, mode=MMSKV_MASS, seed=seed, layer=layer)
+        prox, ql = build_proxies(q_win, cfg, T, Hkv)
+        sc = score(prox, ql, k, cfg, W)
+        mass, anchor = sc.mass, sc.anchor
+        scores = shape_scores(mass, MMSKV_SHAPE_SINKS, B, Hkv, T, sinks=sinks)
+    else:
+        raise ValueError("unknown baseline %r" % name)
+    sel = select_topk(ScoreOut(None, scores, anchor), sel_cfg, budget, c_max, None, Hq, W)
+    ko, vo = gather_kv(k, v, sel)
+    return sel, scores, mass, ko, vo
 
 
 def gather_kv(k: torch.Tensor, v: torch.Tensor, sel: Selected, out=None):

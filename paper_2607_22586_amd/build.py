@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmmshiftkv.so")
-SOURCES = ["api.hip", "proxies.hip", "score.hip", "select.hip", "gather.hip", "hidden.hip", "decode.hip"]
+SOURCES = ["api.hip", "proxies.hip", "score.hip", "select.hip", "gather.hip", "hidden.hip", "decode.hip", "baselines.hip"]
 HEADERS = ["common.hpp", "kernels.hpp", "normal.hpp"]
 ARCH = "gfx950"
 

@@ -442,6 +442,55 @@ int mmshiftkv_decode_check(const mmskv_shape* shape, int32_t n_dec, const uint16
     return status_of(launch_decode_check(a, static_cast<hipStream_t>(stream)));
 }
 
+int mmshiftkv_window_rows(const mmskv_shape* shape, int32_t n, const void* q_win, int32_t q_dtype,
+                          const mmskv_strides* q_strides, uint16_t* rows, uint16_t* q_last, void* stream) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    const int eb = elem_bytes(q_dtype);
+    if (eb == 0 || q_win == nullptr || rows == nullptr || q_last == nullptr) return MMSKV_EINVAL;
+    if (n < 1 || n > shape->W) return MMSKV_EINVAL;
+    rc = check_rows(q_win, q_strides, eb, false);
+    if (rc) return rc;
+    if (!aligned(rows, 2) || !aligned(q_last, 2)) return MMSKV_EINVAL;
+    WindowArgs a;
+    a.q = q_win;
+    a.q_dtype = q_dtype;
+    a.qsb = q_strides->sb;
+    a.qsh = q_strides->sh;
+    a.qst = q_strides->st;
+    a.B = shape->B;
+    a.Hq = shape->Hq;
+    a.W = shape->W;
+    a.d = shape->d;
+    a.n = n;
+    a.scale = query_scale(shape->d);
+    a.rows = rows;
+    a.q_last = q_last;
+    return status_of(launch_window_rows(a, static_cast<hipStream_t>(stream)));
+}
+
+int mmshiftkv_shape_scores(const mmskv_shape* shape, int32_t kind, int32_t window, int32_t pool, int32_t sinks,
+                           const float* mass, float* score, void* stream) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    if (score == nullptr || !aligned(score, 4)) return MMSKV_EINVAL;
+    if (kind < MMSKV_SHAPE_SNAPKV || kind > MMSKV_SHAPE_SINKS) return MMSKV_EINVAL;
+    if (kind != MMSKV_SHAPE_STREAMING && (mass == nullptr || !aligned(mass, 4))) return MMSKV_EINVAL;
+    if (window < 0 || window > shape->T || sinks < 0 || pool < 1 || pool % 2 == 0) return MMSKV_EINVAL;
+    if (shape->T > (1 << 24)) return MMSKV_EUNSUPPORTED;
+    ShapeArgs a;
+    a.mass = mass;
+    a.score = score;
+    a.B = shape->B;
+    a.Hkv = shape->Hkv;
+    a.T = shape->T;
+    a.kind = kind;
+    a.window = window;
+    a.pool = pool;
+    a.sinks = sinks;
+    return status_of(launch_shape_scores(a, static_cast<hipStream_t>(stream)));
+}
+
 size_t mmshiftkv_hidden_stats_workspace(const mmskv_hshape* shape) {
     if (check_hshape(shape)) return 0;
     return hidden_stats_ws(shape);

@@ -111,6 +111,22 @@ struct DecodeArgs {
     float* out;                // [B, Hq, n_dec, d]
 };
 
+struct WindowArgs {
+    const void* q;             // [B, Hq, W, d] window queries
+    int q_dtype;
+    int64_t qsb, qsh, qst;
+    int B, Hq, W, d, n;
+    double scale;              // log2(e) / sqrt(d)
+    uint16_t* rows;            // [B, Hq, n, d] bf16
+    uint16_t* q_last;          // [B, Hq, d] bf16
+};
+
+struct ShapeArgs {
+    const float* mass;         // [B, Hkv, T] (unused by StreamingLLM)
+    float* score;              // [B, Hkv, T]
+    int B, Hkv, T, kind, window, pool, sinks;
+};
+
 int decode_rows_pad(int Gh, int n_dec);
 int decode_key_blocks(int T);
 int decode_max_rows();
@@ -125,5 +141,7 @@ hipError_t launch_hidden_stats(const HiddenArgs& a, hipStream_t s);
 hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s);
 hipError_t launch_project(const ProjectArgs& p, hipStream_t s);
 hipError_t launch_decode_check(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_window_rows(const WindowArgs& a, hipStream_t s);
+hipError_t launch_shape_scores(const ShapeArgs& a, hipStream_t s);
 
 }  // namespace mmskv

@@ -244,3 +244,24 @@ def test_decode_check_rejects(lib):
     assert call(dtype=5) == bd.MMSKV_EINVAL
     assert call(nbytes=need - 1) == bd.MMSKV_EWORKSPACE
     assert call(ws=None) == bd.MMSKV_EWORKSPACE
+
+
+def test_baseline_calls_reject(lib):
+    """Host validation of the baseline-selector calls."""
+    s = _shape(B=1, Hq=4, Hkv=1, T=1024, W=16, d=64)
+    st = bd.Strides(16 * 64, 16 * 64, 64)
+    rows = lambda n=8, q=FAKE, dtype=1, out=FAKE: lib.mmshiftkv_window_rows(  # noqa: E731
+        ctypes.byref(s), n, q, dtype, ctypes.byref(st), out, FAKE, None)
+    assert rows(n=0) == bd.MMSKV_EINVAL
+    assert rows(n=17) == bd.MMSKV_EINVAL              # more rows than window queries
+    assert rows(q=None) == bd.MMSKV_EINVAL
+    assert rows(dtype=4) == bd.MMSKV_EINVAL
+    assert rows(out=None) == bd.MMSKV_EINVAL
+    shp = lambda kind=0, window=32, pool=5, sinks=4, mass=FAKE, score=FAKE: lib.mmshiftkv_shape_scores(  # noqa: E731
+        ctypes.byref(s), kind, window, pool, sinks, mass, score, None)
+    assert shp(kind=3) == bd.MMSKV_EINVAL
+    assert shp(pool=4) == bd.MMSKV_EINVAL             # even pooling kernel
+    assert shp(window=2000) == bd.MMSKV_EINVAL        # window longer than the prompt
+    assert shp(mass=None) == bd.MMSKV_EINVAL          # SnapKV needs the masses
+    assert shp(score=None) == bd.MMSKV_EINVAL
+    assert shp(sinks=-1) == bd.MMSKV_EINVAL
