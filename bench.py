@@ -174,6 +174,70 @@ def decode_check_bench(args):
     print(json.dumps(out), flush=True)
 
 
+def selectors_bench(args):
+    """The method and the baseline selectors (LastAttn = tau 1, SnapKV,
+    StreamingLLM, ExpectedAttn) on the same kernels: per selector, K timed
+    steps of its whole selection path over all layers on one stream, and the
+    mean decode-time coverage of its kept keys (the synthetic analogue of
+    Fig. 1b) for N_DEC decode queries per head.  One JSON line."""
+    import torch
+    from paper_2607_22586_amd import binding as bd
+    from paper_2607_22586_amd import workloads as wl
+    bd.load_library()
+    dev = torch.device("cuda:0")
+    w = wl.WORKLOADS[args.workload]
+    L = args.layers or w.L
+    n_dec = args.selectors
+    B, Hq, Hkv, T, W, d = w.B, w.Hq, w.Hkv, w.T, w.W, w.d
+    log("generating %d layers of %s" % (L, w.name))
+    layers = [wl.make_layer(w, l, device=dev, n_dec=n_dec) for l in range(L)]
+
+    def run(name, l):
+        x = layers[l]
+        if name in ("mm-shiftkv", "lastattn"):
+            cfg = bd.SelectionConfig(seed=w.wid, layer=l, tau=1.0 if name == "lastattn" else 0.95)
+            o = bd.select_layer(x["q_win"], x["k"], x["v"], w.budget, cfg)
+            return o.sel, o.k_out, o.v_out
+        sel, _, _, ko, vo = bd.baseline_select(name, x["q_win"], x["k"], x["v"], w.budget, seed=w.wid, layer=l)
+        return sel, ko, vo
+
+    res = {}
+    for name in ("mm-shiftkv", "lastattn", "snapkv", "expected", "streaming"):
+        for _ in range(args.warmup):
+            for l in range(L):
+                run(name, l)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(args.steps):
+            for l in range(L):
+                run(name, l)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        covs = []
+        for l in range(L):
+            sel, ko, vo = run(name, l)
+            cov, _ = bd.decode_check(layers[l]["q_dec"], layers[l]["k"], sel, ko, vo)
+            covs.append(cov.double())
+        cov = torch.stack(covs)
+        res[name] = {"us_per_layer": ms * 1e3 / L, "keys_per_s": B * L * T / (ms * 1e-3),
+                     "coverage_mean": float(cov.mean()), "coverage_p10": float(torch.quantile(cov.flatten().float(), 0.1))}
+        log("%s: %.1f us/layer, coverage %.4f" % (name, ms * 1e3 / L, res[name]["coverage_mean"]))
+    out = {
+        "metric": "selectors on the same kernels: throughput and decode-time coverage",
+        "value": res["mm-shiftkv"]["coverage_mean"], "unit": "mean coverage (mm-shiftkv)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+        "data": "synthetic", "dtype": "bf16",
+        "config": {"workload": w.name, "layers": L, "batch": B, "T": T, "Hq": Hq, "Hkv": Hkv, "d": d,
+                   "budget": w.budget, "n_dec": n_dec, "decode_var_scale": wl.DECODE_VAR_SCALE,
+                   "snapkv": {"window": 32, "pool": 5}, "streaming": {"sinks": 4},
+                   "expected": {"samples": 512, "gamma": 1.0, "sinks": 4}, "lastattn": {"tau": 1.0}},
+        "selectors": res,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -189,6 +253,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-check", type=int, default=0, metavar="N_DEC",
                     help="time the decode-time coverage check with N_DEC decode queries per head instead")
+    ap.add_argument("--selectors", type=int, default=0, metavar="N_DEC",
+                    help="compare the method with the baseline selectors (throughput and decode-time "
+                         "coverage with N_DEC decode queries per head) instead")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -202,6 +269,9 @@ def main():
         return
     if args.decode_check > 0:
         decode_check_bench(args)
+        return
+    if args.selectors > 0:
+        selectors_bench(args)
         return
 
     import torch
