@@ -68,7 +68,7 @@ int status_of(hipError_t e) { return e == hipSuccess ? MMSKV_OK : MMSKV_EHIP; }
 
 struct ScoreLayout {
     int block_keys, n_kb, rows, rows_pad;
-    size_t part_bytes, lse_off, ref_off, total;
+    size_t part_bytes, lse_off, total;
 };
 
 ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
@@ -81,8 +81,7 @@ ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
     const size_t heads = static_cast<size_t>(s->B) * s->Hkv;
     l.part_bytes = heads * l.n_kb * l.rows_pad * sizeof(float2);
     l.lse_off = align_up(l.part_bytes);
-    l.ref_off = l.lse_off + align_up(heads * l.rows_pad * sizeof(float));
-    l.total = l.ref_off + align_up(heads * l.rows_pad * sizeof(float));
+    l.total = l.lse_off + align_up(heads * l.rows_pad * sizeof(float));
     return l;
 }
 
@@ -140,7 +139,6 @@ int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const ui
     a->anchor_scale = query_scale(shape->d);
     a->part = static_cast<float2*>(ws);
     a->lse = reinterpret_cast<float*>(static_cast<char*>(ws) + l.lse_off);
-    a->ref = reinterpret_cast<float*>(static_cast<char*>(ws) + l.ref_off);
     a->group_mass = nullptr;
     a->mass = nullptr;
     a->anchor = nullptr;

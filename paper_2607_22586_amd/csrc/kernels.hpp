@@ -39,7 +39,6 @@ struct ScoreArgs {
     double anchor_scale;       // log2(e) / sqrt(d), applied to the anchor rows
     float2* part;              // [B, Hkv, n_kb, rows_pad]  (max, sum), base 2
     float* lse;                // [B, Hkv, rows_pad]        log2-domain
-    float* ref;                // [B, Hkv, rows_pad]        row reference (base-2 logit)
     float* group_mass;         // [B, Hkv, G, T] or null
     float* mass;               // [B, Hkv, T]
     float* anchor;             // [B, Hkv, T]

@@ -244,15 +244,16 @@ constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batc
 
 // Pass 1 in the K * P^T layout: lane l holds proxy column l % 32 of a tile and
 // keys key0 + 32*s + 8*(i/4) + 4*(l/32) + i%4 of sub-tile s (value 16*s + i of
-// the lane).  Each row r carries a reference m_r (the largest logit over a
-// sample of the keys, from row_ref_kernel, so the row's own maximum is at
-// least m_r and its sum of 2^(s - m_r) at least one): the accumulator starts
-// at -m_r, so the MFMA leaves s - m_r and every logit costs one exp and one
-// add.  Per tile and column the pair (m_r, l = sum 2^(s - m_r) over the
-// wave's 64 keys) goes to LDS; if some lane's sum reaches 2^64 (a key far
-// above the sample) the whole wave recomputes that tile with its exact
-// maximum instead.  The waves' pairs are merged every kMergeTiles tiles into
-// one partial per (row, key block).  FULL: every key of the block is < T.
+// the lane).  The accumulators start at zero, so the MFMA leaves the base-2
+// logit s itself and every logit costs one exp and one add: per tile and
+// column the pair (0, l = sum 2^s over the wave's 64 keys) goes to LDS.  This
+// is exact while every lane's sum of its 32 terms lies in [2^-60, 2^120):
+// below 2^120 nothing overflows, and at 2^-60 or more the terms that underflow
+// (each below 2^-126) are negligible against the sum.  Otherwise (logits
+// beyond about +/-100) the whole wave takes the tile again relative to its
+// exact per-column maximum m, writing (m, sum 2^(s - m)).  The waves' pairs
+// are merged every kMergeTiles tiles into one partial per (row, key block)
+// by the max-and-rescale rule.  FULL: every key of the block is < T.
 template <int D, int WAVES, bool FULL>
 __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, int b, int c,
                                          u32x4 (&stage)[kRing][TileLds<D>::kSlots],
@@ -287,8 +288,6 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     };
 
     float2* part = a.part + (static_cast<int64_t>(head) * a.n_kb + kb) * a.rows_pad;
-    // this lane's row of tile t: the reference of row 32t + lane % 32
-    const float* refs = a.ref + static_cast<int64_t>(head) * a.rows_pad + (lane & 31);
     // merged (max, sum) over the waves of tiles [16k, 16k+16), all threads
     auto merge_chunk = [&](int k) {
         const int n_in = min(kMergeTiles, n_tiles - kMergeTiles * k);
@@ -329,12 +328,6 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     floatx16 acc[2][kSub];
     auto value = [&](const floatx16 (&ac)[kSub], int idx) { return ac[idx >> 4][idx & 15]; };
     auto ok = [&](int idx) { return FULL || ((valid >> idx) & 1u); };
-    // row references: tile t's in ref_cur (accumulator start), tile t-1's in
-    // ref_prev (written with its sum), tiles t+1 / t+2 fetched ahead
-    float ref_cur = refs[0];
-    float ref_n1 = n_tiles > 1 ? refs[32] : 0.f;
-    float ref_n2 = n_tiles > 2 ? refs[64] : 0.f;
-    float ref_prev = 0.f;
     // One pipeline iteration; STATS: tile t-1 exists.  FAST: tile t exists,
     // tile t+3 is staged and tile t+4 is a proxy tile.
     auto iter = [&](auto t4, auto stats, auto fast, int t) {
@@ -343,16 +336,13 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         constexpr int cur = T4 & 1, prev = cur ^ 1;
         const u32x4* next = stage[(T4 + 1) % kRing];
         const bool mfma_on = FAST || t < n_tiles;
-        floatx16 cstart;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) cstart[i] = -ref_cur;
         float l0 = 0.f, l1 = 0.f;
 #pragma unroll
         for (int kc = 0; kc < D / 16; ++kc) {
 #pragma unroll
             for (int s = 0; s < kSub; ++s) {
                 const int slot = kSub * kc + s;
-                if (mfma_on) acc[cur][s] = mfma32(kf[s][kc], A[kc], kc == 0 ? cstart : acc[cur][s]);
+                if (mfma_on) acc[cur][s] = mfma32(kf[s][kc], A[kc], kc == 0 ? zero16() : acc[cur][s]);
                 if (STATS) {
 #pragma unroll
                     for (int q = 0; q < kPer; ++q) {
@@ -377,9 +367,10 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         if (STATS) {
             const int tp = t - 1;
             float lsum = l0 + l1;
-            float mrow = ref_prev;
-            if (__ballot(!(lsum < 0x1p64f)) != 0) {
-                // a key far above the sample: this tile again with its own maximum
+            float mrow = 0.f;
+            const bool in_range = (lsum >= 0x1p-60f || (!FULL && valid == 0u)) && lsum < 0x1p120f;
+            if (__ballot(!in_range) != 0) {
+                // logits out of the range: this tile again with its own maximum
                 float mx = -INFINITY;
 #pragma unroll
                 for (int idx = 0; idx < 32; ++idx) mx = fmaxf(mx, ok(idx) ? value(acc[prev], idx) : -INFINITY);
@@ -388,20 +379,18 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
                 if (mx != -INFINITY) {
 #pragma unroll
                     for (int idx = 0; idx < 32; ++idx) ls += ok(idx) ? fast_exp2(value(acc[prev], idx) - mx) : 0.f;
-                    mrow = ref_prev + mx;
+                    mrow = mx;
                 }
                 lsum = ls;
             }
             const float l = pair_total(lsum);
+            // an empty sum (no valid key) carries no maximum, so it cannot
+            // outweigh the pairs it is merged with
+            if (!(l > 0.f)) mrow = -INFINITY;
             if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(mrow, l);
             if (T4 == 1 && tp >= kMergeTiles && (tp - kMergeTiles) % kMergeTiles == 0)
                 merge_chunk((tp - kMergeTiles) / kMergeTiles);
         }
-        // advance the references: tile t becomes the previous one
-        ref_prev = ref_cur;
-        ref_cur = ref_n1;
-        ref_n1 = ref_n2;
-        ref_n2 = t + 3 < n_tiles ? refs[32 * (t + 3)] : 0.f;
         if ((T4 & 1) == 0) __syncthreads();
     };
     using Off = Tag<0>;
@@ -425,66 +414,6 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     // chunk k was merged in iteration 16k+17 when that iteration ran (t <= n_tiles)
     const int merged = n_tiles >= kMergeTiles + 1 ? (n_tiles - kMergeTiles - 1) / kMergeTiles + 1 : 0;
     for (int k = merged; k * kMergeTiles < n_tiles; ++k) merge_chunk(k);
-}
-
-// Row references for pass 1: per (b, c) and row r of the padded row space,
-// the largest base-2 logit q~_r . k_t over 64 sampled keys t_i = floor(i T / 64).
-// It is at most the row's maximum over all T keys (the sample is a subset),
-// so the pass-1 sums taken relative to it are at least one.  One wave per
-// (32-row tile, head), in the K * P^T layout of pass 1.
-template <int D>
-__global__ void __launch_bounds__(64) row_ref_kernel(ScoreArgs a) {
-    constexpr int KC = D / 16;
-    const int tile = blockIdx.x, head = blockIdx.y;
-    const int b = head / a.Hkv, c = head - b * a.Hkv;
-    const int lane = lane_id();
-    const int col = 8 * (lane >> 5);
-    bf16x8 kf[kSub][KC];
-#pragma unroll
-    for (int s = 0; s < kSub; ++s) {
-        const int i = 32 * s + (lane & 31);
-        const int t = static_cast<int>(static_cast<int64_t>(i) * a.T / 64);
-        const int64_t off = static_cast<int64_t>(b) * a.ksb + static_cast<int64_t>(c) * a.ksh +
-                            static_cast<int64_t>(t) * a.kst + col;
-        if (a.k_dtype == 1) {
-#pragma unroll
-            for (int kc = 0; kc < KC; ++kc) kf[s][kc] = load_bf16x8(static_cast<const uint16_t*>(a.k) + off + 16 * kc);
-        } else {
-#pragma unroll
-            for (int kc = 0; kc < KC; ++kc) kf[s][kc] = load_f32_as_bf16x8(static_cast<const float*>(a.k) + off + 16 * kc);
-        }
-    }
-    // row fragments: row 32*tile + lane % 32, chunks 2*kc + lane/32 (anchor
-    // rows scaled like the proxies, as in pass 1's staging)
-    const int row = 32 * tile + (lane & 31);
-    const uint16_t* rp = row_ptr<D>(a, b, c, row);
-    bf16x8 B[KC];
-#pragma unroll
-    for (int kc = 0; kc < KC; ++kc) {
-        u32x4 v = *reinterpret_cast<const u32x4*>(rp + 8 * (2 * kc + (lane >> 5)));
-        if (row >= a.rows) {
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                const double lo = static_cast<double>(__uint_as_float(v[w] << 16)) * a.anchor_scale;
-                const double hi = static_cast<double>(__uint_as_float(v[w] & 0xFFFF0000u)) * a.anchor_scale;
-                v[w] = f32_to_bf16_bits(static_cast<float>(lo)) | (f32_to_bf16_bits(static_cast<float>(hi)) << 16);
-            }
-        }
-        B[kc] = __builtin_bit_cast(bf16x8, v);
-    }
-    floatx16 acc[kSub];
-#pragma unroll
-    for (int s = 0; s < kSub; ++s) {
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc) acc[s] = mfma32(kf[s][kc], B[kc], kc == 0 ? zero16() : acc[s]);
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int s = 0; s < kSub; ++s)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[s][i]);
-    mx = pair_max(mx);
-    if (lane < 32) a.ref[static_cast<int64_t>(head) * a.rows_pad + row] = mx;
 }
 
 template <int D, int WAVES>
@@ -797,9 +726,6 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
 
 template <int D, int WAVES>
 hipError_t lse_impl(const ScoreArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((row_ref_kernel<D>), dim3(a.rows_pad / 32, a.B * a.Hkv), dim3(64), 0, s, a);
-    hipError_t e0 = hipGetLastError();
-    if (e0 != hipSuccess) return e0;
     hipLaunchKernelGGL((score_lse_kernel<D, WAVES>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
