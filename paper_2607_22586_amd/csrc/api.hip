@@ -378,10 +378,18 @@ int check_decode(const mmskv_shape* shape, int32_t n_dec) {
     return MMSKV_OK;
 }
 
-size_t decode_ws(const mmskv_shape* shape, int32_t n_dec) {
+// partials, then the scaled decode queries
+size_t decode_part_bytes(const mmskv_shape* shape, int32_t n_dec) {
     const int64_t Gh = shape->Hq / shape->Hkv;
     return align_up(static_cast<size_t>(shape->B) * shape->Hkv * decode_key_blocks(shape->T) *
                     decode_rows_pad(static_cast<int>(Gh), n_dec) * sizeof(float4));
+}
+
+size_t decode_ws(const mmskv_shape* shape, int32_t n_dec) {
+    const int64_t Gh = shape->Hq / shape->Hkv;
+    return decode_part_bytes(shape, n_dec) +
+           align_up(static_cast<size_t>(shape->B) * shape->Hkv * decode_rows_pad(static_cast<int>(Gh), n_dec) *
+                    shape->d * sizeof(uint16_t));
 }
 
 }  // namespace
@@ -435,6 +443,7 @@ int mmshiftkv_decode_check(const mmskv_shape* shape, int32_t n_dec, const uint16
     a.n_kb = decode_key_blocks(shape->T);
     a.scale = query_scale(shape->d);
     a.part = static_cast<float4*>(workspace);
+    a.qsc = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + decode_part_bytes(shape, n_dec));
     a.coverage = coverage;
     a.out = out;
     return status_of(launch_decode_check(a, static_cast<hipStream_t>(stream)));

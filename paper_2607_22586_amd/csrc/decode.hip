@@ -4,8 +4,8 @@
 // compacted cache (Sec. 3.1's prefill-only protocol).
 //
 // Coverage: one workgroup of 4 waves per (b, c, block of 512 keys).  The
-// Gh * n_dec decode queries of KV head c are scaled like the anchor query
-// (log2(e)/sqrt(d) in fp64, then fp32, then bf16), staged once in LDS, and
+// Gh * n_dec decode queries of KV head c, scaled once like the anchor query
+// (log2(e)/sqrt(d) in fp64, then fp32, then bf16), are staged in LDS and
 // streamed past the block's keys in 32-row tiles with v_mfma_f32_32x32x16_bf16
 // in the K * Q^T layout (lane = query row, its 32 values = its keys), so a
 // row's block statistics are in-lane sums.  Per (row, block) the kernel
@@ -49,6 +49,28 @@ __device__ __forceinline__ uint32_t scaled_bf16(uint32_t bits16, double scale) {
     return f32_to_bf16_bits(static_cast<float>(v));
 }
 
+// the decode queries of each KV head scaled once, in the coverage kernel's
+// row order (row r = head c*Gh + r / n_dec, query r % n_dec; rows past
+// Gh * n_dec zero): qsc [B*Hkv, rows_pad, d] bf16; one 16-byte chunk per thread
+__global__ void __launch_bounds__(256) decode_scale_kernel(DecodeArgs a) {
+    const int chunks = a.d / 8;
+    const int i = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x);
+    const int bc = blockIdx.y;
+    if (i >= a.rows_pad * chunks) return;
+    const int r = i / chunks, ch = i - r * chunks;
+    const int b = bc / a.Hkv, c = bc - b * a.Hkv;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < a.rows) {
+        const int h = c * a.Gh + r / a.n_dec, j = r - (r / a.n_dec) * a.n_dec;
+        const u32x4 raw = *reinterpret_cast<const u32x4*>(
+            a.q_dec + ((static_cast<int64_t>(b) * a.Hq + h) * a.n_dec + j) * a.d + 8 * ch);
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+            v[w] = scaled_bf16(raw[w] & 0xFFFFu, a.scale) | (scaled_bf16(raw[w] >> 16, a.scale) << 16);
+    }
+    *reinterpret_cast<u32x4*>(a.qsc + (static_cast<int64_t>(bc) * a.rows_pad + r) * a.d + 8 * ch) = v;
+}
+
 template <int D>
 __global__ void __launch_bounds__(64 * kDecWaves) decode_cover_kernel(DecodeArgs a) {
     constexpr int KC = D / 16;                 // 16-element k steps
@@ -62,21 +84,6 @@ __global__ void __launch_bounds__(64 * kDecWaves) decode_cover_kernel(DecodeArgs
     const int tid = threadIdx.x, wave = tid / kWave, lane = lane_id();
     const int key_base = kb * kDecKeys;
 
-    // scaled queries: row r = (head c*Gh + r / n_dec, query r % n_dec); rows
-    // past Gh * n_dec are zero
-    for (int i = tid; i < a.rows_pad * (D / 8); i += 64 * kDecWaves) {
-        const int r = i / (D / 8), ch = i - r * (D / 8);
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (r < a.rows) {
-            const int h = c * a.Gh + r / a.n_dec, j = r - (r / a.n_dec) * a.n_dec;
-            const u32x4 raw = *reinterpret_cast<const u32x4*>(
-                a.q_dec + ((static_cast<int64_t>(b) * a.Hq + h) * a.n_dec + j) * D + 8 * ch);
-#pragma unroll
-            for (int w = 0; w < 4; ++w)
-                v[w] = scaled_bf16(raw[w] & 0xFFFFu, a.scale) | (scaled_bf16(raw[w] >> 16, a.scale) << 16);
-        }
-        qs[r * kRow + ch] = v;
-    }
     // kept flags of this block's keys (idx is any list of in-range indices)
     if (tid < kDecKeys / 32) kept[tid] = 0u;
     __syncthreads();
@@ -108,6 +115,12 @@ __global__ void __launch_bounds__(64 * kDecWaves) decode_cover_kernel(DecodeArgs
     };
 #pragma unroll
     for (int sb = 0; sb < kDecSub; ++sb) load_keys(kfs[sb], key_base + 256 * sb + 64 * wave);
+    // the head's scaled queries (decode_scale_kernel), copied to LDS while the keys arrive
+    const u32x4* qsrc = reinterpret_cast<const u32x4*>(a.qsc + static_cast<int64_t>(bc) * a.rows_pad * D);
+    for (int i = tid; i < a.rows_pad * (D / 8); i += 64 * kDecWaves) {
+        const int r = i / (D / 8), ch = i - r * (D / 8);
+        qs[r * kRow + ch] = qsrc[i];
+    }
     // per (wave, row) running (m, sum all, sum kept), merged over the sub-blocks
     for (int r = lane; r < a.rows_pad; r += kWave) part[wave][r] = make_float4(-INFINITY, 0.f, 0.f, 0.f);
     __syncthreads();
@@ -140,27 +153,43 @@ __global__ void __launch_bounds__(64 * kDecWaves) decode_cover_kernel(DecodeArgs
 #pragma unroll
                 for (int s = 0; s < 2; ++s) acc[s] = mfma_32x32x16(kf[s][kc], q, acc[s]);
             }
-            float mx = -INFINITY;
+            // sums of 2^s relative to 0 while every lane's sum is in
+            // [2^-60, 2^120) (as in the row log-sum-exp pass), else relative
+            // to the exact per-column maximum
+            float mx = 0.f, la = 0.f, lk = 0.f;
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if ((valid >> (16 * s + i)) & 1u) mx = fmaxf(mx, acc[s][i]);
-            mx = pair_max2(mx);
-            float la = 0.f, lk = 0.f;
-            if (mx != -INFINITY) {
+                for (int i = 0; i < 16; ++i) {
+                    const float e = ((valid >> (16 * s + i)) & 1u) ? fast_exp2(acc[s][i]) : 0.f;
+                    la += e;
+                    lk += ((keep >> (16 * s + i)) & 1u) ? e : 0.f;
+                }
+            const bool in_range = (la >= 0x1p-60f || valid == 0u) && la < 0x1p120f;
+            if (__ballot(!in_range) != 0) {
+                mx = -INFINITY;
 #pragma unroll
                 for (int s = 0; s < 2; ++s)
 #pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const float e = ((valid >> (16 * s + i)) & 1u) ? fast_exp2(acc[s][i] - mx) : 0.f;
-                        la += e;
-                        lk += ((keep >> (16 * s + i)) & 1u) ? e : 0.f;
-                    }
+                    for (int i = 0; i < 16; ++i)
+                        if ((valid >> (16 * s + i)) & 1u) mx = fmaxf(mx, acc[s][i]);
+                mx = pair_max2(mx);
+                la = 0.f;
+                lk = 0.f;
+                if (mx != -INFINITY) {
+#pragma unroll
+                    for (int s = 0; s < 2; ++s)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const float e = ((valid >> (16 * s + i)) & 1u) ? fast_exp2(acc[s][i] - mx) : 0.f;
+                            la += e;
+                            lk += ((keep >> (16 * s + i)) & 1u) ? e : 0.f;
+                        }
+                }
             }
             la = pair_sum2(la);
             lk = pair_sum2(lk);
-            if (lane < 32 && mx != -INFINITY) {
+            if (lane < 32 && la > 0.f) {
                 const float4 o = part[wave][r0 + lane];
                 const float M = fmaxf(o.x, mx);
                 const float fo = o.x == -INFINITY ? 0.f : fast_exp2(o.x - M), fn = fast_exp2(mx - M);
@@ -239,15 +268,18 @@ __global__ void __launch_bounds__(256) decode_attend_kernel(DecodeArgs a) {
     const int b = static_cast<int>(row / (static_cast<int64_t>(a.Hq) * a.n_dec));
     const int64_t bc = static_cast<int64_t>(b) * a.Hkv + h / a.Gh;
     const int n = min(max(a.counts[bc], 0), a.c_max);
-    // the scaled query, fp32 values of its bf16 bits, in every lane
+    // the scaled query (decode_scale_kernel's row (h % Gh) * n_dec + j of KV
+    // head bc), fp32 values of its bf16 bits, in every lane
+    const int jq = static_cast<int>(row % a.n_dec);
+    const uint16_t* qrow = a.qsc + (bc * a.rows_pad + (h % a.Gh) * a.n_dec + jq) * D;
     float q[D];
 #pragma unroll
     for (int c8 = 0; c8 < kChunks; ++c8) {
-        const u32x4 raw = *reinterpret_cast<const u32x4*>(a.q_dec + row * D + 8 * c8);
+        const u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 8 * c8);
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            q[8 * c8 + 2 * w] = __uint_as_float(scaled_bf16(raw[w] & 0xFFFFu, a.scale) << 16);
-            q[8 * c8 + 2 * w + 1] = __uint_as_float(scaled_bf16(raw[w] >> 16, a.scale) << 16);
+            q[8 * c8 + 2 * w] = __uint_as_float(raw[w] << 16);
+            q[8 * c8 + 2 * w + 1] = __uint_as_float(raw[w] & 0xFFFF0000u);
         }
     }
     float mx = -INFINITY;
@@ -346,6 +378,8 @@ int decode_max_compact() { return kDecMaxCompact; }
 int decode_key_blocks(int T) { return (T + kDecKeys - 1) / kDecKeys; }
 
 hipError_t launch_decode_check(const DecodeArgs& a, hipStream_t s) {
+    dim3 g0((a.rows_pad * (a.d / 8) + 255) / 256, a.B * a.Hkv);
+    hipLaunchKernelGGL(decode_scale_kernel, g0, dim3(256), 0, s, a);
     dim3 g1(a.n_kb, a.B * a.Hkv);
     // staged queries: up to 256 rows of 17 chunks (69.6 KB at d = 128)
     const size_t lds = static_cast<size_t>(a.rows_pad) * (a.d / 8 + 1) * 16;

@@ -106,6 +106,7 @@ struct DecodeArgs {
     int n_kb;                  // key blocks
     double scale;              // log2(e) / sqrt(d), applied to the queries
     float4* part;              // [B, Hkv, n_kb, rows_pad] (max, sum all, sum kept), base 2
+    uint16_t* qsc;             // [B, Hkv, rows_pad, d] scaled decode queries (bf16)
     float* coverage;           // [B, Hq, n_dec]
     float* out;                // [B, Hq, n_dec, d]
 };
