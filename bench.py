@@ -58,7 +58,7 @@ def measured_traffic(workload, kernel):
     if t.get("workload") != workload or t.get("score_hip_sha256") != src:
         return None
     # a pass is the kernels one C-ABI call launches
-    parts = {"score_lse": ("row_ref", "score_lse", "lse_combine")}.get(kernel, (kernel,))
+    parts = {"score_lse": ("score_lse", "lse_combine")}.get(kernel, (kernel,))
     ks = [t.get("kernels", {}).get(p) for p in parts]
     if any(k is None or k.get("hbm_bytes_per_launch") is None for k in ks):
         return None
@@ -374,8 +374,8 @@ def main():
     # algorithmic MFMA work of one scoring launch: 2*Gh*P*d flops per prompt
     # key per KV head (one proxy-by-key contraction), times B*Hkv*T keys
     flops = 2.0 * w.Gh * cfg.P * d * B * Hkv * T
-    # one launch = one C-ABI pass call: score_lse = row_ref_kernel + score_lse_kernel +
-    # lse_combine_kernel, score_mass = score_mass_kernel
+    # one launch = one C-ABI pass call: score_lse = score_lse_kernel + lse_combine_kernel,
+    # score_mass = score_mass_kernel
     dom = "score_mass" if mass_ms >= lse_ms else "score_lse"
     dom_ms = max(mass_ms, lse_ms)
     achieved = flops / (dom_ms * 1e-3) / 1e12
