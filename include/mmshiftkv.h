@@ -96,8 +96,9 @@ typedef struct {
  * (fp64, summed in window order, divisor W - std_ddof).  Proxy i of head h:
  *   x_j = mu_j + (gamma * sigma_j) * z_j,
  * z from Philox4x32-10 (counter (j/4, i, h, (b<<16)|layer), key = seed) and
- * Box-Muller on series-evaluated ln/sin/cos in fp64, each product and sum
- * rounded separately; optional rotate-half rotary embedding (pairs j, j+d/2)
+ * Box-Muller on series-evaluated ln/sin/cos in fp32 (each product and sum
+ * rounded separately, division and square root correctly rounded), widened
+ * to fp64; optional rotate-half rotary embedding (pairs j, j+d/2)
  * from the caller's cos/sin tables; then multiplied by the softmax scale
  * c = log2(e)/sqrt(d) (fp64; the proxies carry Eq. 7's 1/sqrt(d), so their
  * products with the keys are base-2 logits) and rounded fp64 -> fp32 ->

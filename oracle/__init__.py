@@ -58,10 +58,10 @@ def _load():
     i32, u64, f64, i64 = ctypes.c_int, ctypes.c_uint64, ctypes.c_double, ctypes.c_int64
     lib.oracle_philox4x32_10.argtypes = [P, P, P]
     lib.oracle_uniform.argtypes = [ctypes.c_uint32]
-    lib.oracle_uniform.restype = f64
-    lib.oracle_ln.argtypes = [f64]
-    lib.oracle_ln.restype = f64
-    lib.oracle_sincos_2pi.argtypes = [f64, P, P]
+    lib.oracle_uniform.restype = ctypes.c_float
+    lib.oracle_ln.argtypes = [ctypes.c_float]
+    lib.oracle_ln.restype = ctypes.c_float
+    lib.oracle_sincos_2pi.argtypes = [ctypes.c_uint32, P, P]
     lib.oracle_normal4.argtypes = [u64, i32, i32, i32, i32, i32, P]
     lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
     lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
@@ -117,18 +117,20 @@ def philox4x32_10(ctr, key) -> np.ndarray:
 
 
 def uniform(x: int) -> float:
+    """32-bit word -> (2*(x>>9)+1) * 2^-24 (an fp32 value)."""
     return float(_load().oracle_uniform(int(x)))
 
 
 def ln(u: float) -> float:
+    """The generator's fp32 series natural log (u in (0, 1), an fp32 value)."""
     return float(_load().oracle_ln(float(u)))
 
 
-def sincos_2pi(u: float):
-    s = ctypes.c_double()
-    c = ctypes.c_double()
-    _load().oracle_sincos_2pi(float(u), ctypes.byref(s), ctypes.byref(c))
-    return s.value, c.value
+def sincos_2pi(x: int):
+    """(sin 2 pi u, cos 2 pi u) in fp32 by the generator's series, u = uniform(x)."""
+    s, c = ctypes.c_float(), ctypes.c_float()
+    _load().oracle_sincos_2pi(int(x), ctypes.byref(s), ctypes.byref(c))
+    return float(s.value), float(c.value)
 
 
 def normal4(seed: int, b: int, layer: int, h: int, i: int, jq: int) -> np.ndarray:

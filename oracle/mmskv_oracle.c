@@ -97,70 +97,76 @@ void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t
     out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
 }
 
-/* A 32-bit word x -> uniform (2*(x>>9) + 1) * 2^-24, exactly representable,
- * strictly inside (0, 1). */
-double oracle_uniform(uint32_t x)
+/* A 32-bit word x -> uniform (2*(x>>9) + 1) * 2^-24: an odd multiple of
+ * 2^-24, exact in fp32, strictly inside (0, 1). */
+float oracle_uniform(uint32_t x)
 {
-    return (double)(2u * (x >> 9) + 1u) * (1.0 / 16777216.0);
+    return (float)(2u * (x >> 9) + 1u) * (1.0f / 16777216.0f);
 }
 
-/* Natural logarithm for u in (0,1), written from the series
- *   ln m = 2 * sum_k s^(2k+1) / (2k+1),  s = (m-1)/(m+1),
- * after splitting u = m * 2^e with m in [sqrt(1/2), sqrt(2)).  Twelve terms
- * (|s| <= 0.1716 makes the next term < 1e-20).  Horner form, plain mul/add. */
-double oracle_ln(double u)
+/* Natural logarithm for u in (0,1), in fp32, written from the series
+ *   ln m = 2 * sum_{k=0..5} s^(2k+1) / (2k+1),  s = (m-1)/(m+1),
+ * after splitting u = m * 2^e with m in [r, 2r), r the fp32 value of
+ * sqrt(1/2) rounded down; |s| <= 0.1716, so the first omitted term is below
+ * 1e-10 of the result.  Horner form, plain fp32 mul/add; the coefficients
+ * are 1.0f/(2k+1). */
+float oracle_ln(float u)
 {
     int e;
-    double f = frexp(u, &e);               /* u = f * 2^e, f in [0.5, 1) */
-    double m = f;
-    if (f < 0.70710678118654752440) {      /* sqrt(1/2) */
-        m = 2.0 * f;
+    float f = frexpf(u, &e);               /* u = f * 2^e, f in [0.5, 1) */
+    float m = f;
+    if (f < 0x1.6a09e6p-1f) {
+        m = 2.0f * f;
         e = e - 1;
     }
-    double s = (m - 1.0) / (m + 1.0);
-    double s2 = s * s;
-    double poly = 1.0 / 23.0;
-    for (int k = 10; k >= 0; --k) {
+    float s = (m - 1.0f) / (m + 1.0f);
+    float s2 = s * s;
+    float poly = 1.0f / 11.0f;
+    for (int k = 4; k >= 0; --k) {
         poly = poly * s2;
-        poly = poly + 1.0 / (double)(2 * k + 1);
+        poly = poly + 1.0f / (float)(2 * k + 1);
     }
-    double ln_m = 2.0 * s;
+    float ln_m = 2.0f * s;
     ln_m = ln_m * poly;
-    double ln2 = 0.69314718055994530942;   /* nearest double to ln 2 */
-    double eln2 = (double)e * ln2;
+    float ln2 = 0x1.62e430p-1f;            /* nearest fp32 to ln 2 */
+    float eln2 = (float)e * ln2;
     return eln2 + ln_m;
 }
 
-/* sin and cos of 2*pi*u for u in (0,1): the quarter-turn q nearest to 4u is
- * removed exactly, the remainder f in [-1/8, 1/8] is scaled by 2*pi, and the
- * Taylor series (sin to phi^21, cos to phi^20, coefficients by repeated
- * division) are evaluated in Horner form; the quarter turns are then
- * restored by the usual quadrant identities. */
-void oracle_sincos_2pi(double u, double *sin_out, double *cos_out)
+/* sin and cos of 2*pi*u, in fp32, for the uniform u = n * 2^-24 of word x
+ * (n = 2*(x>>9) + 1, odd): the quarter turn q nearest to 4u = n / 2^22 is
+ * removed in integer arithmetic (n is odd, so 4u is never halfway), which
+ * leaves f = u - q/4 = (n - q 2^22) 2^-24 with |f| < 1/8, exact in fp32;
+ * phi = f * 2pi (2pi rounded to fp32); Taylor series of sin to phi^11 and
+ * of cos to phi^10 (|phi| < pi/4, first omitted terms below 1e-10),
+ * coefficients by repeated fp32 division, Horner form; the quarter turns
+ * are then restored by the quadrant identities. */
+void oracle_sincos_2pi(uint32_t x, float *sin_out, float *cos_out)
 {
-    double four_u = 4.0 * u;
-    int q = (int)floor(four_u + 0.5);
-    double f = u - (double)q * 0.25;
-    double two_pi = 6.28318530717958647692;
-    double phi = f * two_pi;
-    double p2 = phi * phi;
+    int32_t n = (int32_t)(2u * (x >> 9) + 1u);
+    int32_t q = (n + (1 << 21)) >> 22;
+    int32_t rem = n - q * (1 << 22);
+    float f = (float)rem * (1.0f / 16777216.0f);
+    float two_pi = 0x1.921fb6p+2f;         /* nearest fp32 to 2 pi */
+    float phi = f * two_pi;
+    float p2 = phi * phi;
 
-    double cs[11], cc[11];
-    cs[0] = 1.0;
-    cc[0] = 1.0;
-    for (int k = 1; k <= 10; ++k) {
-        cs[k] = -cs[k - 1] / (double)((2 * k) * (2 * k + 1));
-        cc[k] = -cc[k - 1] / (double)((2 * k - 1) * (2 * k));
+    float cs[6], cc[6];
+    cs[0] = 1.0f;
+    cc[0] = 1.0f;
+    for (int k = 1; k <= 5; ++k) {
+        cs[k] = -cs[k - 1] / (float)((2 * k) * (2 * k + 1));
+        cc[k] = -cc[k - 1] / (float)((2 * k - 1) * (2 * k));
     }
-    double ps = cs[10], pc = cc[10];
-    for (int k = 9; k >= 0; --k) {
+    float ps = cs[5], pc = cc[5];
+    for (int k = 4; k >= 0; --k) {
         ps = ps * p2;
         ps = ps + cs[k];
         pc = pc * p2;
         pc = pc + cc[k];
     }
-    double sp = phi * ps;
-    double cp = pc;
+    float sp = phi * ps;
+    float cp = pc;
     switch (q & 3) {
     case 0: *sin_out = sp;  *cos_out = cp;  break;
     case 1: *sin_out = cp;  *cos_out = -sp; break;
@@ -171,9 +177,10 @@ void oracle_sincos_2pi(double u, double *sin_out, double *cos_out)
 
 /* Standard normals for dims 4*jq .. 4*jq+3 of proxy i of query head h,
  * batch b, layer l: Philox counter (jq, i, h, (b<<16)|l), key = seed split in
- * two 32-bit halves; uniforms (u0,u1) and (u2,u3) each give one Box-Muller
+ * two 32-bit halves; words (x0,x1) and (x2,x3) each give one Box-Muller
  * pair (Box & Muller 1958): r = sqrt(-2 ln u_a), z = (r cos 2pi u_b,
- * r sin 2pi u_b). */
+ * r sin 2pi u_b), in fp32 (correctly rounded division and square root),
+ * then widened to fp64 for the proxy formula. */
 void oracle_normal4(uint64_t seed, int b, int layer, int h, int i, int jq, double z[4])
 {
     uint32_t ctr[4] = {(uint32_t)jq, (uint32_t)i, (uint32_t)h,
@@ -182,13 +189,14 @@ void oracle_normal4(uint64_t seed, int b, int layer, int h, int i, int jq, doubl
     uint32_t x[4];
     oracle_philox4x32_10(ctr, key, x);
     for (int pair = 0; pair < 2; ++pair) {
-        double ua = oracle_uniform(x[2 * pair]);
-        double ub = oracle_uniform(x[2 * pair + 1]);
-        double r = sqrt(-2.0 * oracle_ln(ua));
-        double sn, cs;
-        oracle_sincos_2pi(ub, &sn, &cs);
-        z[2 * pair] = r * cs;
-        z[2 * pair + 1] = r * sn;
+        float ua = oracle_uniform(x[2 * pair]);
+        float r = sqrtf(-2.0f * oracle_ln(ua));
+        float sn, cs;
+        oracle_sincos_2pi(x[2 * pair + 1], &sn, &cs);
+        float z0 = r * cs;
+        float z1 = r * sn;
+        z[2 * pair] = (double)z0;
+        z[2 * pair + 1] = (double)z1;
     }
 }
 

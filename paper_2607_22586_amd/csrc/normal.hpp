@@ -1,7 +1,9 @@
 // Counter-based standard normals shared by the proxy kernels: Philox4x32-10
 // words (Salmon et al., SC 2011) turned into Box-Muller pairs with ln, sin and
-// cos evaluated by fixed series in fp64, every step rounded on its own (no
-// fused multiply-add), so the draws are a fixed function of the counter.
+// cos evaluated by fixed series in fp32, every step rounded on its own (no
+// fused multiply-add; division and square root correctly rounded), so the
+// draws are a fixed function of the counter.  The pairs are widened to fp64
+// for the proxy formula.
 #pragma once
 #pragma clang fp contract(off)
 
@@ -28,64 +30,66 @@ __device__ __forceinline__ void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32
     }
 }
 
-// 32-bit word -> (2*(x>>9)+1) * 2^-24, exact, inside (0,1).
-__device__ __forceinline__ double word_to_unit(uint32_t x) {
-    return static_cast<double>(2u * (x >> 9) + 1u) * 0x1p-24;
+// 32-bit word -> (2*(x>>9)+1) * 2^-24, an odd multiple of 2^-24, exact in
+// fp32, inside (0,1).
+__device__ __forceinline__ float word_to_unit(uint32_t x) {
+    return static_cast<float>(2u * (x >> 9) + 1u) * 0x1p-24f;
 }
 
-// ln(u), u in (0,1): u = m * 2^e with m in [sqrt(1/2), sqrt(2)) taken from the
-// exponent field; ln m = 2 s (1 + s^2/3 + ... + s^22/23), s = (m-1)/(m+1),
-// Horner in s^2.
-__device__ double ln_unit(double u) {
-    const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(u));
-    int e = static_cast<int>((bits >> 52) & 0x7FF) - 1022;
-    const double f = __longlong_as_double(
-        static_cast<long long>((bits & 0x000FFFFFFFFFFFFFull) | 0x3FE0000000000000ull));
-    double m = f;
-    if (f < 0x1.6a09e667f3bcdp-1) {
-        m = f * 2.0;
+// ln(u), u in (0,1) normal: u = m * 2^e with m in [r, 2r), r = fp32 sqrt(1/2)
+// rounded down, taken from the exponent field; ln m = 2 s (1 + s^2/3 + ... +
+// s^10/11), s = (m-1)/(m+1), Horner in s^2.
+__device__ float ln_unit(float u) {
+    const uint32_t bits = __float_as_uint(u);
+    int e = static_cast<int>((bits >> 23) & 0xFFu) - 126;
+    const float f = __uint_as_float((bits & 0x007FFFFFu) | 0x3F000000u);   // [0.5, 1)
+    float m = f;
+    if (f < 0x1.6a09e6p-1f) {
+        m = f * 2.0f;
         e = e - 1;
     }
-    const double s = (m - 1.0) / (m + 1.0);
-    const double s2 = s * s;
-    double h = 1.0 / 23.0;
+    const float s = (m - 1.0f) / (m + 1.0f);
+    const float s2 = s * s;
+    float h = 1.0f / 11.0f;
 #pragma unroll
-    for (int k = 10; k >= 0; --k) {
+    for (int k = 4; k >= 0; --k) {
         h = h * s2;
-        h = h + 1.0 / static_cast<double>(2 * k + 1);
+        h = h + 1.0f / static_cast<float>(2 * k + 1);
     }
-    double r = 2.0 * s;
+    float r = 2.0f * s;
     r = r * h;
-    const double e_ln2 = static_cast<double>(e) * 0x1.62e42fefa39efp-1;
+    const float e_ln2 = static_cast<float>(e) * 0x1.62e430p-1f;
     return e_ln2 + r;
 }
 
-// sin / cos of 2*pi*u, u in (0,1): remove the nearest quarter turn exactly,
-// Taylor series of the remainder angle (|phi| <= pi/4) up to phi^21 / phi^20,
-// then the quadrant identities.
-__device__ void sincos_turn(double u, double& sn, double& cs) {
-    const int q = static_cast<int>(4.0 * u + 0.5);
-    const double f = u - static_cast<double>(q) * 0.25;
-    const double phi = f * 0x1.921fb54442d18p+2;
-    const double p2 = phi * phi;
-    double as[11], ac[11];
-    as[0] = 1.0;
-    ac[0] = 1.0;
+// sin / cos of 2*pi*u for u = word_to_unit(x): the nearest quarter turn q of
+// 4u = n / 2^22 (n odd, never halfway) comes off in integers, the remainder
+// angle (|phi| < pi/4) goes through Taylor series up to phi^11 / phi^10, then
+// the quadrant identities.
+__device__ void sincos_turn(uint32_t x, float& sn, float& cs) {
+    const int n = static_cast<int>(2u * (x >> 9) + 1u);
+    const int q = (n + (1 << 21)) >> 22;
+    const float f = static_cast<float>(n - q * (1 << 22)) * 0x1p-24f;
+    const float phi = f * 0x1.921fb6p+2f;
+    const float p2 = phi * phi;
+    float as[6], ac[6];
+    as[0] = 1.0f;
+    ac[0] = 1.0f;
 #pragma unroll
-    for (int k = 1; k <= 10; ++k) {
-        as[k] = -as[k - 1] / static_cast<double>((2 * k) * (2 * k + 1));
-        ac[k] = -ac[k - 1] / static_cast<double>((2 * k - 1) * (2 * k));
+    for (int k = 1; k <= 5; ++k) {
+        as[k] = -as[k - 1] / static_cast<float>((2 * k) * (2 * k + 1));
+        ac[k] = -ac[k - 1] / static_cast<float>((2 * k - 1) * (2 * k));
     }
-    double ps = as[10], pc = ac[10];
+    float ps = as[5], pc = ac[5];
 #pragma unroll
-    for (int k = 9; k >= 0; --k) {
+    for (int k = 4; k >= 0; --k) {
         ps = ps * p2;
         ps = ps + as[k];
         pc = pc * p2;
         pc = pc + ac[k];
     }
-    const double s0 = phi * ps;
-    const double c0 = pc;
+    const float s0 = phi * ps;
+    const float c0 = pc;
     switch (q & 3) {
         case 0: sn = s0; cs = c0; break;
         case 1: sn = c0; cs = -s0; break;
@@ -106,13 +110,13 @@ __device__ void normal_quad(uint32_t k0, uint32_t k1, int b, int layer, int h, i
     const uint32_t w[4] = {c0, c1, c2, c3};
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
-        const double ua = word_to_unit(w[2 * p]);
-        const double ub = word_to_unit(w[2 * p + 1]);
-        const double r = sqrt(-2.0 * ln_unit(ua));
-        double sn, cs;
-        sincos_turn(ub, sn, cs);
-        z[2 * p] = r * cs;
-        z[2 * p + 1] = r * sn;
+        const float r = sqrtf(-2.0f * ln_unit(word_to_unit(w[2 * p])));
+        float sn, cs;
+        sincos_turn(w[2 * p + 1], sn, cs);
+        const float z0 = r * cs;
+        const float z1 = r * sn;
+        z[2 * p] = static_cast<double>(z0);
+        z[2 * p + 1] = static_cast<double>(z1);
     }
 }
 

@@ -1,13 +1,13 @@
 // Variance-expanded query proxies (Sec. 3.2.1 Eqs. 4-5; Appendix A.4 Eq. 15)
 // and the anchor query of Sec. 3.2.3 Eq. 11, on gfx950.
 //
-// Every floating-point step here is an fp64 operation rounded on its own
-// (no fused multiply-add), so the proxies are a fixed function of the
-// inputs: window statistics summed in window order, Philox4x32-10 words,
-// Box-Muller with series-evaluated ln / sin / cos, the softmax scale
-// log2(e)/sqrt(d) that the queries carry (Sec. 3.2.2 Eq. 7, so the score
-// products are base-2 logits), fp64 -> fp32 -> bf16.  The anchor query is
-// returned unscaled.
+// Every floating-point step here is rounded on its own (no fused
+// multiply-add), so the proxies are a fixed function of the inputs: window
+// statistics summed in window order (fp64), Philox4x32-10 words, Box-Muller
+// with series-evaluated ln / sin / cos (fp32, widened to fp64), the proxy
+// formula and the softmax scale log2(e)/sqrt(d) that the queries carry
+// (fp64; Sec. 3.2.2 Eq. 7, so the score products are base-2 logits), then
+// fp64 -> fp32 -> bf16.  The anchor query is returned unscaled.
 #pragma clang fp contract(off)
 
 #include "common.hpp"
