@@ -20,6 +20,11 @@ Prints one JSON line: keys scored+selected per second (B*L*T / step time),
 the roofline of the dominant kernel (algorithmic MFMA flops per launch /
 launch time, events on the launch stream) and the CPU oracle timed on a
 bounded sample of the same workload.
+
+Other modes, one JSON line each: --decode-check N_DEC (the decode-time
+coverage check), --selectors N_DEC (the method beside the baseline
+selectors on the same kernels), --hidden (the hidden-state form of the
+proxies in front of the same scoring and selection).
 """
 from __future__ import annotations
 
@@ -238,6 +243,119 @@ def selectors_bench(args):
     print(json.dumps(out), flush=True)
 
 
+def hidden_bench(args):
+    """The hidden-state form of the proxies (Sec. 3.2.1 Eqs. 4-6, Algorithm 1)
+    in front of the same scoring, selection and gather: per layer, the
+    statistics of the T prefill hidden states, the hidden-space samples and
+    their projection by every head's W_Q replace the query-space proxy call.
+    K steps over all layers on one stream, events around every call; the
+    roofline is taken for the slowest of the three hidden-path calls.  The
+    hidden states of HIDDEN_LAYERS distinct layers (470 MiB each at the 16k
+    batch-4 shape, more than the last-level cache) are reused cyclically.
+    One JSON line."""
+    import torch
+    from paper_2607_22586_amd import binding as bd
+    from paper_2607_22586_amd import workloads as wl
+    bd.load_library()
+    dev = torch.device("cuda:0")
+    w = wl.WORKLOADS[args.workload]
+    L = args.layers or w.L
+    nh = max(1, min(L, args.hidden_layers))
+    B, Hq, Hkv, T, W, d = w.B, w.Hq, w.Hkv, w.T, w.W, w.d
+    D = Hq * d
+    cfgs = [bd.SelectionConfig(seed=w.wid, layer=l) for l in range(L)]
+    cfg = cfgs[0]
+    log("generating %d layers of %s and %d hidden-state layers" % (L, w.name, nh))
+    layers = [wl.make_layer(w, l, device=dev) for l in range(L)]
+    hid = [wl.make_hidden(w, l, device=dev) for l in range(nh)]
+    torch.cuda.synchronize()
+    st = torch.empty((B, 2, D), dtype=torch.float64, device=dev)
+    ws_st = torch.empty(bd.hidden_stats_workspace(B, T, D), dtype=torch.uint8, device=dev)
+    hp = torch.empty((B, cfg.P, D), dtype=torch.bfloat16, device=dev)
+    prox = torch.empty((B, Hq, cfg.P, d), dtype=torch.bfloat16, device=dev)
+    sc = bd.ScoreOut(torch.empty((B, Hkv, cfg.G, T), dtype=torch.float32, device=dev),
+                     torch.empty((B, Hkv, T), dtype=torch.float32, device=dev),
+                     torch.empty((B, Hkv, T), dtype=torch.float32, device=dev))
+    ws_score = torch.empty(bd.score_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(bd.select_workspace(B, Hq, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev)
+    sel = bd.Selected(torch.empty((B, Hkv, w.budget), dtype=torch.int32, device=dev),
+                      torch.empty((B, Hkv), dtype=torch.int32, device=dev), None)
+    kv_out = (torch.empty((B, Hkv, w.budget, d), dtype=layers[0]["k"].dtype, device=dev),
+              torch.empty((B, Hkv, w.budget, d), dtype=layers[0]["k"].dtype, device=dev))
+    names = ("hidden_stats", "hidden_proxies", "project_proxies", "score_select_gather")
+
+    def step(ev=None):
+        for l in range(L):
+            x, hx, c = layers[l], hid[l % nh], cfgs[l]
+            if ev is not None:
+                ev[l][0].record()
+            bd.hidden_stats(hx["hidden"], out=st, workspace=ws_st)
+            if ev is not None:
+                ev[l][1].record()
+            bd.hidden_proxies(st, c, T, out=hp)
+            if ev is not None:
+                ev[l][2].record()
+            bd.project_proxies(hp, hx["wq"], Hq, out=prox)
+            if ev is not None:
+                ev[l][3].record()
+            bd.score_lse(prox, hx["q_last"], x["k"], c, ws_score, W)
+            bd.score_mass(prox, hx["q_last"], x["k"], c, ws_score, W, out=sc)
+            bd.select_topk(sc, c, w.budget, w.budget, None, Hq, W, out=sel, workspace=ws_sel)
+            bd.gather_kv(x["k"], x["v"], sel, out=kv_out)
+            if ev is not None:
+                ev[l][4].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(args.steps):
+        step()
+    t1.record()
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(L)] for _ in range(args.steps)]
+    for s_ in range(args.steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    us = {n: 1e3 * sum(ev[s_][l][i].elapsed_time(ev[s_][l][i + 1]) for s_ in range(args.steps) for l in range(L))
+          / (args.steps * L) for i, n in enumerate(names)}
+    # algorithmic work per call: the statistics read the hidden states once
+    # and write mean / std; the projection is a (B*P) x D by D x (Hq*d)
+    # product.  The samples (the generator, as in the query-space proxy
+    # call) are ALU work and are reported by time only.
+    hb = hid[0]["hidden"].element_size()
+    rl = {
+        "hidden_stats": {"bound": "hbm", "work": B * T * D * hb + B * 2 * D * 8, "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s"},
+        "project_proxies": {"bound": "mfma", "work": 2.0 * B * cfg.P * D * Hq * d, "peak": PEAK_BF16_TFLOPS,
+                            "unit": "TFLOP/s"},
+    }
+    for n, r in rl.items():
+        scale = 1e9 if r["unit"] == "GB/s" else 1e12
+        r["achieved"] = r["work"] / (us[n] * 1e-6) / scale
+        r["frac"] = r["achieved"] / r["peak"]
+        r["us_per_call"] = us[n]
+    dom = max(rl, key=lambda n: us[n])
+    r = rl[dom]
+    out = {
+        "metric": "prompt keys scored+selected/sec (hidden-state proxies)",
+        "value": B * L * T / (ms_step * 1e-3), "unit": "keys/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "us_per_layer": ms_step * 1e3 / L, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "hidden_layers": nh, "batch": B, "T": T, "D": D,
+                   "Hq": Hq, "Hkv": Hkv, "d": d, "P": cfg.P, "G": cfg.G, "budget": w.budget,
+                   "proxies": "hidden-state (Eqs. 4-6)", "streams": 1},
+        "stages_us_per_layer": us,
+        "roofline": {"kernel": dom, "bound": r["bound"], "achieved": r["achieved"], "peak": r["peak"],
+                     "unit": r["unit"], "frac": r["frac"], "traffic": None},
+        "hidden_rooflines": rl,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -256,6 +374,11 @@ def main():
     ap.add_argument("--selectors", type=int, default=0, metavar="N_DEC",
                     help="compare the method with the baseline selectors (throughput and decode-time "
                          "coverage with N_DEC decode queries per head) instead")
+    ap.add_argument("--hidden", action="store_true",
+                    help="time the hidden-state form of the proxies (statistics, samples, W_Q projection) "
+                         "in front of the same scoring, selection and gather")
+    ap.add_argument("--hidden-layers", type=int, default=4,
+                    help="distinct hidden-state layers generated for --hidden (reused cyclically)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -272,6 +395,9 @@ def main():
         return
     if args.selectors > 0:
         selectors_bench(args)
+        return
+    if args.hidden:
+        hidden_bench(args)
         return
 
     import torch

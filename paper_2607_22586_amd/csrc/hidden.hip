@@ -31,7 +31,7 @@
 namespace mmskv {
 namespace {
 
-constexpr int kStatThreads = 256;
+constexpr int kStatThreads = 64;           // one wave per workgroup (no shared state)
 
 // fp32 value times the query scale, in fp64, rounded back to fp32.
 __device__ __forceinline__ float scaled(float v, double scale) {
@@ -39,25 +39,41 @@ __device__ __forceinline__ float scaled(float v, double scale) {
     return static_cast<float>(y);
 }
 constexpr int kStatVec = 8;                 // features per thread (one 16-byte bf16 load)
+constexpr int kStatFlight = 8;              // tokens per group of loads in flight
 
-// 8 consecutive features of one token as fp64.
-__device__ __forceinline__ void load8(const HiddenArgs& a, int64_t off, double (&v)[kStatVec]) {
-    if (a.dtype == 1) {
-        const u32x4 r = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.hidden) + off);
+// Running sums of one token's kStatVec features.  The square of a bf16 or fp32
+// value is exact in fp64, so the fused multiply-add rounds exactly like a
+// separate product and sum.
+__device__ __forceinline__ void accum_token(const double (&v)[kStatVec], double (&s)[kStatVec],
+                                       double (&ss)[kStatVec]) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            v[2 * q] = static_cast<double>(__uint_as_float(r[q] << 16));
-            v[2 * q + 1] = static_cast<double>(__uint_as_float(r[q] & 0xFFFF0000u));
-        }
-    } else {
-        const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.hidden) + off);
-        const float4 y = *reinterpret_cast<const float4*>(static_cast<const float*>(a.hidden) + off + 4);
-        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-        v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+    for (int e = 0; e < kStatVec; ++e) {
+        s[e] = s[e] + v[e];
+        ss[e] = fma(v[e], v[e], ss[e]);
     }
 }
 
-// Chunk sums: grid (n_chunks, ceil(D / (8*256)), B).
+__device__ __forceinline__ void unpack_bf16x8(const u32x4& r, double (&v)[kStatVec]) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        v[2 * q] = static_cast<double>(__uint_as_float(r[q] << 16));
+        v[2 * q + 1] = static_cast<double>(__uint_as_float(r[q] & 0xFFFF0000u));
+    }
+}
+
+// 8 consecutive fp32 features of one token as fp64.
+__device__ __forceinline__ void load8_f32(const HiddenArgs& a, int64_t off, double (&v)[kStatVec]) {
+    const float4 x = *reinterpret_cast<const float4*>(static_cast<const float*>(a.hidden) + off);
+    const float4 y = *reinterpret_cast<const float4*>(static_cast<const float*>(a.hidden) + off + 4);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+}
+
+// Chunk sums: grid (n_chunks, ceil(D / (8*64)), B); thread j owns features
+// [8j, 8j+8) of the block and sums them over the chunk's tokens in token
+// order.  bf16 rows: the raw 16-byte loads of the next kStatFlight tokens
+// are issued before the current ones are summed (two register sets used in
+// turn), so up to two groups of loads are in flight per thread.
 __global__ void __launch_bounds__(kStatThreads) hidden_stats_partial_kernel(HiddenArgs a) {
     const int c = blockIdx.x, b = blockIdx.z;
     const int j0 = (static_cast<int>(blockIdx.y) * kStatThreads + static_cast<int>(threadIdx.x)) * kStatVec;
@@ -67,29 +83,37 @@ __global__ void __launch_bounds__(kStatThreads) hidden_stats_partial_kernel(Hidd
 #pragma unroll
     for (int e = 0; e < kStatVec; ++e) { s[e] = 0.0; ss[e] = 0.0; }
     const int64_t base = static_cast<int64_t>(b) * a.sb + j0;
-    int t = t0;
-    // four tokens' loads in flight, accumulated in token order
-    for (; t + 4 <= t1; t += 4) {
-        double v[4][kStatVec];
+    if (a.dtype == 1) {
+        const uint16_t* h = static_cast<const uint16_t*>(a.hidden) + base;
+        auto fetch = [&](int t, u32x4 (&r)[kStatFlight]) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) load8(a, base + static_cast<int64_t>(t + u) * a.st, v[u]);
+            for (int u = 0; u < kStatFlight; ++u)
+                if (t + u < t1) r[u] = *reinterpret_cast<const u32x4*>(h + static_cast<int64_t>(t + u) * a.st);
+        };
+        auto sum = [&](int t, const u32x4 (&r)[kStatFlight]) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int e = 0; e < kStatVec; ++e) {
-                const double sq = v[u][e] * v[u][e];
-                s[e] = s[e] + v[u][e];
-                ss[e] = ss[e] + sq;
+            for (int u = 0; u < kStatFlight; ++u) {
+                if (t + u < t1) {
+                    double v[kStatVec];
+                    unpack_bf16x8(r[u], v);
+                    accum_token(v, s, ss);
+                }
             }
-    }
-    for (; t < t1; ++t) {
-        double v[kStatVec];
-        load8(a, base + static_cast<int64_t>(t) * a.st, v);
-#pragma unroll
-        for (int e = 0; e < kStatVec; ++e) {
-            const double sq = v[e] * v[e];
-            s[e] = s[e] + v[e];
-            ss[e] = ss[e] + sq;
+        };
+        // two register sets, A for tokens [t, t+F), B for [t+F, t+2F)
+        u32x4 ra[kStatFlight], rb[kStatFlight];
+        fetch(t0, ra);
+        for (int t = t0; t < t1; t += 2 * kStatFlight) {
+            if (t + kStatFlight < t1) fetch(t + kStatFlight, rb);
+            sum(t, ra);
+            if (t + 2 * kStatFlight < t1) fetch(t + 2 * kStatFlight, ra);
+            if (t + kStatFlight < t1) sum(t + kStatFlight, rb);
+        }
+    } else {
+        for (int t = t0; t < t1; ++t) {
+            double v[kStatVec];
+            load8_f32(a, base + static_cast<int64_t>(t) * a.st, v);
+            accum_token(v, s, ss);
         }
     }
     double2* out = a.partial + (static_cast<int64_t>(b) * a.n_chunks + c) * a.D + j0;
@@ -103,10 +127,21 @@ __global__ void __launch_bounds__(256) hidden_stats_final_kernel(HiddenArgs a) {
     if (j >= a.D) return;
     const double2* p = a.partial + static_cast<int64_t>(b) * a.n_chunks * a.D + j;
     double S = 0.0, SS = 0.0;
-    for (int c = 0; c < a.n_chunks; ++c) {
-        const double2 v = p[static_cast<int64_t>(c) * a.D];
-        S = S + v.x;
-        SS = SS + v.y;
+    // kFinalBatch chunk partials fetched at once (their latencies overlap),
+    // then added in chunk order
+    constexpr int kFinalBatch = 16;
+    for (int c0 = 0; c0 < a.n_chunks; c0 += kFinalBatch) {
+        double2 v[kFinalBatch];
+#pragma unroll
+        for (int u = 0; u < kFinalBatch; ++u)
+            if (c0 + u < a.n_chunks) v[u] = p[static_cast<int64_t>(c0 + u) * a.D];
+#pragma unroll
+        for (int u = 0; u < kFinalBatch; ++u) {
+            if (c0 + u < a.n_chunks) {
+                S = S + v[u].x;
+                SS = SS + v[u].y;
+            }
+        }
     }
     const double mean = S / static_cast<double>(a.T);
     const double sm = S * mean;
@@ -202,15 +237,20 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
 
-    GemmStage st;
-    gemm_fetch(p, m0, n0, 0, st);
-    gemm_store(st, lds, lds + kTileSlots);
+    // k steps: LDS holds steps ks (being multiplied) and ks+1 (written during
+    // step ks); two register stages hold the global loads of steps ks+1 and
+    // ks+2, so every load has two steps of MFMA work to arrive in
+    GemmStage s0, s1;
+    gemm_fetch(p, m0, n0, 0, s0);
+    gemm_store(s0, lds, lds + kTileSlots);
+    if (1 < n_k) gemm_fetch(p, m0, n0, kBK, s1);
+    if (2 < n_k) gemm_fetch(p, m0, n0, 2 * kBK, s0);
     __syncthreads();
-    for (int ks = 0; ks < n_k; ++ks) {
+    // step ks; `nx` holds the loads of step ks+1 and is refilled with ks+3
+    auto step = [&](int ks, GemmStage& nx) {
         const int cur = ks & 1;
         const u32x4* la = lds + cur * 2 * kTileSlots;
         const u32x4* lw = la + kTileSlots;
-        if (ks + 1 < n_k) gemm_fetch(p, m0, n0, (ks + 1) * kBK, st);
 #pragma unroll
         for (int kc = 0; kc < kBK / 16; ++kc) {
             bf16x8 fa[2], fw[2];
@@ -227,9 +267,14 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
         }
         if (ks + 1 < n_k) {
             u32x4* na = lds + (cur ^ 1) * 2 * kTileSlots;
-            gemm_store(st, na, na + kTileSlots);
+            gemm_store(nx, na, na + kTileSlots);
+            if (ks + 3 < n_k) gemm_fetch(p, m0, n0, (ks + 3) * kBK, nx);
         }
         __syncthreads();
+    };
+    for (int ks = 0; ks < n_k; ks += 2) {
+        step(ks, s1);
+        if (ks + 1 < n_k) step(ks + 1, s0);
     }
 
     // epilogue: fp32 tile [kBM][kBN + 4] in LDS, then rotary pairs and bf16
