@@ -438,6 +438,7 @@ __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) 
     __shared__ uint32_t s_digit, s_cnt;
     __shared__ unsigned long long s_rem;
     __shared__ int32_t s_tcut;
+    __shared__ uint32_t s_theta;
 
     const int g = blockIdx.x, c = blockIdx.y, b = blockIdx.z;
     const int64_t hcg = (static_cast<int64_t>(b) * a.Hkv + c) * a.G + g;
@@ -492,6 +493,17 @@ __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) 
         descending_crossing<unsigned long long, kTauThreads>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
         prefix |= s_digit << tau_shift(pass);
         need = s_rem;
+        if (pass < 2 && s_cnt == 1u) {
+            // one key left in the crossing bucket: its mass is theta, and the
+            // remaining passes would only spell out its low bits
+            const uint32_t fixed = tau_mask(pass + 1);
+#pragma unroll
+            for (int j = 0; j < KPT; ++j)
+                if (t0 + j < a.T && (mb[j] & fixed) == prefix) s_theta = mb[j];
+            __syncthreads();
+            prefix = s_theta;
+            break;
+        }
     }
     const uint64_t f_theta = fixed_of(prefix, S);
     const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
