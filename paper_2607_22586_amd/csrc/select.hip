@@ -7,7 +7,8 @@
 //           finds the cut mass theta and, among keys whose mass equals theta,
 //           the last admitted index, such that
 //           {mass > theta} u {mass == theta, index <= tcut} is the shortest
-//           (mass desc, index asc) prefix whose mass reaches tau * total.
+//           (mass desc, index asc) prefix whose mass reaches tau * total;
+//           the passes stop early once the crossing bucket holds one key.
 //           Masses are summed as integers in units of 2^-S (converted from
 //           the float bits exactly), so every decision is independent of
 //           summation order.
