@@ -79,7 +79,7 @@ def _load():
     lib.oracle_gather.argtypes = [i32, i32, i32, i64, i32, P, P, P, P]
     lib.oracle_gather.restype = i32
     lib.oracle_num_threads.restype = i32
-    lib.oracle_hidden_stats.argtypes = [i32, i32, i32, i32, i32, P, i32, P]
+    lib.oracle_hidden_stats.argtypes = [i32, i32, i32, i32, P, i32, P]
     lib.oracle_hidden_stats.restype = i32
     lib.oracle_hidden_proxies.argtypes = [i32, i32, i32, f64, u64, i32, i32, P, P]
     lib.oracle_hidden_proxies.restype = i32
@@ -296,18 +296,16 @@ def select_layer(q_win, k, v, Hkv: int, budget: int, P: int = 512, G: int = 32, 
                        gather(v, sel.idx, sel.counts))
 
 
-HIDDEN_STATS_CHUNK = 256
-
-
-def hidden_stats(hidden: np.ndarray, ddof: int = 0, chunk: int = HIDDEN_STATS_CHUNK) -> np.ndarray:
+def hidden_stats(hidden: np.ndarray, ddof: int = 0) -> np.ndarray:
     """Sec. 3.2.1 Eq. 4 over the prefill hidden states [B, T, D] (fp32, or
-    bf16 bits as uint16): per (batch row, dim) mean and std, chunked merge in
-    token order.  Returns [B, 2, D] fp64."""
+    bf16 bits as uint16): per (batch row, dim) mean, then the standard
+    deviation from the squared deviations about it (two passes over the
+    tokens, sums in token order).  Returns [B, 2, D] fp64."""
     lib = _load()
     h = np.ascontiguousarray(hidden)
     B, T, D = h.shape
     st = np.zeros((B, 2, D), dtype=np.float64)
-    rc = lib.oracle_hidden_stats(B, T, D, chunk, ddof, _ptr(h), _dtype_code(h), _ptr(st))
+    rc = lib.oracle_hidden_stats(B, T, D, ddof, _ptr(h), _dtype_code(h), _ptr(st))
     if rc != 0:
         raise ValueError("oracle_hidden_stats: invalid arguments")
     return st

@@ -24,15 +24,20 @@
  *     j+d/2) for one synthetic future position (Sec. 3.2.1, last paragraph).
  *   - The softmax scale of Sec. 3.2.2 Eq. 7, 1/sqrt(head_dim), is carried by
  *     the queries: proxies are multiplied by c = log2(e)/sqrt(head_dim) in
- *     fp64 and then rounded fp64 -> fp32 -> bf16 (round to nearest even), as
- *     attention implementations scale queries before the low-precision
- *     product; the anchor query is scaled the same way (fp64 product of its
- *     bf16 value and c, then fp32, then bf16).  Scoring keys are rounded
- *     fp32 -> bf16 the same way.  The logits q~ . k are then computed in fp64
- *     on those bf16 values (mixed-precision inference, Sec. 4.1
- *     "Implementation and Hyperparameters") and are base-2 logits: the
- *     softmax is 2^(s - L) with L = log2 sum_t 2^(s_t), which equals
- *     exp(q.k/sqrt(d) - lse) up to the bf16 rounding of the scaled queries.
+ *     fp64 and then rounded fp64 -> fp32 -> bf16 (round to nearest even);
+ *     the anchor query, a bf16 input, is scaled the same way (fp64 product
+ *     of its bf16 value and c, then fp32, then bf16), so it is rounded twice.
+ *     The paper fixes no rounding point for its mixed-precision inference
+ *     (Sec. 4.1; the FlashAttention kernel it names applies the scale to the
+ *     fp32 scores instead).  This point is a convention, chosen because it
+ *     saves the GPU kernel one multiply per logit; the other choice, bf16
+ *     queries with the scale on the logit, moves individual probabilities
+ *     by about 1% at gamma = 10, so the two are not interchangeable at the
+ *     parity bar.  Scoring keys are rounded fp32 -> bf16 the same way.  The
+ *     logits q~ . k are then computed in fp64 on those bf16 values and are
+ *     base-2 logits: the softmax is 2^(s - L) with L = log2 sum_t 2^(s_t),
+ *     which equals exp(q.k/sqrt(d) - lse) up to the bf16 rounding of the
+ *     scaled queries.
  *   - Softmax over all T prompt keys (Sec. 3.2.2 Eq. 7).
  *   - Groups are contiguous proxy blocks I_g = {g*P/G .. (g+1)*P/G - 1}
  *     (Sec. 3.2.2 Eq. 8 leaves the partition open).
@@ -366,42 +371,32 @@ int oracle_build_proxies_at(int B, int Hq, int W, int d, int P, double gamma, in
 /* them, and their projection by the query weights of every head.          */
 /* ------------------------------------------------------------------------ */
 /*
- * Per (batch row, feature dimension): mean and std over the T prompt tokens
- * (Eq. 4), from the sums of the values and of their squares:
- *   mean = S / T,  var = (SS - S * mean) / (T - ddof),  std = sqrt(var)
- * (var clamped at 0).  S and SS are accumulated in consecutive chunks of
- * `chunk` tokens, each summed in token order, and the chunk sums are added
- * in chunk order; this fixes every rounding step.
+ * Per (batch row, feature dimension): mean and standard deviation over the
+ * T prompt tokens (Eq. 4), by their definitions, in two passes:
+ *   mean = (sum_t h_t) / T,
+ *   var  = (sum_t (h_t - mean)^2) / (T - ddof),  std = sqrt(var),
+ * each sum taken sequentially in token order.
  * hidden [B, T, D] (row stride D), dtype 0 fp32 / 1 bf16; stats [B, 2, D].
  */
-int oracle_hidden_stats(int B, int T, int D, int chunk, int ddof, const void *hidden, int dtype,
-                        double *stats)
+int oracle_hidden_stats(int B, int T, int D, int ddof, const void *hidden, int dtype, double *stats)
 {
-    if (B < 1 || T < 1 || D < 1 || chunk < 1 || ddof < 0 || T - ddof < 1)
+    if (B < 1 || T < 1 || D < 1 || ddof < 0 || T - ddof < 1)
         return -1;
 #pragma omp parallel for collapse(2) schedule(static)
     for (int b = 0; b < B; ++b) {
         for (int j = 0; j < D; ++j) {
-            double S = 0.0, SS = 0.0;
-            for (int c0 = 0; c0 < T; c0 += chunk) {
-                int c1 = c0 + chunk < T ? c0 + chunk : T;
-                double s = 0.0, ss = 0.0;
-                for (int t = c0; t < c1; ++t) {
-                    double v = load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j);
-                    double sq = v * v;
-                    s = s + v;
-                    ss = ss + sq;
-                }
-                S = S + s;
-                SS = SS + ss;
+            double s = 0.0;
+            for (int t = 0; t < T; ++t)
+                s = s + load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j);
+            double mean = s / (double)T;
+            double ss = 0.0;
+            for (int t = 0; t < T; ++t) {
+                double dv = load_elem(hidden, dtype, ((int64_t)b * T + t) * D + j) - mean;
+                double sq = dv * dv;
+                ss = ss + sq;
             }
-            double mean = S / (double)T;
-            double sm = S * mean;
-            double var = (SS - sm) / (double)(T - ddof);
-            if (var < 0.0)
-                var = 0.0;
             stats[((int64_t)b * 2) * D + j] = mean;
-            stats[((int64_t)b * 2 + 1) * D + j] = sqrt(var);
+            stats[((int64_t)b * 2 + 1) * D + j] = sqrt(ss / (double)(T - ddof));
         }
     }
     return 0;

@@ -178,3 +178,35 @@ def check_layer(gpu: dict, ref, cfg, budget, k_np, v_np, keep_last=True, budgets
     rep["heads"] = B * H
     rep["sel_symdiff"] = sym
     return rep
+
+
+U64 = 2.0 ** -53     # unit roundoff of fp64
+
+
+def check_hidden_stats(gpu, h64, ref, ddof=0):
+    """GPU hidden-state statistics [B, 2, D] against the oracle's two-pass
+    definition (Sec. 3.2.1 Eq. 4), within the fp64 rounding bound of ANY
+    summation of the tokens by sums of values and of squares (the GPU's
+    chunked one-pass form).  With n = T tokens, u = 2^-53 and every input
+    and square exact in fp64:
+      |S~ - S| <= (n-1) u sum|h|,  |SS~ - SS| <= (n-1) u SS,
+      mean:  |mean~ - mean| <= ((n+1) u sum|h|) / n + u |mean|,
+      var:   the numerator SS - S*mean loses at most ~3 n u SS (S^2/n <= SS
+             and (sum|h|)^2 <= n SS by Cauchy-Schwarz), so
+             |var~ - var| <= tol = (4n + 8) u SS / (n - ddof),
+      std:   |sqrt(a) - sqrt(b)| <= min(sqrt|a-b|, |a-b| / (sqrt a + sqrt b)).
+    h64: the hidden states [B, T, D] as fp64 values."""
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    n = h64.shape[1]
+    sabs = np.abs(h64).sum(axis=1)
+    ss = (h64 * h64).sum(axis=1)
+    tol_mean = (2 * n + 4) * U64 * sabs / n + 4 * U64 * np.abs(ref[:, 0])
+    dm = np.abs(gpu[:, 0] - ref[:, 0])
+    assert np.all(dm <= tol_mean), "mean outside the fp64 bound (max excess %r)" % float((dm - tol_mean).max())
+    tol_var = (4 * n + 8) * U64 * ss / (n - ddof)
+    sg, sr = gpu[:, 1], ref[:, 1]
+    tol_std = np.minimum(np.sqrt(tol_var), tol_var / np.maximum(sg + sr, 1e-300)) + 4 * U64 * sr
+    ds = np.abs(sg - sr)
+    assert np.all(ds <= tol_std), "std outside the fp64 bound (max excess %r)" % float((ds - tol_std).max())
+    return float((ds / np.maximum(sr, 1e-300)).max())

@@ -27,30 +27,46 @@ def hidden_states(B, T, D, seed, scale=1.0):
 
 
 # ---------------------------------------------------------------- Eq. 4
-@pytest.mark.parametrize("T,chunk", [(1, 256), (5, 2), (300, 256), (512, 256), (777, 64), (40, 1), (33, 33)])
-def test_hidden_stats_match_numpy(oracle_lib, T, chunk):
-    """Mean and std per (batch row, feature) over all prompt tokens; a wrong
-    axis, a dropped chunk or a wrong divisor moves these far off."""
+@pytest.mark.parametrize("T", [1, 2, 5, 40, 300, 512, 777])
+def test_hidden_stats_match_numpy(oracle_lib, T):
+    """Mean and std per (batch row, feature) over all prompt tokens, against
+    numpy's mean / std (ddof 0 and 1); a wrong axis, a dropped token or a
+    wrong divisor moves these far off."""
     h = hidden_states(2, T, 24, T)
-    st = oracle_lib.hidden_stats(h, ddof=0, chunk=chunk)
+    st = oracle_lib.hidden_stats(h, ddof=0)
     h64 = h.astype(np.float64)
     np.testing.assert_allclose(st[:, 0], h64.mean(axis=1), rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(st[:, 1], h64.std(axis=1, ddof=0), rtol=1e-10, atol=1e-13)
     if T > 1:
-        st1 = oracle_lib.hidden_stats(h, ddof=1, chunk=chunk)
+        st1 = oracle_lib.hidden_stats(h, ddof=1)
         np.testing.assert_allclose(st1[:, 1], h64.std(axis=1, ddof=1), rtol=1e-10, atol=1e-13)
 
 
-def test_hidden_stats_chunk_merge_exact_small_case(oracle_lib):
-    """Tokens 1, 2, 3 | 4, 5 (chunk 3): S = 15, SS = 55, so mean 3 and
-    SS - S*mean = 10 exactly: population std sqrt(2), sample std sqrt(2.5);
-    a dropped chunk or a square missing from SS fails."""
+def test_hidden_stats_exact_small_case(oracle_lib):
+    """Tokens 1..5: mean 3, squared deviations 4, 1, 0, 1, 4 (sum 10), so the
+    population std is sqrt(2) and the sample std sqrt(2.5), exactly; a
+    dropped token, a missing square or a wrong divisor fails."""
     h = np.array([1, 2, 3, 4, 5], dtype=np.float32).reshape(1, 5, 1)
-    st = oracle_lib.hidden_stats(h, ddof=0, chunk=3)
+    st = oracle_lib.hidden_stats(h, ddof=0)
     assert st[0, 0, 0] == 3.0
     assert st[0, 1, 0] == math.sqrt(2.0)
-    st1 = oracle_lib.hidden_stats(h, ddof=1, chunk=3)
+    st1 = oracle_lib.hidden_stats(h, ddof=1)
     assert st1[0, 1, 0] == math.sqrt(2.5)
+
+
+def test_hidden_stats_large_offset_is_stable(oracle_lib):
+    """Features with a mean far above their spread (6e7 + a spread of a few
+    units, exact in fp32): the squared deviations about the mean keep the
+    std exact to rounding, where E[h^2] - E[h]^2 in fp64 loses every digit
+    (the sum of squares ~3.6e18 has an ulp of 512)."""
+    rng = np.random.default_rng(5)
+    T = 1000
+    spread = rng.integers(-8, 9, size=(1, T, 3)).astype(np.float64) * 4.0
+    h = (6.0e7 + spread).astype(np.float32)
+    assert np.array_equal(h.astype(np.float64), 6.0e7 + spread)
+    st = oracle_lib.hidden_stats(h)
+    np.testing.assert_allclose(st[0, 1], spread[0].std(axis=0), rtol=1e-12)
+    np.testing.assert_allclose(st[0, 0], 6.0e7 + spread[0].mean(axis=0), rtol=1e-15)
 
 
 def test_hidden_stats_constant_and_bf16_input(oracle_lib):
@@ -59,7 +75,7 @@ def test_hidden_stats_constant_and_bf16_input(oracle_lib):
     h = hidden_states(1, 300, 8, 7)
     h[0, :, 3] = 1.25
     hb = bf16_bits(h)
-    st = oracle_lib.hidden_stats(hb, chunk=128)
+    st = oracle_lib.hidden_stats(hb)
     assert st[0, 0, 3] == 1.25 and st[0, 1, 3] == 0.0
     ref = brute.bits_to_f64(hb)
     np.testing.assert_allclose(st[:, 0], ref.mean(axis=1), rtol=1e-12, atol=1e-14)

@@ -89,6 +89,43 @@ def test_proxy_composition_rounding(oracle_lib):
             assert np.array_equal(prox[0, h, i], bf16_bits(x.astype(np.float32)))
 
 
+def test_expected_score_closed_form_eq14(oracle_lib):
+    """Appendix A Eq. 14: for a Gaussian query q ~ N(mu, Sigma) and a fixed key
+    k, E[exp(q.k / sqrt(d))] = exp(mu.k / sqrt(d) + k^T Sigma k / (2d)); with
+    the proxies' law Sigma = diag((gamma sigma)^2) (Eq. 5).  The Monte-Carlo
+    mean of 2^(q~ . k) over 2^20 oracle proxies (q~ carries log2(e)/sqrt(d),
+    so 2^(q~.k) is exp(q.k/sqrt(d)) up to the bf16 rounding of q~) must match
+    the closed form within 5 standard errors plus the worst-case effect of
+    that rounding, computed per sample: |ln2 (q~.k) - q.k/sqrt(d)| <=
+    ln2 (2^-8 + 2^-23) sum_j |q~_j k_j|.  sigma and k are large on the same
+    dimensions, so a dropped variance term (-11%), gamma applied to the
+    variance (-10%), noise scales paired with the wrong dimensions (-10%) or
+    a wrong-signed mean (x0.55) all fail by far more than the tolerance."""
+    d, P, gamma = 16, 1 << 20, 0.3
+    mu = np.array([0.25, -0.125, 0.375, 0.25, -0.25, 0.125, 0.5, -0.375] * 2, dtype=np.float64)
+    sigma = np.array([1.5] * 8 + [0.25] * 8, dtype=np.float64)
+    k = np.array([1.5, -1.5, 1.5, 1.5, -1.5, 1.5, 1.5, -1.5] + [0.5, -0.5] * 4, dtype=np.float64)
+    # two window queries mu -/+ sigma: mean mu and population std sigma, exactly
+    q = np.stack([mu - sigma, mu + sigma]).astype(np.float32).reshape(1, 1, 2, d)
+    prox, _, st = oracle_lib.build_proxies(q, P, gamma, seed=2024)
+    assert np.array_equal(st[0, 0, 0], mu) and np.array_equal(st[0, 0, 1], sigma)
+    x = brute.bits_to_f64(prox[0, 0])                      # [P, d], scaled by log2(e)/sqrt(d)
+    t = np.exp2(x @ k)
+    m = t.mean()
+    se = t.std() / math.sqrt(P)
+    e = (2.0 ** -8 + 2.0 ** -23) * (np.abs(x) * np.abs(k)).sum(axis=1)
+    rnd = float((t * np.expm1(e * math.log(2.0))).mean())
+    closed = math.exp(mu @ k / math.sqrt(d) + gamma ** 2 * np.sum(sigma ** 2 * k ** 2) / (2 * d))
+    tol = 5 * se + rnd
+    assert abs(m - closed) <= tol, (m, closed, se, rnd)
+    # the tolerance is tight enough to reject each plausible mistake
+    for wrong in (math.exp(mu @ k / math.sqrt(d)),
+                  math.exp(mu @ k / math.sqrt(d) + gamma ** 4 * np.sum(sigma ** 2 * k ** 2) / (2 * d)),
+                  math.exp(mu @ k / math.sqrt(d) + gamma ** 2 * np.sum(sigma[::-1] ** 2 * k ** 2) / (2 * d)),
+                  math.exp(-mu @ k / math.sqrt(d) + gamma ** 2 * np.sum(sigma ** 2 * k ** 2) / (2 * d))):
+        assert abs(wrong - closed) > 3 * tol, (wrong, closed, tol)
+
+
 def test_gamma_zero_proxies_are_the_mean(oracle_lib):
     q, _ = rand_inputs(1, 3, 1, 4, 9, 16, 2)
     prox, _, st = oracle_lib.build_proxies(q, 5, 0.0, seed=3)
