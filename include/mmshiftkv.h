@@ -53,7 +53,9 @@ typedef enum {
     MMSKV_MASS = 1  /* total proxy mass (votes and anchor not used) */
 } mmskv_mode;
 
-/* Problem sizes of one layer.
+/* Problem sizes of one layer.  Each call reads the fields its comment names
+ * (the proxy, score, decode and window calls read all of them; the others
+ * ignore the rest, which may then hold any value).
  *   B    batch rows (<= 65535)        Hq   query heads
  *   Hkv  KV heads (Hq % Hkv == 0; the Gh = Hq/Hkv query heads h with
  *        h / Gh == c share KV head c)
@@ -169,7 +171,8 @@ int mmshiftkv_score_mass(const mmskv_shape *shape, const mmskv_params *params,
  *   votes  [B, Hkv, T] uint8 out or NULL (VOTE mode only)
  * Requires c_max >= min(C, T) for every head (checked on the host for the
  * scalar budget; per-head budgets above c_max are clamped to c_max).
- * Workspace: mmshiftkv_select_workspace bytes. */
+ * Reads shape->B, Hq, Hkv, T (W and d are ignored) and params->P, G, tau,
+ * lambda, mode, keep_last.  Workspace: mmshiftkv_select_workspace bytes. */
 size_t mmshiftkv_select_workspace(const mmskv_shape *shape, const mmskv_params *params);
 int mmshiftkv_select_topk(const mmskv_shape *shape, const mmskv_params *params,
                           const float *group_mass, const float *mass, const float *anchor,
@@ -180,7 +183,9 @@ int mmshiftkv_select_topk(const mmskv_shape *shape, const mmskv_params *params,
 /* Step 4 -- compacted cache (Appendix B: retained tokens in temporal order,
  * inserted through the standard cache update).  For j < counts[b,c]:
  *   k_out[b,c,j,:] = k[b,c,idx[b,c,j],:], v_out likewise (byte copies);
- * rows j >= counts[b,c] are zero-filled.
+ * rows j >= counts[b,c] are zero-filled.  Reads shape->B, Hkv, T and d
+ * (Hq and W are ignored); a row of d elements must be a whole number of
+ * 16-byte vectors (d * element size % 16 == 0, d <= 65536).
  *   k, v          [B, Hkv, T, d] dtype, strides k_strides / v_strides
  *   k_out, v_out  [B, Hkv, c_max, d] dtype, contiguous
  * idx entries outside [0, T) are not read (their row is zero-filled). */
@@ -300,7 +305,8 @@ typedef enum {
     MMSKV_SHAPE_SINKS = 2      /* t < sinks kept, else mass[t] */
 } mmskv_shape_kind;
 
-/* Per-key baseline score from a mass (fp32 sums in ascending u):
+/* Per-key baseline score from a mass (fp32 sums in ascending u); reads
+ * shape->B, Hkv and T only:
  *   mass   [B, Hkv, T] fp32 (may be NULL for MMSKV_SHAPE_STREAMING)
  *   score  [B, Hkv, T] fp32 out
  * 0 <= window <= T, sinks >= 0, pool odd >= 1, T <= 2^24. */

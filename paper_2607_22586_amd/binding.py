@@ -359,8 +359,7 @@ def select_topk(s: ScoreOut, cfg: SelectionConfig, budget: int, c_max: int | Non
     B, Hkv, T = s.mass.shape
     Hq = Hkv if Hq is None else Hq
     c_max = int(budget if c_max is None else c_max)
-    d = 64
-    shape = _shape(B, Hq, Hkv, T, W, d)
+    shape = _shape(B, Hq, Hkv, T, 0, 0)           # W and d are not read by the selection
     prm = cfg.c_params()
     lib = load_library()
     need = int(lib.mmshiftkv_select_workspace(ctypes.byref(shape), ctypes.byref(prm)))
@@ -435,7 +434,7 @@ def shape_scores(mass: torch.Tensor | None, kind: int, B: int, Hkv: int, T: int,
     """mmshiftkv_shape_scores: per-key baseline scores [B, Hkv, T] fp32."""
     dev = _dev(mass) if mass is not None else torch.device(device if device is not None else "cuda:0")
     score = out if out is not None else torch.empty((B, Hkv, T), dtype=torch.float32, device=dev)
-    shape = _shape(B, Hkv, Hkv, T, 1, 64)
+    shape = _shape(B, 0, Hkv, T, 0, 0)            # only B, Hkv and T are read
     with torch.cuda.device(dev):
         rc = load_library().mmshiftkv_shape_scores(ctypes.byref(shape), int(kind), int(window), int(pool), int(sinks),
                                                    _p(mass), _p(score), _stream(dev))
@@ -485,7 +484,7 @@ def gather_kv(k: torch.Tensor, v: torch.Tensor, sel: Selected, out=None):
     if v.shape != k.shape or v.dtype != k.dtype:
         raise ValueError("k and v must have the same shape and dtype")
     c_max = sel.idx.shape[2]
-    shape = _shape(B, Hkv, Hkv, T, 1, d)
+    shape = _shape(B, 0, Hkv, T, 0, d)            # Hq and W are not read by the gather
     if out is None:
         out = (torch.empty((B, Hkv, c_max, d), dtype=k.dtype, device=dev),
                torch.empty((B, Hkv, c_max, d), dtype=k.dtype, device=dev))

@@ -26,29 +26,44 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 
 int elem_bytes(int32_t dtype) { return dtype == MMSKV_F32 ? 4 : (dtype == MMSKV_BF16 ? 2 : 0); }
 
-int check_shape(const mmskv_shape* s) {
+// The head layout every call reads: B, Hq, Hkv (Hq % Hkv == 0) and T.
+int check_heads(const mmskv_shape* s) {
     if (s == nullptr) return MMSKV_EINVAL;
-    if (s->B < 1 || s->B > 65535 || s->Hq < 1 || s->Hkv < 1 || s->T < 1 || s->W < 1 || s->d < 1)
-        return MMSKV_EINVAL;
+    if (s->B < 1 || s->B > 65535 || s->Hq < 1 || s->Hkv < 1 || s->Hkv > 65535 || s->T < 1) return MMSKV_EINVAL;
     if (s->Hq % s->Hkv != 0) return MMSKV_EINVAL;
-    if (s->Hkv > 65535) return MMSKV_EINVAL;
+    return MMSKV_OK;
+}
+
+// The whole shape, for the calls that read the window queries and scores.
+int check_shape(const mmskv_shape* s) {
+    int rc = check_heads(s);
+    if (rc) return rc;
+    if (s->W < 1 || s->d < 1) return MMSKV_EINVAL;
     if (s->d != 64 && s->d != 128) return MMSKV_EUNSUPPORTED;
     return MMSKV_OK;
 }
 
-int check_params(const mmskv_shape* s, const mmskv_params* p) {
+// The parameters that the selection reads (group layout, tau, lambda, mode).
+int check_method(const mmskv_params* p) {
     if (p == nullptr) return MMSKV_EINVAL;
     if (p->P < 1 || p->G < 1 || p->P % p->G != 0) return MMSKV_EINVAL;
     if (p->G > 255) return MMSKV_EUNSUPPORTED;
     if ((p->P / p->G) % 16 != 0 || p->P % 32 != 0) return MMSKV_EUNSUPPORTED;
-    if (!(p->gamma >= 0.0) || !isfinite(p->gamma)) return MMSKV_EINVAL;
     if (!(p->tau > 0.0 && p->tau <= 1.0)) return MMSKV_EINVAL;
     if (!(p->lambda >= 0.0) || !isfinite(p->lambda)) return MMSKV_EINVAL;
+    if (p->mode != MMSKV_VOTE && p->mode != MMSKV_MASS) return MMSKV_EINVAL;
+    if (p->keep_last != 0 && p->keep_last != 1) return MMSKV_EINVAL;
+    return MMSKV_OK;
+}
+
+// Every parameter (the proxy and score calls).
+int check_params(const mmskv_shape* s, const mmskv_params* p) {
+    int rc = check_method(p);
+    if (rc) return rc;
+    if (!(p->gamma >= 0.0) || !isfinite(p->gamma)) return MMSKV_EINVAL;
     if (p->std_ddof != 0 && p->std_ddof != 1) return MMSKV_EINVAL;
     if (s->W - p->std_ddof < 1) return MMSKV_EINVAL;
     if (p->layer < 0 || p->layer > 65535) return MMSKV_EINVAL;
-    if (p->mode != MMSKV_VOTE && p->mode != MMSKV_MASS) return MMSKV_EINVAL;
-    if (p->keep_last != 0 && p->keep_last != 1) return MMSKV_EINVAL;
     return MMSKV_OK;
 }
 
@@ -137,6 +152,7 @@ int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const ui
     a->rows = l.rows;
     a->rows_pad = l.rows_pad;
     a->anchor_scale = query_scale(shape->d);
+    a->lane_sum_hi = lane_sum_limit(shape->T);
     a->part = static_cast<float2*>(ws);
     a->lse = reinterpret_cast<float*>(static_cast<char*>(ws) + l.lse_off);
     a->group_mass = nullptr;
@@ -276,7 +292,7 @@ int mmshiftkv_score(const mmskv_shape* shape, const mmskv_params* params, const 
 }
 
 size_t mmshiftkv_select_workspace(const mmskv_shape* shape, const mmskv_params* params) {
-    if (check_shape(shape) || check_params(shape, params)) return 0;
+    if (check_heads(shape) || check_method(params)) return 0;
     return select_layout(shape, params).total;
 }
 
@@ -284,9 +300,9 @@ int mmshiftkv_select_topk(const mmskv_shape* shape, const mmskv_params* params, 
                           const float* mass, const float* anchor, const int32_t* budgets, int32_t budget,
                           int32_t c_max, int32_t* idx, int32_t* counts, uint8_t* votes, void* workspace,
                           size_t workspace_bytes, void* stream) {
-    int rc = check_shape(shape);
+    int rc = check_heads(shape);
     if (rc) return rc;
-    rc = check_params(shape, params);
+    rc = check_method(params);
     if (rc) return rc;
     if (idx == nullptr || counts == nullptr || c_max < 1) return MMSKV_EINVAL;
     if (budgets == nullptr && (budget < 1 || c_max < (budget < shape->T ? budget : shape->T)))
@@ -334,13 +350,16 @@ int mmshiftkv_gather_kv(const mmskv_shape* shape, const void* k, const void* v, 
                         const mmskv_strides* k_strides, const mmskv_strides* v_strides,
                         const int32_t* idx, const int32_t* counts, int32_t c_max, void* k_out,
                         void* v_out, void* stream) {
-    int rc = check_shape(shape);
-    if (rc) return rc;
-    const int eb = elem_bytes(dtype);
-    if (eb == 0 || k == nullptr || v == nullptr || idx == nullptr || counts == nullptr || c_max < 1 ||
-        k_out == nullptr || v_out == nullptr)
+    if (shape == nullptr) return MMSKV_EINVAL;
+    if (shape->B < 1 || shape->B > 65535 || shape->Hkv < 1 || shape->Hkv > 65535 || shape->T < 1 ||
+        shape->d < 1 || shape->d > 65536)
         return MMSKV_EINVAL;
-    rc = check_rows(k, k_strides, eb, true);
+    const int eb = elem_bytes(dtype);
+    if (eb == 0 || (shape->d * eb) % 16 != 0) return MMSKV_EINVAL;
+    if (k == nullptr || v == nullptr || idx == nullptr || counts == nullptr || c_max < 1 || k_out == nullptr ||
+        v_out == nullptr)
+        return MMSKV_EINVAL;
+    int rc = check_rows(k, k_strides, eb, true);
     if (rc) return rc;
     rc = check_rows(v, v_strides, eb, true);
     if (rc) return rc;
@@ -442,6 +461,7 @@ int mmshiftkv_decode_check(const mmskv_shape* shape, int32_t n_dec, const uint16
     a.rows_pad = decode_rows_pad(a.Gh, n_dec);
     a.n_kb = decode_key_blocks(shape->T);
     a.scale = query_scale(shape->d);
+    a.lane_sum_hi = lane_sum_limit(shape->T);
     a.part = static_cast<float4*>(workspace);
     a.qsc = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + decode_part_bytes(shape, n_dec));
     a.coverage = coverage;
@@ -478,8 +498,9 @@ int mmshiftkv_window_rows(const mmskv_shape* shape, int32_t n, const void* q_win
 
 int mmshiftkv_shape_scores(const mmskv_shape* shape, int32_t kind, int32_t window, int32_t pool, int32_t sinks,
                            const float* mass, float* score, void* stream) {
-    int rc = check_shape(shape);
-    if (rc) return rc;
+    if (shape == nullptr) return MMSKV_EINVAL;
+    if (shape->B < 1 || shape->B > 65535 || shape->Hkv < 1 || shape->Hkv > 65535 || shape->T < 1)
+        return MMSKV_EINVAL;
     if (score == nullptr || !aligned(score, 4)) return MMSKV_EINVAL;
     if (kind < MMSKV_SHAPE_SNAPKV || kind > MMSKV_SHAPE_SINKS) return MMSKV_EINVAL;
     if (kind != MMSKV_SHAPE_STREAMING && (mass == nullptr || !aligned(mass, 4))) return MMSKV_EINVAL;

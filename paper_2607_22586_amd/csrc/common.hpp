@@ -9,7 +9,6 @@ namespace mmskv {
 constexpr int kWave = 64;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // fp32 -> bf16 bit pattern, round to nearest even (inputs are finite).
@@ -41,19 +40,9 @@ __device__ __forceinline__ bf16x8 zero_bf16x8() {
     return __builtin_bit_cast(bf16x8, v);
 }
 
-// D(16x16, fp32) += A(16x32, bf16) * B(32x16, bf16) on one wave.
-// Lane l supplies row (l % 16) of A and column (l % 16) of B, each as eight
-// consecutive k values starting at 8*(l/16); it receives D rows
-// 4*(l/16) + {0,1,2,3} of column (l % 16).
-__device__ __forceinline__ floatx4 mfma16x16x32(bf16x8 a, bf16x8 b, floatx4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
-
-__device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, kWave); }
 
 __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
     uint32_t lo = __shfl(static_cast<uint32_t>(v), src, kWave);
@@ -69,11 +58,6 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
     for (int m = 1; m < kWave; m <<= 1) v += shfl_xor_u64(v, m);
-    return v;
-}
-
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
-    for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
     return v;
 }
 

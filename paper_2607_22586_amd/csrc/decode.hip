@@ -154,8 +154,8 @@ __global__ void __launch_bounds__(64 * kDecWaves) decode_cover_kernel(DecodeArgs
                 for (int s = 0; s < 2; ++s) acc[s] = mfma_32x32x16(kf[s][kc], q, acc[s]);
             }
             // sums of 2^s relative to 0 while every lane's sum is in
-            // [2^-60, 2^120) (as in the row log-sum-exp pass), else relative
-            // to the exact per-column maximum
+            // [2^-60, lane_sum_limit(T)) (as in the row log-sum-exp pass),
+            // else relative to the exact per-column maximum
             float mx = 0.f, la = 0.f, lk = 0.f;
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -165,7 +165,7 @@ __global__ void __launch_bounds__(64 * kDecWaves) decode_cover_kernel(DecodeArgs
                     la += e;
                     lk += ((keep >> (16 * s + i)) & 1u) ? e : 0.f;
                 }
-            const bool in_range = (la >= 0x1p-60f || valid == 0u) && la < 0x1p120f;
+            const bool in_range = (la >= 0x1p-60f || valid == 0u) && la < a.lane_sum_hi;
             if (__ballot(!in_range) != 0) {
                 mx = -INFINITY;
 #pragma unroll

@@ -37,6 +37,7 @@ struct ScoreArgs {
     int rows;                  // Gh * P proxy rows per KV head
     int rows_pad;              // rows + 32 * ceil(Gh / 32) (anchor rows, padded)
     double anchor_scale;       // log2(e) / sqrt(d), applied to the anchor rows
+    float lane_sum_hi;         // pass 1 sums from zero while every lane sum is below this
     float2* part;              // [B, Hkv, n_kb, rows_pad]  (max, sum), base 2
     float* lse;                // [B, Hkv, rows_pad]        log2-domain
     float* group_mass;         // [B, Hkv, G, T] or null
@@ -105,6 +106,7 @@ struct DecodeArgs {
     int rows_pad;              // rows rounded up to 32
     int n_kb;                  // key blocks
     double scale;              // log2(e) / sqrt(d), applied to the queries
+    float lane_sum_hi;         // block sums from zero while every lane sum is below this
     float4* part;              // [B, Hkv, n_kb, rows_pad] (max, sum all, sum kept), base 2
     uint16_t* qsc;             // [B, Hkv, rows_pad, d] scaled decode queries (bf16)
     float* coverage;           // [B, Hq, n_dec]
@@ -126,6 +128,13 @@ struct ShapeArgs {
     float* score;              // [B, Hkv, T]
     int B, Hkv, T, kind, window, pool, sinks;
 };
+
+// Upper end of the lane sums (32 terms of 2^s each) that the score and
+// decode kernels add relative to zero.  A row's total over T keys is made of
+// at most ceil(T/32) such sums, so with every one below 2^(127 - ceil(log2
+// ceil(T/32))) the total stays below 2^127 and no partial or merged sum can
+// overflow fp32; capped at 2^120.
+float lane_sum_limit(int T);
 
 int decode_rows_pad(int Gh, int n_dec);
 int decode_key_blocks(int T);

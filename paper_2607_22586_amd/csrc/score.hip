@@ -50,13 +50,6 @@ __device__ __forceinline__ floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// Compile-time buffer parity for the two-stage software pipeline (keeps the
-// double-buffered accumulators in registers).
-template <int N>
-struct Parity {
-    static constexpr int value = N;
-};
-
 __device__ __forceinline__ floatx16 zero16() {
     floatx16 z;
 #pragma unroll
@@ -368,7 +361,7 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
             const int tp = t - 1;
             float lsum = l0 + l1;
             float mrow = 0.f;
-            const bool in_range = (lsum >= 0x1p-60f || (!FULL && valid == 0u)) && lsum < 0x1p120f;
+            const bool in_range = (lsum >= 0x1p-60f || (!FULL && valid == 0u)) && lsum < a.lane_sum_hi;
             if (__ballot(!in_range) != 0) {
                 // logits out of the range: this tile again with its own maximum
                 float mx = -INFINITY;
@@ -742,6 +735,14 @@ hipError_t mass_impl(const ScoreArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+float lane_sum_limit(int T) {
+    const long n = (static_cast<long>(T) + 31) / 32;   // lane sums per row
+    int bits = 0;
+    while ((1L << bits) < n) ++bits;                   // ceil(log2 n)
+    const int e = 127 - bits < 120 ? 127 - bits : 120;
+    return ldexpf(1.0f, e);
+}
 
 int score_block_waves(int B, int Hkv, int T) {
     // 8-wave blocks (512 keys) when that still gives every CU two blocks of

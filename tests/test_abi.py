@@ -172,6 +172,22 @@ def test_select_rejects(lib):
     assert call(64, 64, votes=FAKE, prm=_params(mode=bd.MMSKV_MASS)) == bd.MMSKV_EINVAL
 
 
+def test_select_ignores_window_and_head_dim(lib):
+    """The selection reads B, Hq, Hkv, T and the method parameters only: W = 0,
+    d = 0 and a gamma / ddof the proxy call would refuse still pass its
+    validation (the call below stops at the workspace check)."""
+    s = _shape(W=0, d=0)
+    p = _params()
+    p.gamma = -1.0
+    p.std_ddof = 7
+    need = lib.mmshiftkv_select_workspace(ctypes.byref(s), ctypes.byref(p))
+    assert need == lib.mmshiftkv_select_workspace(ctypes.byref(_shape()), ctypes.byref(_params())) > 0
+    rc = lib.mmshiftkv_select_topk(ctypes.byref(s), ctypes.byref(p), FAKE, FAKE, FAKE, None, 64, 64, FAKE, FAKE,
+                                   None, FAKE, need - 8, None)
+    assert rc == bd.MMSKV_EWORKSPACE
+    assert lib.mmshiftkv_select_workspace(ctypes.byref(_shape(Hkv=3)), ctypes.byref(p)) == 0   # Hq % Hkv
+
+
 def test_gather_rejects(lib):
     s = _shape()
     st = bd.Strides(1024 * 64, 1024 * 64, 64)
@@ -181,6 +197,10 @@ def test_gather_rejects(lib):
     assert call(out=ctypes.c_void_p(0x10004)) == bd.MMSKV_EINVAL
     assert call(dtype=3) == bd.MMSKV_EINVAL
     assert call(c_max=0) == bd.MMSKV_EINVAL
+    # rows must be whole 16-byte vectors: d = 100 bf16 (200 bytes) is refused
+    odd = _shape(d=100)
+    assert lib.mmshiftkv_gather_kv(ctypes.byref(odd), FAKE, FAKE, 1, ctypes.byref(st), ctypes.byref(st), FAKE,
+                                   FAKE, 64, FAKE, FAKE, None) == bd.MMSKV_EINVAL
 
 
 def test_binding_refuses_host_tensors():
