@@ -39,6 +39,11 @@ def bits(t):
     return wl.to_numpy_bits(t)
 
 
+def values(a):
+    """fp64 values of an oracle input array (fp32, or bf16 bits as uint16)."""
+    return a.astype(np.float64) if a.dtype == np.float32 else brute.bits_to_f64(a)
+
+
 def bf16_ulp(x):
     """Spacing of bf16 numbers at |x| (normal range)."""
     _, e = np.frexp(np.maximum(np.abs(x), 2.0 ** -120))
@@ -90,7 +95,7 @@ def test_hidden_stats_within_fp64_bound(B, T, D, dtype, ddof, pad):
     torch.cuda.synchronize()
     hb = bits(x[:, :, :D].contiguous())
     ref = oracle.hidden_stats(hb, ddof=ddof)
-    rel = parity.check_hidden_stats(st.cpu().numpy(), brute.bits_to_f64(hb), ref, ddof)
+    rel = parity.check_hidden_stats(st.cpu().numpy(), values(hb), ref, ddof)
     print("hidden stats", (B, T, D, dtype, ddof), "max relative std difference", rel, flush=True)
 
 
@@ -156,7 +161,7 @@ def test_hidden_path_layer_parity():
     hb = bits(hx["hidden"])
     rst = oracle.hidden_stats(hb)
     st_np = st.cpu().numpy()
-    parity.check_hidden_stats(st_np, brute.bits_to_f64(hb), rst)
+    parity.check_hidden_stats(st_np, values(hb), rst)
     # the samples from the GPU's statistics (the generator is checked on equal inputs)
     rhp = oracle.hidden_proxies(st_np, cfg.P, cfg.gamma, cfg.seed, cfg.layer)
     assert np.array_equal(bits(hp), rhp)
@@ -190,7 +195,7 @@ def test_full_size_hidden_sampled(name):
     sub = bits(hx["hidden"][:, :, torch.as_tensor(cols, device=DEV)].contiguous())
     rst = oracle.hidden_stats(sub)
     st_np = st.cpu().numpy()
-    parity.check_hidden_stats(st_np[:, :, cols], brute.bits_to_f64(sub), rst)
+    parity.check_hidden_stats(st_np[:, :, cols], values(sub), rst)
     for b in (0, 3):
         rhp = oracle.hidden_proxies(st_np[b:b + 1], cfg.P, cfg.gamma, cfg.seed, layer, b0=b)
         assert np.array_equal(bits(hp[b:b + 1]), rhp), "samples of batch row %d differ" % b
