@@ -26,7 +26,8 @@
  *     MMSKV_EHIP reports a launch error from the HIP runtime.
  *   - bf16 tensors are passed as uint16_t bit patterns.
  *   - Inputs containing NaN or Inf give unspecified (but memory-safe) results.
- *   - Calls are thread-safe; the library holds no mutable global state.
+ *   - Calls are thread-safe.  The only global state is the per-GPU scratch
+ *     array of mmshiftkv_score_noalloc (see there).
  */
 #ifndef MMSHIFTKV_H
 #define MMSHIFTKV_H
@@ -43,7 +44,9 @@ typedef enum {
     MMSKV_EINVAL = -1,       /* invalid argument: shape, pointer, parameter */
     MMSKV_EUNSUPPORTED = -2, /* valid per the paper but not built: see each call */
     MMSKV_EWORKSPACE = -3,   /* workspace pointer NULL or smaller than required */
-    MMSKV_EHIP = -4          /* the HIP runtime reported a launch error */
+    MMSKV_EHIP = -4,         /* the HIP runtime reported a launch error */
+    MMSKV_ESCRATCH = -5      /* mmshiftkv_score_noalloc: the problem needs more
+                                than MMSKV_NOALLOC_SCRATCH_BYTES of scratch */
 } mmskv_status;
 
 typedef enum { MMSKV_F32 = 0, MMSKV_BF16 = 1 } mmskv_dtype;
@@ -141,6 +144,27 @@ int mmshiftkv_score(const mmskv_shape *shape, const mmskv_params *params,
                     const void *k, int32_t k_dtype, const mmskv_strides *k_strides,
                     float *group_mass, float *mass, float *anchor,
                     void *workspace, size_t workspace_bytes, void *stream);
+
+/* mmshiftkv_score without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): same arguments, results and kernels as
+ * mmshiftkv_score, with the scratch memory taken from a library-owned array
+ * of MMSKV_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU instead of the workspace.
+ * The call itself allocates nothing and never frees; the array of a GPU is
+ * set up on the first call with that GPU current and held until the process
+ * ends.  It runs on the CURRENT device (hipGetDevice), so `stream` must
+ * belong to that device.  Every call on one GPU shares that GPU's array:
+ * calls that overlap in time on one GPU (different streams, or threads
+ * without ordering) race and give undefined results; calls ordered on one
+ * stream are safe.  Nothing in the array needs clearing between calls (each
+ * call writes every byte it reads first).  A problem whose workspace
+ * (mmshiftkv_score_workspace) exceeds the array returns MMSKV_ESCRATCH with
+ * nothing enqueued; the benchmark workloads need at most ~17 MiB. */
+#define MMSKV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int mmshiftkv_score_noalloc(const mmskv_shape *shape, const mmskv_params *params,
+                            const uint16_t *proxies, const uint16_t *q_last,
+                            const void *k, int32_t k_dtype, const mmskv_strides *k_strides,
+                            float *group_mass, float *mass, float *anchor, void *stream);
 
 /* The two passes of mmshiftkv_score as separate calls (same arguments and
  * workspace), for callers that schedule or time them separately:

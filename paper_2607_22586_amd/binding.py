@@ -16,7 +16,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmmshiftkv.so")
 
-MMSKV_OK, MMSKV_EINVAL, MMSKV_EUNSUPPORTED, MMSKV_EWORKSPACE, MMSKV_EHIP = 0, -1, -2, -3, -4
+MMSKV_OK, MMSKV_EINVAL, MMSKV_EUNSUPPORTED, MMSKV_EWORKSPACE, MMSKV_EHIP, MMSKV_ESCRATCH = 0, -1, -2, -3, -4, -5
+NOALLOC_SCRATCH_BYTES = 32 << 20
 MMSKV_F32, MMSKV_BF16 = 0, 1
 MMSKV_VOTE, MMSKV_MASS = 0, 1
 
@@ -25,7 +26,8 @@ EXPORTED = ("mmshiftkv_build_proxies", "mmshiftkv_score_workspace", "mmshiftkv_s
             "mmshiftkv_select_topk", "mmshiftkv_gather_kv", "mmshiftkv_status_string",
             "mmshiftkv_version", "mmshiftkv_hidden_stats_workspace", "mmshiftkv_hidden_stats",
             "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies", "mmshiftkv_decode_workspace",
-            "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores")
+            "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores",
+            "mmshiftkv_score_noalloc")
 
 
 class Shape(ctypes.Structure):
@@ -75,6 +77,7 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_score.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V, SZ, V]
     lib.mmshiftkv_score_lse.argtypes = [PS, PP, V, V, V, I32, PT, V, SZ, V]
     lib.mmshiftkv_score_mass.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V, SZ, V]
+    lib.mmshiftkv_score_noalloc.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V]
     lib.mmshiftkv_select_workspace.argtypes = [PS, PP]
     lib.mmshiftkv_select_workspace.restype = SZ
     lib.mmshiftkv_select_topk.argtypes = [PS, PP, V, V, V, V, I32, I32, V, V, V, V, SZ, V]
@@ -96,7 +99,8 @@ def load_library(path: str | None = None):
     for name in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_score_lse",
                  "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_gather_kv",
                  "mmshiftkv_hidden_stats", "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies",
-                 "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores"):
+                 "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores",
+            "mmshiftkv_score_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -330,6 +334,26 @@ def score(proxies, q_last, k, cfg: SelectionConfig, W: int = 1, out: ScoreOut | 
           workspace: torch.Tensor | None = None) -> ScoreOut:
     """mmshiftkv_score: group masses, total mass and anchor for every (b, KV head)."""
     return _score_call("full", proxies, q_last, k, cfg, W, out, workspace)
+
+
+def score_noalloc(proxies, q_last, k, cfg: SelectionConfig, out: ScoreOut, W: int = 1) -> ScoreOut:
+    """mmshiftkv_score_noalloc: mmshiftkv_score with the library's per-GPU
+    scratch instead of a workspace (the outputs `out` are the caller's)."""
+    dev = _dev(k)
+    B, Hkv, T, d = k.shape
+    Hq = proxies.shape[1]
+    if proxies.dtype != torch.bfloat16 or q_last.dtype != torch.bfloat16:
+        raise TypeError("proxies and q_last are bf16")
+    if not (proxies.is_contiguous() and q_last.is_contiguous()):
+        raise ValueError("proxies and q_last must be contiguous")
+    shape = _shape(B, Hq, Hkv, T, W, d)
+    prm = cfg.c_params()
+    with torch.cuda.device(dev):
+        rc = load_library().mmshiftkv_score_noalloc(
+            ctypes.byref(shape), ctypes.byref(prm), _p(proxies), _p(q_last), _p(k), _dtype_code(k),
+            ctypes.byref(_strides4(k)), _p(out.group_mass), _p(out.mass), _p(out.anchor), _stream(dev))
+    _check("mmshiftkv_score_noalloc", rc)
+    return out
 
 
 def score_lse(proxies, q_last, k, cfg: SelectionConfig, workspace: torch.Tensor, W: int = 1):

@@ -3,6 +3,9 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "../../include/mmshiftkv.h"
 #include "kernels.hpp"
 
@@ -194,6 +197,7 @@ const char* mmshiftkv_status_string(int status) {
         case MMSKV_EUNSUPPORTED: return "unsupported configuration";
         case MMSKV_EWORKSPACE: return "workspace missing, misaligned or too small";
         case MMSKV_EHIP: return "HIP launch error";
+        case MMSKV_ESCRATCH: return "problem needs more scratch memory than the allocation-free entry point holds";
         default: return "unknown status";
     }
 }
@@ -289,6 +293,59 @@ int mmshiftkv_score(const mmskv_shape* shape, const mmskv_params* params, const 
     rc = status_of(launch_score_lse(a, s));
     if (rc) return rc;
     return status_of(launch_score_mass(a, s));
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch memory of mmshiftkv_score_noalloc: one array per GPU, held until
+// the process ends.  In host code `scratch` names a host-side stand-in, so
+// the device address of each GPU's copy is taken once, with that GPU
+// current, and only that address is handed to the kernels.
+constexpr size_t kScratchBytes = MMSKV_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+int scratch_address(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MMSKV_EHIP;
+    void* p = g_scratch[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch[dev].load(std::memory_order_relaxed);
+        if (p == nullptr) {
+            if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return MMSKV_EHIP;
+            g_scratch[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return MMSKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mmshiftkv_score_noalloc(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                            const uint16_t* q_last, const void* k, int32_t k_dtype,
+                            const mmskv_strides* k_strides, float* group_mass, float* mass, float* anchor,
+                            void* stream) {
+    int rc = check_shape(shape);
+    if (rc) return rc;
+    rc = check_params(shape, params);
+    if (rc) return rc;
+    if (score_layout(shape, params).total > kScratchBytes) return MMSKV_ESCRATCH;
+    void* ws = nullptr;
+    rc = scratch_address(&ws);
+    if (rc) return rc;
+    // every byte of the workspace that the passes read is written first by
+    // the same call, so nothing needs clearing
+    return mmshiftkv_score(shape, params, proxies, q_last, k, k_dtype, k_strides, group_mass, mass, anchor, ws,
+                           kScratchBytes, stream);
 }
 
 size_t mmshiftkv_select_workspace(const mmskv_shape* shape, const mmskv_params* params) {

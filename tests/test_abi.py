@@ -285,3 +285,19 @@ def test_baseline_calls_reject(lib):
     assert shp(mass=None) == bd.MMSKV_EINVAL          # SnapKV needs the masses
     assert shp(score=None) == bd.MMSKV_EINVAL
     assert shp(sinks=-1) == bd.MMSKV_EINVAL
+
+
+def test_score_noalloc_refuses_problems_beyond_its_array(lib):
+    """The allocation-free score call refuses, before touching the GPU, a
+    problem whose workspace exceeds its fixed per-GPU scratch array."""
+    shape = _shape(B=64, Hq=28, Hkv=4, T=16384, W=64, d=128)
+    p = _params()
+    assert lib.mmshiftkv_score_workspace(ctypes.byref(shape), ctypes.byref(p)) > bd.NOALLOC_SCRATCH_BYTES
+    st = bd.Strides(4 * 16384 * 128, 16384 * 128, 128)
+    rc = lib.mmshiftkv_score_noalloc(ctypes.byref(shape), ctypes.byref(p), FAKE, FAKE, FAKE, 1, ctypes.byref(st),
+                                     FAKE, FAKE, FAKE, None)
+    assert rc == bd.MMSKV_ESCRATCH
+    assert lib.mmshiftkv_score_noalloc(ctypes.byref(_shape(d=96)), ctypes.byref(p), FAKE, FAKE, FAKE, 1,
+                                       ctypes.byref(st), FAKE, FAKE, FAKE, None) == bd.MMSKV_EUNSUPPORTED
+    text = open(HEADER).read()
+    assert "MMSKV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)" in text and bd.NOALLOC_SCRATCH_BYTES == 32 << 20
