@@ -85,21 +85,26 @@ int check_rows(const void* base, const mmskv_strides* st, int eb, bool vec16) {
 int status_of(hipError_t e) { return e == hipSuccess ? MMSKV_OK : MMSKV_EHIP; }
 
 struct ScoreLayout {
-    int block_keys, n_kb, rows, rows_pad;
-    size_t part_bytes, lse_off, total;
+    ScorePlan plan;
+    int n_kb, block_keys, mass_n_kb, rows, rows_pad;
+    size_t part_bytes, lse_off, anchor_off, total;
 };
 
 ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
     ScoreLayout l;
     const int Gh = s->Hq / s->Hkv;
-    l.block_keys = 64 * score_block_waves(s->B, s->Hkv, s->T);
-    l.n_kb = (s->T + l.block_keys - 1) / l.block_keys;
+    l.plan = score_plan(s->B, s->Hkv, s->T);
+    const int lse_keys = 32 * l.plan.lse_sub * l.plan.lse_waves;
+    l.n_kb = (s->T + lse_keys - 1) / lse_keys;
+    l.block_keys = 64 * l.plan.mass_waves;
+    l.mass_n_kb = (s->T + l.block_keys - 1) / l.block_keys;
     l.rows = Gh * p->P;
     l.rows_pad = l.rows + 32 * ((Gh + 31) / 32);
     const size_t heads = static_cast<size_t>(s->B) * s->Hkv;
     l.part_bytes = heads * l.n_kb * l.rows_pad * sizeof(float2);
     l.lse_off = align_up(l.part_bytes);
-    l.total = l.lse_off + align_up(heads * l.rows_pad * sizeof(float));
+    l.anchor_off = l.lse_off + align_up(heads * l.rows_pad * sizeof(float));
+    l.total = l.anchor_off + align_up(heads * (l.rows_pad - l.rows) * s->d * sizeof(uint16_t));
     return l;
 }
 
@@ -150,14 +155,18 @@ int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const ui
     a->P = params->P;
     a->G = params->G;
     a->Gh = shape->Hq / shape->Hkv;
-    a->block_keys = l.block_keys;
+    a->lse_waves = l.plan.lse_waves;
+    a->lse_sub = l.plan.lse_sub;
     a->n_kb = l.n_kb;
+    a->block_keys = l.block_keys;
+    a->mass_n_kb = l.mass_n_kb;
     a->rows = l.rows;
     a->rows_pad = l.rows_pad;
     a->anchor_scale = query_scale(shape->d);
-    a->lane_sum_hi = lane_sum_limit(shape->T);
+    a->lane_sum_hi = lane_sum_limit(shape->T, 16);     // pass 1 sums 16 keys per lane and chain
     a->part = static_cast<float2*>(ws);
     a->lse = reinterpret_cast<float*>(static_cast<char*>(ws) + l.lse_off);
+    a->anchors = reinterpret_cast<const uint16_t*>(static_cast<char*>(ws) + l.anchor_off);
     a->group_mass = nullptr;
     a->mass = nullptr;
     a->anchor = nullptr;
@@ -518,7 +527,7 @@ int mmshiftkv_decode_check(const mmskv_shape* shape, int32_t n_dec, const uint16
     a.rows_pad = decode_rows_pad(a.Gh, n_dec);
     a.n_kb = decode_key_blocks(shape->T);
     a.scale = query_scale(shape->d);
-    a.lane_sum_hi = lane_sum_limit(shape->T);
+    a.lane_sum_hi = lane_sum_limit(shape->T, 32);
     a.part = static_cast<float4*>(workspace);
     a.qsc = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + decode_part_bytes(shape, n_dec));
     a.coverage = coverage;

@@ -154,7 +154,7 @@ __global__ void __launch_bounds__(64 * kDecWaves) decode_cover_kernel(DecodeArgs
                 for (int s = 0; s < 2; ++s) acc[s] = mfma_32x32x16(kf[s][kc], q, acc[s]);
             }
             // sums of 2^s relative to 0 while every lane's sum is in
-            // [2^-60, lane_sum_limit(T)) (as in the row log-sum-exp pass),
+            // [2^-60, lane_sum_limit(T, 32)) (as in the row log-sum-exp pass),
             // else relative to the exact per-column maximum
             float mx = 0.f, la = 0.f, lk = 0.f;
 #pragma unroll

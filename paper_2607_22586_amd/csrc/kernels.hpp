@@ -7,8 +7,12 @@
 
 namespace mmskv {
 
-// Waves per score workgroup (each wave scores 64 keys) for a problem size.
-int score_block_waves(int B, int Hkv, int T);
+// Workgroup shapes of the two score passes for a problem size: pass 1 runs
+// lse_waves waves of 32 * lse_sub keys each, pass 2 mass_waves waves of 64.
+struct ScorePlan {
+    int lse_waves, lse_sub, mass_waves;
+};
+ScorePlan score_plan(int B, int Hkv, int T);
 
 struct ProxyArgs {
     const void* q;        // [B, Hq, W, d]
@@ -32,12 +36,15 @@ struct ScoreArgs {
     int k_dtype;
     int64_t ksb, ksh, kst;
     int B, Hq, Hkv, T, d, P, G, Gh;
-    int block_keys;            // keys per workgroup (64 * waves)
-    int n_kb;                  // key blocks of block_keys
+    int lse_waves, lse_sub;    // pass 1: waves per workgroup, 32-key sub-tiles per wave
+    int n_kb;                  // pass-1 key blocks (32 * lse_sub * lse_waves keys each)
+    int block_keys;            // pass 2: keys per workgroup (64 * waves)
+    int mass_n_kb;             // pass-2 key blocks
     int rows;                  // Gh * P proxy rows per KV head
     int rows_pad;              // rows + 32 * ceil(Gh / 32) (anchor rows, padded)
     double anchor_scale;       // log2(e) / sqrt(d), applied to the anchor rows
     float lane_sum_hi;         // pass 1 sums from zero while every lane sum is below this
+    const uint16_t* anchors;   // [B, Hkv, rows_pad - rows, d] scaled anchor rows (workspace)
     float2* part;              // [B, Hkv, n_kb, rows_pad]  (max, sum), base 2
     float* lse;                // [B, Hkv, rows_pad]        log2-domain
     float* group_mass;         // [B, Hkv, G, T] or null
@@ -129,12 +136,12 @@ struct ShapeArgs {
     int B, Hkv, T, kind, window, pool, sinks;
 };
 
-// Upper end of the lane sums (32 terms of 2^s each) that the score and
-// decode kernels add relative to zero.  A row's total over T keys is made of
-// at most ceil(T/32) such sums, so with every one below 2^(127 - ceil(log2
-// ceil(T/32))) the total stays below 2^127 and no partial or merged sum can
-// overflow fp32; capped at 2^120.
-float lane_sum_limit(int T);
+// Upper end of the lane sums (keys_per_sum terms of 2^s each) that the score
+// and decode kernels add relative to zero.  A row's total over T keys is
+// made of at most n = ceil(T / keys_per_sum) such sums, so with every one
+// below 2^(127 - ceil(log2 n)) the total stays below 2^127 and no partial or
+// merged sum can overflow fp32; capped at 2^120.
+float lane_sum_limit(int T, int keys_per_sum);
 
 int decode_rows_pad(int Gh, int n_dec);
 int decode_key_blocks(int T);

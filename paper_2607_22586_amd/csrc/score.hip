@@ -84,17 +84,12 @@ __device__ __forceinline__ bf16x8 lds_frag(const u32x4* stage, int row, int chun
     return __builtin_bit_cast(bf16x8, stage[row * TileLds<D>::kRow + chunk]);
 }
 
-// Global address of row `r` of the padded row space of head (b, c): rows
-// [0, Gh*P) are the proxies of the Gh query heads back to back, the rest the
-// anchor (last window) query of each head, zero-padded to a multiple of 32
-// (padding rows read head 0's anchor row and are masked out by the users).
+// The anchor rows of head (b, c) in the workspace: 32 * ceil(Gh / 32) rows of
+// D bf16 values, row h < Gh the scaled last window query of query head
+// c * Gh + h, the rest zero (written by anchor_rows_kernel before pass 1).
 template <int D>
-__device__ __forceinline__ const uint16_t* row_ptr(const ScoreArgs& a, int b, int c, int r) {
-    const int64_t hq0 = static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh;
-    if (r < a.rows) return a.proxies + (hq0 * a.P + r) * D;
-    int hl = r - a.rows;
-    if (hl >= a.Gh) hl = 0;
-    return a.q_last + (hq0 + hl) * D;
+__device__ __forceinline__ const uint16_t* anchor_block(const ScoreArgs& a, int head) {
+    return a.anchors + static_cast<int64_t>(head) * (a.rows_pad - a.rows) * D;
 }
 
 // Per-thread share of staging one tile: thread j moves 16-byte chunks
@@ -126,29 +121,6 @@ struct Stager {
         for (int k = 0; k < kPer; ++k)
             if (active(k)) v[k] = *reinterpret_cast<const u32x4*>(base + off[k]);
     }
-    // any tile of the padded row space; anchor rows (the raw last window
-    // queries) are scaled by log2(e)/sqrt(d) in fp64 and rounded back to
-    // bf16 (fp64 -> fp32 -> bf16), like the proxies
-    __device__ __forceinline__ void load_rows(const ScoreArgs& a, int b, int c, int row0) {
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            if (active(k)) {
-                const int q = chunk_of(k);
-                const int r = q / TileLds<D>::kChunks;
-                const int cs = q - r * TileLds<D>::kChunks;
-                v[k] = *reinterpret_cast<const u32x4*>(row_ptr<D>(a, b, c, row0 + r) + 8 * cs);
-                if (row0 + r >= a.rows) {
-#pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        const double lo = static_cast<double>(__uint_as_float(v[k][w] << 16)) * a.anchor_scale;
-                        const double hi = static_cast<double>(__uint_as_float(v[k][w] & 0xFFFF0000u)) * a.anchor_scale;
-                        v[k][w] = f32_to_bf16_bits(static_cast<float>(lo)) |
-                                  (f32_to_bf16_bits(static_cast<float>(hi)) << 16);
-                    }
-                }
-            }
-        }
-    }
     __device__ __forceinline__ void store(u32x4* stage) const {
 #pragma unroll
         for (int k = 0; k < kPer; ++k)
@@ -156,15 +128,15 @@ struct Stager {
     }
 };
 
-// Key fragments of the wave's 64 keys: kf[s][kc] holds key
+// Key fragments of the wave's 32*NS keys: kf[s][kc] holds key
 // key0 + 32*s + (lane % 32), dims [16*kc + 8*(lane/32), +8).
-template <int D>
+template <int D, int NS = kSub>
 __device__ __forceinline__ void load_keys(const ScoreArgs& a, int b, int c, int key0,
-                                          bf16x8 (&kf)[kSub][D / 16]) {
+                                          bf16x8 (&kf)[NS][D / 16]) {
     const int lane = lane_id();
     const int col = 8 * (lane >> 5);
 #pragma unroll
-    for (int s = 0; s < kSub; ++s) {
+    for (int s = 0; s < NS; ++s) {
         const int t = key0 + 32 * s + (lane & 31);
         const bool ok = t < a.T;
         const int64_t off = static_cast<int64_t>(b) * a.ksb + static_cast<int64_t>(c) * a.ksh +
@@ -235,35 +207,44 @@ struct Tag {
 // ---------------------------------------------------------------- pass 1
 constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batched
 
-// Pass 1 in the K * P^T layout: lane l holds proxy column l % 32 of a tile and
-// keys key0 + 32*s + 8*(i/4) + 4*(l/32) + i%4 of sub-tile s (value 16*s + i of
-// the lane).  The accumulators start at zero, so the MFMA leaves the base-2
-// logit s itself and every logit costs one exp and one add: per tile and
-// column the pair (0, l = sum 2^s over the wave's 64 keys) goes to LDS.  This
-// is exact while every lane's sum of its 32 terms lies in [2^-60, 2^120):
-// below 2^120 nothing overflows, and at 2^-60 or more the terms that underflow
-// (each below 2^-126) are negligible against the sum.  Otherwise (logits
-// beyond about +/-100) the whole wave takes the tile again relative to its
-// exact per-column maximum m, writing (m, sum 2^(s - m)).  The waves' pairs
-// are merged every kMergeTiles tiles into one partial per (row, key block)
-// by the max-and-rescale rule.  FULL: every key of the block is < T.
-template <int D, int WAVES, bool FULL>
+// Pass 1 in the K * P^T layout.  Each wave holds NS sub-tiles of 32 keys; for
+// every 32-row tile of the row space it runs one chain of D/16 dependent
+// MFMAs per sub-tile (keys as rows, the tile's proxy rows as columns), so
+// lane l holds column l % 32 (row 32t + l % 32) and keys key0 + 32*s +
+// 8*(i/4) + 4*(l/32) + i%4 of sub-tile s (value i).  The 16 values of a
+// chain are turned into 2^s and summed while the next chain's MFMAs run;
+// two accumulator sets alternate between the chains.  The accumulators start
+// at zero, so the MFMA leaves the base-2 logit itself and every logit costs
+// one exp and one add.  A chain's lane sum is kept relative to zero while it
+// lies in [2^-60, H) with H = lane_sum_hi, the bound under which no partial
+// of a row's total can overflow; at 2^-60 or more the terms that underflow
+// (each below 2^-126) are negligible against the sum.  Otherwise the whole
+// wave takes that chain again relative to each lane's exact maximum while its
+// values are still in registers, and the lane's (max, sum) pair is merged by
+// the max-and-rescale rule.  Per tile, the two half-waves' sums of each
+// column are combined and the waves' pairs are merged every kMergeTiles tiles
+// into one partial per (row, key block).  FULL: every key of the block is < T.
+template <int D, int WAVES, int NS, bool FULL>
 __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, int b, int c,
                                          u32x4 (&stage)[kRing][TileLds<D>::kSlots],
                                          float2 (&mrg)[2][kMergeTiles][WAVES][32]) {
     using St = Stager<D, WAVES>;
+    constexpr int KC = D / 16;                 // MFMAs per chain
+    constexpr int PER = 16 / KC;               // previous-chain values per MFMA slot
+    static_assert(NS % 2 == 0, "chains alternate between two accumulator sets");
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
-    const int key0 = kb * 64 * WAVES + wave * kWaveKeys;
+    const int key0 = kb * (32 * NS * WAVES) + wave * (32 * NS);
 
-    bf16x8 kf[kSub][D / 16];
-    load_keys<D>(a, b, c, key0, kf);
-    uint32_t valid = 0;
+    bf16x8 kf[NS][KC];
+    load_keys<D, NS>(a, b, c, key0, kf);
+    uint64_t valid = 0;                        // bit 16 s + i: value i of sub-tile s is a key < T
     if (!FULL) {
 #pragma unroll
-        for (int s = 0; s < kSub; ++s)
+        for (int s2 = 0; s2 < NS; ++s2)
 #pragma unroll
             for (int i = 0; i < 16; ++i)
-                valid |= (key0 + 32 * s + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3) < a.T) ? (1u << (16 * s + i)) : 0u;
+                if (key0 + 32 * s2 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3) < a.T)
+                    valid |= 1ull << (16 * s2 + i);
     }
 
     const int n_tiles = a.rows_pad / 32;
@@ -275,9 +256,10 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     for (int k = 0; k < St::kPer; ++k) off[k] = St::src_off(k);
     St st;
     // tile t = rows [32t, 32t+32) of the padded row space
+    const uint16_t* abase = anchor_block<D>(a, head);
     auto load_tile = [&](int t) {
         if (t < n_prox) st.load_block(pbase + static_cast<int64_t>(32 * t) * D, off);
-        else st.load_rows(a, b, c, 32 * t);
+        else st.load_block(abase + static_cast<int64_t>(32 * (t - n_prox)) * D, off);
     };
 
     float2* part = a.part + (static_cast<int64_t>(head) * a.n_kb + kb) * a.rows_pad;
@@ -299,12 +281,7 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         }
     };
 
-    // Pipeline over the tiles t (LDS slot t % 4), as in pass 2: iteration t
-    // issues the MFMAs of tile t while refilling the fragments with tile t+1
-    // and forming the column statistics of tile t-1, then stages tile t+3
-    // (registers -> LDS) and fetches tile t+4; one barrier after every even
-    // iteration.  The chunk of tiles [16k, 16k+16) is merged in iteration
-    // 16k+17, after the barrier that follows its last statistics.
+    // Prologue: tiles 0-2 to LDS slots 0-2, tile 3 in the staging registers.
     for (int k = 0; k < 3; ++k) {
         if (k < n_tiles) {
             load_tile(k);
@@ -313,42 +290,119 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     }
     if (3 < n_tiles) load_tile(3);
     __syncthreads();
-    bf16x8 A[D / 16];
-    read_frags<D>(stage[0], A, lane);
+    bf16x8 A[KC];
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) A[kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
 
-    constexpr int kMfmas = kSub * (D / 16);
-    constexpr int kPer = 32 / kMfmas;                       // values per MFMA slot
-    floatx16 acc[2][kSub];
-    auto value = [&](const floatx16 (&ac)[kSub], int idx) { return ac[idx >> 4][idx & 15]; };
-    auto ok = [&](int idx) { return FULL || ((valid >> idx) & 1u); };
-    // One pipeline iteration; STATS: tile t-1 exists.  FAST: tile t exists,
-    // tile t+3 is staged and tile t+4 is a proxy tile.
-    auto iter = [&](auto t4, auto stats, auto fast, int t) {
+    floatx16 acc[2];
+    auto ok = [&](int s2, int i) { return FULL || ((valid >> (16 * s2 + i)) & 1ull); };
+    // per-lane pair of the tile being summed: fast part relative to zero,
+    // exact part (max, sum) from chains that left the fast range
+    float sf = 0.f, me = -INFINITY, se = 0.f;
+    bool exact_tile = false;                   // wave-uniform
+
+    // finish chain (values in acc[SETP], sub-tile SP) after its exps: range
+    // check and, if needed, the exact form
+    auto finish_chain = [&](auto setp, auto sp, float lsum) {
+        constexpr int SETP = decltype(setp)::value, SP = decltype(sp)::value;
+        uint32_t cv = 0;
+        if (!FULL) cv = static_cast<uint32_t>(valid >> (16 * SP)) & 0xFFFFu;
+        const bool in_range = (lsum >= 0x1p-60f || (!FULL && cv == 0u)) && lsum < a.lane_sum_hi;
+        if (__ballot(!in_range) == 0) {
+            sf += lsum;
+        } else {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, ok(SP, i) ? acc[SETP][i] : -INFINITY);
+            if (mx != -INFINITY) {
+                float ls = 0.f;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) ls += ok(SP, i) ? fast_exp2(acc[SETP][i] - mx) : 0.f;
+                const float mm = fmaxf(me, mx);
+                se = (me == -INFINITY ? 0.f : se * fast_exp2(me - mm)) + ls * fast_exp2(mx - mm);
+                me = mm;
+            }
+            exact_tile = true;
+        }
+    };
+    // column (max, sum) of tile tp from both half-waves, to LDS
+    auto finish_tile = [&](int tp, bool merge_now) {
+        float mrow = 0.f, l;
+        if (!exact_tile) {
+            l = pair_total(sf);
+        } else {
+            // lane pair: fast part (max 0) and exact part
+            float M = sf > 0.f ? fmaxf(0.f, me) : me;
+            float S = 0.f;
+            if (M != -INFINITY) S = (sf > 0.f ? sf * fast_exp2(-M) : 0.f) + (me == -INFINITY ? 0.f : se * fast_exp2(me - M));
+            const auto rm = __builtin_amdgcn_permlane32_swap(__float_as_uint(M), __float_as_uint(M), false, false);
+            const auto rs = __builtin_amdgcn_permlane32_swap(__float_as_uint(S), __float_as_uint(S), false, false);
+            const float m0 = __uint_as_float(rm[0]), m1 = __uint_as_float(rm[1]);
+            const float s0 = __uint_as_float(rs[0]), s1 = __uint_as_float(rs[1]);
+            mrow = fmaxf(m0, m1);
+            l = 0.f;
+            if (mrow != -INFINITY)
+                l = (m0 == -INFINITY ? 0.f : s0 * fast_exp2(m0 - mrow)) + (m1 == -INFINITY ? 0.f : s1 * fast_exp2(m1 - mrow));
+        }
+        // an empty sum (no valid key) carries no maximum, so it cannot
+        // outweigh the pairs it is merged with
+        if (!(l > 0.f)) mrow = -INFINITY;
+        if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(mrow, l);
+        if (merge_now) merge_chunk((tp - kMergeTiles) / kMergeTiles);
+        sf = 0.f;
+        me = -INFINITY;
+        se = 0.f;
+        exact_tile = false;
+    };
+
+    // One pipeline iteration over tile t (LDS slot t % 4): chain s of tile t
+    // runs its MFMAs while the exps of the chain before it (the last chain of
+    // tile t-1 for s = 0) are formed; the last chain refills the fragments
+    // with tile t+1; then tile t+3 is staged (registers -> LDS) and tile t+4
+    // fetched; one barrier after every even iteration.  PREV: tile t-1
+    // exists.  MF: tile t exists.  FAST: tile t+3 is staged and tile t+4 is
+    // a proxy tile.
+    auto iter = [&](auto t4, auto prev, auto mf, auto fast, int t) {
         constexpr int T4 = decltype(t4)::value;
-        constexpr bool STATS = decltype(stats)::value != 0, FAST = decltype(fast)::value != 0;
-        constexpr int cur = T4 & 1, prev = cur ^ 1;
+        constexpr bool PREV = decltype(prev)::value != 0, MF = decltype(mf)::value != 0,
+                       FAST = decltype(fast)::value != 0;
         const u32x4* next = stage[(T4 + 1) % kRing];
-        const bool mfma_on = FAST || t < n_tiles;
-        float l0 = 0.f, l1 = 0.f;
+        auto chain = [&](auto si) {
+            constexpr int S = decltype(si)::value;
+            constexpr int CUR = S & 1, PRV = CUR ^ 1, SP = (S + NS - 1) % NS;
+            constexpr bool HAVE_PREV = S > 0 ? MF : PREV;
+            float l0 = 0.f, l1 = 0.f;
 #pragma unroll
-        for (int kc = 0; kc < D / 16; ++kc) {
+            for (int kc = 0; kc < KC; ++kc) {
+                if (MF) acc[CUR] = mfma32(kf[S][kc], A[kc], kc == 0 ? zero16() : acc[CUR]);
+                if (HAVE_PREV) {
 #pragma unroll
-            for (int s = 0; s < kSub; ++s) {
-                const int slot = kSub * kc + s;
-                if (mfma_on) acc[cur][s] = mfma32(kf[s][kc], A[kc], kc == 0 ? zero16() : acc[cur][s]);
-                if (STATS) {
-#pragma unroll
-                    for (int q = 0; q < kPer; ++q) {
-                        const int idx = slot * kPer + q;
-                        const float e = fast_exp2(value(acc[prev], idx));
-                        const float ev = ok(idx) ? e : 0.f;
+                    for (int q = 0; q < PER; ++q) {
+                        const int i = kc * PER + q;
+                        const float e = fast_exp2(acc[PRV][i]);
+                        const float ev = ok(SP, i) ? e : 0.f;
                         if (q & 1) l1 += ev; else l0 += ev;
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
+                if (MF && S == NS - 1) A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
+                __builtin_amdgcn_sched_barrier(0);
             }
-            if (mfma_on) A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
-            __builtin_amdgcn_sched_barrier(0);
+            if (HAVE_PREV) {
+                finish_chain(Tag<PRV>{}, Tag<SP>{}, l0 + l1);
+                if (S == 0) {
+                    const int tp = t - 1;
+                    finish_tile(tp, T4 == 1 && tp >= kMergeTiles && (tp - kMergeTiles) % kMergeTiles == 0);
+                }
+            }
+        };
+        chain(Tag<0>{});
+        if constexpr (MF) {
+            chain(Tag<1>{});
+            if constexpr (NS > 2) {
+                chain(Tag<2>{});
+                chain(Tag<3>{});
+            }
         }
         if (FAST) {
             st.store(stage[(T4 + 3) % kRing]);
@@ -357,51 +411,31 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
             st.store(stage[(T4 + 3) % kRing]);
             if (t + 4 < n_tiles) load_tile(t + 4);
         }
-        if (STATS) {
-            const int tp = t - 1;
-            float lsum = l0 + l1;
-            float mrow = 0.f;
-            const bool in_range = (lsum >= 0x1p-60f || (!FULL && valid == 0u)) && lsum < a.lane_sum_hi;
-            if (__ballot(!in_range) != 0) {
-                // logits out of the range: this tile again with its own maximum
-                float mx = -INFINITY;
-#pragma unroll
-                for (int idx = 0; idx < 32; ++idx) mx = fmaxf(mx, ok(idx) ? value(acc[prev], idx) : -INFINITY);
-                mx = pair_max(mx);
-                float ls = 0.f;
-                if (mx != -INFINITY) {
-#pragma unroll
-                    for (int idx = 0; idx < 32; ++idx) ls += ok(idx) ? fast_exp2(value(acc[prev], idx) - mx) : 0.f;
-                    mrow = mx;
-                }
-                lsum = ls;
-            }
-            const float l = pair_total(lsum);
-            // an empty sum (no valid key) carries no maximum, so it cannot
-            // outweigh the pairs it is merged with
-            if (!(l > 0.f)) mrow = -INFINITY;
-            if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(mrow, l);
-            if (T4 == 1 && tp >= kMergeTiles && (tp - kMergeTiles) % kMergeTiles == 0)
-                merge_chunk((tp - kMergeTiles) / kMergeTiles);
-        }
         if ((T4 & 1) == 0) __syncthreads();
     };
     using Off = Tag<0>;
     using On = Tag<1>;
-    iter(Tag<0>{}, Off{}, Off{}, 0);
+    iter(Tag<0>{}, Off{}, On{}, Off{}, 0);
     int t = 1;
     __builtin_amdgcn_s_waitcnt(0);
     for (; t + 3 + 4 < n_prox; t += 4) {
-        iter(Tag<1>{}, On{}, On{}, t);
-        iter(Tag<2>{}, On{}, On{}, t + 1);
-        iter(Tag<3>{}, On{}, On{}, t + 2);
-        iter(Tag<0>{}, On{}, On{}, t + 3);
+        iter(Tag<1>{}, On{}, On{}, On{}, t);
+        iter(Tag<2>{}, On{}, On{}, On{}, t + 1);
+        iter(Tag<3>{}, On{}, On{}, On{}, t + 2);
+        iter(Tag<0>{}, On{}, On{}, On{}, t + 3);
     }
-    for (; t <= n_tiles; t += 4) {
-        iter(Tag<1>{}, On{}, Off{}, t);
-        if (t + 1 <= n_tiles) iter(Tag<2>{}, On{}, Off{}, t + 1);
-        if (t + 2 <= n_tiles) iter(Tag<3>{}, On{}, Off{}, t + 2);
-        if (t + 3 <= n_tiles) iter(Tag<0>{}, On{}, Off{}, t + 3);
+    for (; t < n_tiles; t += 4) {
+        iter(Tag<1>{}, On{}, On{}, Off{}, t);
+        if (t + 1 < n_tiles) iter(Tag<2>{}, On{}, On{}, Off{}, t + 1);
+        if (t + 2 < n_tiles) iter(Tag<3>{}, On{}, On{}, Off{}, t + 2);
+        if (t + 3 < n_tiles) iter(Tag<0>{}, On{}, On{}, Off{}, t + 3);
+    }
+    // drain: the exps of the last tile's last chain (t == n_tiles here)
+    switch (n_tiles & 3) {
+        case 0: iter(Tag<0>{}, On{}, Off{}, Off{}, n_tiles); break;
+        case 1: iter(Tag<1>{}, On{}, Off{}, Off{}, n_tiles); break;
+        case 2: iter(Tag<2>{}, On{}, Off{}, Off{}, n_tiles); break;
+        default: iter(Tag<3>{}, On{}, Off{}, Off{}, n_tiles); break;
     }
     __syncthreads();
     // chunk k was merged in iteration 16k+17 when that iteration ran (t <= n_tiles)
@@ -409,17 +443,39 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     for (int k = merged; k * kMergeTiles < n_tiles; ++k) merge_chunk(k);
 }
 
-template <int D, int WAVES>
+template <int D, int WAVES, int NS>
 __global__ void __launch_bounds__(64 * WAVES) score_lse_kernel(ScoreArgs a) {
     __shared__ u32x4 stage[kRing][TileLds<D>::kSlots];
     __shared__ float2 mrg[2][kMergeTiles][WAVES][32];
     int head, kb;
     block_work(a.n_kb, head, kb);
     const int b = head / a.Hkv, c = head - b * a.Hkv;
-    if ((kb + 1) * 64 * WAVES <= a.T)
-        lse_body<D, WAVES, true>(a, head, kb, b, c, stage, mrg);
+    if ((kb + 1) * (32 * NS * WAVES) <= a.T)
+        lse_body<D, WAVES, NS, true>(a, head, kb, b, c, stage, mrg);
     else
-        lse_body<D, WAVES, false>(a, head, kb, b, c, stage, mrg);
+        lse_body<D, WAVES, NS, false>(a, head, kb, b, c, stage, mrg);
+}
+
+// The anchor rows of every head (b, c): row h < Gh is query head c*Gh + h's
+// last window query (a bf16 value) times log2(e)/sqrt(d) in fp64, rounded
+// fp64 -> fp32 -> bf16 like the proxies; the padding rows are zero.  One
+// thread per pair of elements.
+__global__ void __launch_bounds__(256) anchor_rows_kernel(ScoreArgs a) {
+    const int head = static_cast<int>(blockIdx.y);
+    const int b = head / a.Hkv, c = head - b * a.Hkv;
+    const int n_rows = a.rows_pad - a.rows;
+    const int i = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x);   // element pair
+    if (i >= n_rows * a.d / 2) return;
+    const int r = (2 * i) / a.d, j = 2 * i - r * a.d;
+    uint32_t out = 0u;
+    if (r < a.Gh) {
+        const int64_t hq = static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh + r;
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(a.q_last + hq * a.d + j);
+        const double lo = static_cast<double>(__uint_as_float(v << 16)) * a.anchor_scale;
+        const double hi = static_cast<double>(__uint_as_float(v & 0xFFFF0000u)) * a.anchor_scale;
+        out = f32_to_bf16_bits(static_cast<float>(lo)) | (f32_to_bf16_bits(static_cast<float>(hi)) << 16);
+    }
+    reinterpret_cast<uint32_t*>(const_cast<uint16_t*>(a.anchors) + static_cast<int64_t>(head) * n_rows * a.d)[i] = out;
 }
 
 // L_row = M + log2(sum_kb S_kb * 2^(M_kb - M)), one thread per row; the
@@ -474,7 +530,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     float* Llds = reinterpret_cast<float*>(dyn_lds);     // [rows_pad]
 
     int head, kb;
-    block_work(a.n_kb, head, kb);
+    block_work(a.mass_n_kb, head, kb);
     const int b = head / a.Hkv, c = head - b * a.Hkv;
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
     const int key0 = kb * 64 * WAVES + wave * kWaveKeys;
@@ -688,7 +744,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     float aacc[kSub] = {0.f, 0.f};
     for (int ta = 0; ta < n_anc; ++ta) {
         __syncthreads();
-        st[0].load_rows(a, b, c, a.rows + 32 * ta);
+        st[0].load_block(anchor_block<D>(a, head) + static_cast<int64_t>(32 * ta) * D, off);
         st[0].store(stage[0]);
         __syncthreads();
         read_frags<D>(stage[0], A, lane);
@@ -717,10 +773,14 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     }
 }
 
-template <int D, int WAVES>
+template <int D, int WAVES, int NS>
 hipError_t lse_impl(const ScoreArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((score_lse_kernel<D, WAVES>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES), 0, s, a);
+    const int pairs = (a.rows_pad - a.rows) * a.d / 2;
+    hipLaunchKernelGGL(anchor_rows_kernel, dim3((pairs + 255) / 256, a.B * a.Hkv), dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((score_lse_kernel<D, WAVES, NS>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES), 0, s, a);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g2((a.rows_pad + 255) / 256, a.B * a.Hkv);
     hipLaunchKernelGGL(lse_combine_kernel, g2, dim3(256), 0, s, a);
@@ -729,32 +789,50 @@ hipError_t lse_impl(const ScoreArgs& a, hipStream_t s) {
 
 template <int D, int WAVES>
 hipError_t mass_impl(const ScoreArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((score_mass_kernel<D, WAVES>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES),
+    hipLaunchKernelGGL((score_mass_kernel<D, WAVES>), dim3(a.B * a.Hkv * a.mass_n_kb), dim3(64 * WAVES),
                        static_cast<size_t>(a.rows_pad) * sizeof(float), s, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
-float lane_sum_limit(int T) {
-    const long n = (static_cast<long>(T) + 31) / 32;   // lane sums per row
+float lane_sum_limit(int T, int keys_per_sum) {
+    const long n = (static_cast<long>(T) + keys_per_sum - 1) / keys_per_sum;   // lane sums per row
     int bits = 0;
     while ((1L << bits) < n) ++bits;                   // ceil(log2 n)
     const int e = 127 - bits < 120 ? 127 - bits : 120;
     return ldexpf(1.0f, e);
 }
 
-int score_block_waves(int B, int Hkv, int T) {
-    // 8-wave blocks (512 keys) when that still gives every CU two blocks of
-    // work, else 4-wave blocks (256 keys)
-    const long blocks8 = static_cast<long>(B) * Hkv * ((T + 511) / 512);
-    return blocks8 >= 512 ? 8 : 4;
+ScorePlan score_plan(int B, int Hkv, int T) {
+    // the largest key blocks that still give every CU one block of work:
+    // pass 1 with 8 waves of 128 keys, else 8 waves of 64, else 4 waves of
+    // 64; pass 2 with 8-wave blocks (512 keys) when that gives every CU two
+    // blocks, else 4-wave blocks (256 keys)
+    const long heads = static_cast<long>(B) * Hkv;
+    ScorePlan p;
+    if (heads * ((T + 1023) / 1024) >= 256) {
+        p.lse_waves = 8;
+        p.lse_sub = 4;
+    } else if (heads * ((T + 511) / 512) >= 256) {
+        p.lse_waves = 8;
+        p.lse_sub = 2;
+    } else {
+        p.lse_waves = 4;
+        p.lse_sub = 2;
+    }
+    p.mass_waves = heads * ((T + 511) / 512) >= 512 ? 8 : 4;
+    return p;
 }
 
 hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s) {
-    const int w = a.block_keys / 64;
-    if (a.d == 64) return w == 8 ? lse_impl<64, 8>(a, s) : lse_impl<64, 4>(a, s);
-    return w == 8 ? lse_impl<128, 8>(a, s) : lse_impl<128, 4>(a, s);
+    const int w = a.lse_waves, ns = a.lse_sub;
+    if (a.d == 64) {
+        if (w == 8) return ns == 4 ? lse_impl<64, 8, 4>(a, s) : lse_impl<64, 8, 2>(a, s);
+        return lse_impl<64, 4, 2>(a, s);
+    }
+    if (w == 8) return ns == 4 ? lse_impl<128, 8, 4>(a, s) : lse_impl<128, 8, 2>(a, s);
+    return lse_impl<128, 4, 2>(a, s);
 }
 
 hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s) {
