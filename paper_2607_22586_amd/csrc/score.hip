@@ -215,7 +215,9 @@ constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batc
 // chain are turned into 2^s and summed while the next chain's MFMAs run;
 // two accumulator sets alternate between the chains.  The accumulators start
 // at zero, so the MFMA leaves the base-2 logit itself and every logit costs
-// one exp and one add.  A chain's lane sum is kept relative to zero while it
+// one exp and one add (in a block with keys past T, a chain's accumulator
+// starts at -inf on their rows instead).  A chain's lane sum is kept
+// relative to zero while it
 // lies in [2^-60, H) with H = lane_sum_hi, the bound under which no partial
 // of a row's total can overflow; at 2^-60 or more the terms that underflow
 // (each below 2^-126) are negligible against the sum.  Otherwise the whole
@@ -230,22 +232,16 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
                                          float2 (&mrg)[2][kMergeTiles][WAVES][32]) {
     using St = Stager<D, WAVES>;
     constexpr int KC = D / 16;                 // MFMAs per chain
-    constexpr int PER = 16 / KC;               // previous-chain values per MFMA slot
     static_assert(NS % 2 == 0, "chains alternate between two accumulator sets");
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
     const int key0 = kb * (32 * NS * WAVES) + wave * (32 * NS);
 
     bf16x8 kf[NS][KC];
     load_keys<D, NS>(a, b, c, key0, kf);
-    uint64_t valid = 0;                        // bit 16 s + i: value i of sub-tile s is a key < T
-    if (!FULL) {
-#pragma unroll
-        for (int s2 = 0; s2 < NS; ++s2)
-#pragma unroll
-            for (int i = 0; i < 16; ++i)
-                if (key0 + 32 * s2 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3) < a.T)
-                    valid |= 1ull << (16 * s2 + i);
-    }
+    // keys of sub-tile s held by this lane that are < T: value i is key
+    // key0 + 32 s + 8 (i / 4) + 4 (lane / 32) + i % 4, valid while
+    // 8 (i / 4) + i % 4 < n_keys(s)
+    auto n_keys = [&](int s2) { return a.T - key0 - 32 * s2 - 4 * (lane >> 5); };
 
     const int n_tiles = a.rows_pad / 32;
     const int n_prox = a.rows / 32;
@@ -290,12 +286,13 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     }
     if (3 < n_tiles) load_tile(3);
     __syncthreads();
-    bf16x8 A[KC];
+    // fragments of tile t in set t % 2; the other set is refilled with tile
+    // t+1 while tile t's chains run, one 16-byte read per NS/2 MFMAs
+    bf16x8 A[2][KC];
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc) A[kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
+    for (int kc = 0; kc < KC; ++kc) A[0][kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
 
     floatx16 acc[2];
-    auto ok = [&](int s2, int i) { return FULL || ((valid >> (16 * s2 + i)) & 1ull); };
     // per-lane pair of the tile being summed: fast part relative to zero,
     // exact part (max, sum) from chains that left the fast range
     float sf = 0.f, me = -INFINITY, se = 0.f;
@@ -305,19 +302,19 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     // check and, if needed, the exact form
     auto finish_chain = [&](auto setp, auto sp, float lsum) {
         constexpr int SETP = decltype(setp)::value, SP = decltype(sp)::value;
-        uint32_t cv = 0;
-        if (!FULL) cv = static_cast<uint32_t>(valid >> (16 * SP)) & 0xFFFFu;
-        const bool in_range = (lsum >= 0x1p-60f || (!FULL && cv == 0u)) && lsum < a.lane_sum_hi;
+        // a lane whose keys are all past T has nothing to sum
+        const bool in_range = (lsum >= 0x1p-60f || (!FULL && n_keys(SP) <= 0)) && lsum < a.lane_sum_hi;
         if (__ballot(!in_range) == 0) {
             sf += lsum;
         } else {
+            // (keys past T hold -inf and drop out of both)
             float mx = -INFINITY;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, ok(SP, i) ? acc[SETP][i] : -INFINITY);
+            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[SETP][i]);
             if (mx != -INFINITY) {
                 float ls = 0.f;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) ls += ok(SP, i) ? fast_exp2(acc[SETP][i] - mx) : 0.f;
+                for (int i = 0; i < 16; ++i) ls += fast_exp2(acc[SETP][i] - mx);
                 const float mm = fmaxf(me, mx);
                 se = (me == -INFINITY ? 0.f : se * fast_exp2(me - mm)) + ls * fast_exp2(mx - mm);
                 me = mm;
@@ -371,21 +368,38 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
             constexpr int S = decltype(si)::value;
             constexpr int CUR = S & 1, PRV = CUR ^ 1, SP = (S + NS - 1) % NS;
             constexpr bool HAVE_PREV = S > 0 ? MF : PREV;
+            constexpr int AS = T4 & 1, AN = AS ^ 1;    // fragment sets of tiles t and t+1
             float l0 = 0.f, l1 = 0.f;
+            if (!FULL && MF) {
+                // keys past T start at -inf, so their 2^s is 0 (the mask is
+                // opaque here so that the start values are not kept live
+                // across the loop)
+                int nk = n_keys(S);
+                asm volatile("" : "+v"(nk));
+#pragma unroll
+                for (int i = 0; i < 16; ++i) acc[CUR][i] = (8 * (i >> 2) + (i & 3) < nk) ? 0.f : -INFINITY;
+            }
 #pragma unroll
             for (int kc = 0; kc < KC; ++kc) {
-                if (MF) acc[CUR] = mfma32(kf[S][kc], A[kc], kc == 0 ? zero16() : acc[CUR]);
-                if (HAVE_PREV) {
+                if (MF) acc[CUR] = mfma32(kf[S][kc], A[AS][kc], kc == 0 ? (FULL ? zero16() : acc[CUR]) : acc[CUR]);
+                __builtin_amdgcn_sched_barrier(0);
+                // the previous chain's values go to slots 1 .. KC-1, so none of
+                // them is read before its last MFMA has had a slot to finish
+                if (HAVE_PREV && kc > 0) {
+                    constexpr int kSlots = KC - 1;
 #pragma unroll
-                    for (int q = 0; q < PER; ++q) {
-                        const int i = kc * PER + q;
+                    for (int i = 16 * (kc - 1) / kSlots; i < 16 * kc / kSlots; ++i) {
                         const float e = fast_exp2(acc[PRV][i]);
-                        const float ev = ok(SP, i) ? e : 0.f;
-                        if (q & 1) l1 += ev; else l0 += ev;
+                        if (i & 1) l1 += e; else l0 += e;
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                if (MF && S == NS - 1) A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
+                // MFMA slot j = S * KC + kc of the tile refills fragment j / NS
+                // of tile t+1 after every NS-th slot
+                if (MF && ((S * KC + kc) % NS) == NS - 1) {
+                    const int f = (S * KC + kc) / NS;
+                    A[AN][f] = lds_frag<D>(next, lane & 31, 2 * f + (lane >> 5));
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
             if (HAVE_PREV) {
