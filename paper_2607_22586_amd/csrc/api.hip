@@ -109,7 +109,7 @@ ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
 }
 
 struct SelectLayout {
-    size_t theta_off, tcut_off, keys_off, total;
+    size_t theta_off, tcut_off, keys_off, planes_off, hist_off, total;
 };
 
 SelectLayout select_layout(const mmskv_shape* s, const mmskv_params* p) {
@@ -118,7 +118,10 @@ SelectLayout select_layout(const mmskv_shape* s, const mmskv_params* p) {
     l.theta_off = 0;
     l.tcut_off = align_up(heads * p->G * sizeof(uint32_t));
     l.keys_off = l.tcut_off + align_up(heads * p->G * sizeof(int32_t));
-    l.total = l.keys_off + align_up(heads * s->T * sizeof(uint64_t));
+    l.planes_off = l.keys_off + align_up(heads * static_cast<size_t>(select_key_stride(s->T)) * sizeof(uint64_t));
+    const size_t words = (static_cast<size_t>(s->T) + 31) / 32;
+    l.hist_off = l.planes_off + align_up(heads * words * p->G * sizeof(uint32_t));
+    l.total = l.hist_off + align_up(heads * 2048 * sizeof(uint32_t));
     return l;
 }
 
@@ -406,6 +409,10 @@ int mmshiftkv_select_topk(const mmskv_shape* shape, const mmskv_params* params, 
     a.theta = reinterpret_cast<uint32_t*>(w + l.theta_off);
     a.tcut = reinterpret_cast<int32_t*>(w + l.tcut_off);
     a.keys = reinterpret_cast<uint64_t*>(w + l.keys_off);
+    a.planes = reinterpret_cast<uint32_t*>(w + l.planes_off);
+    a.hist0 = reinterpret_cast<uint32_t*>(w + l.hist_off);
+    a.kpt = select_kpt(shape->T);
+    a.key_stride = select_key_stride(shape->T);
     a.idx = idx;
     a.counts = counts;
     a.votes = votes;

@@ -44,21 +44,45 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
-__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
-    uint32_t lo = __shfl(static_cast<uint32_t>(v), src, kWave);
-    uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src, kWave);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
+// Lane moves through DPP (no LDS round trip): x of the source lane for the
+// lanes of the rows in ROWS, 0 for the other lanes and for lanes whose
+// source falls outside their 16-lane row.  Controls: row_shr:n = 0x110 + n,
+// row_bcast:15 = 0x142 (lane 15 of each row to the next row), row_bcast:31
+// = 0x143 (lane 31 to rows 2 and 3).
+template <int CTRL, int ROWS, typename U>
+__device__ __forceinline__ U dpp_take(U x) {
+    static_assert(sizeof(U) == 4 || sizeof(U) == 8, "32- or 64-bit lanes");
+    auto move = [](uint32_t v) {
+        return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, ROWS, 0xF, true));
+    };
+    if constexpr (sizeof(U) == 4) {
+        return static_cast<U>(move(static_cast<uint32_t>(x)));
+    } else {
+        const uint64_t v = static_cast<uint64_t>(x);
+        const uint64_t lo = move(static_cast<uint32_t>(v)), hi = move(static_cast<uint32_t>(v >> 32));
+        return static_cast<U>((hi << 32) | lo);
+    }
 }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-    uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), m, kWave);
-    uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), m, kWave);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
+// Inclusive prefix sum over the 64 lanes (lane order): shifts of 1, 2, 4
+// and 8 within each row, then each row adds the totals of the rows below.
+template <typename U>
+__device__ __forceinline__ U wave_incl_scan(U x) {
+    x += dpp_take<0x111, 0xF>(x);
+    x += dpp_take<0x112, 0xF>(x);
+    x += dpp_take<0x114, 0xF>(x);
+    x += dpp_take<0x118, 0xF>(x);
+    x += dpp_take<0x142, 0xA>(x);
+    x += dpp_take<0x143, 0xC>(x);
+    return x;
 }
 
+// Sum over the 64 lanes, the same in every lane.
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-    for (int m = 1; m < kWave; m <<= 1) v += shfl_xor_u64(v, m);
-    return v;
+    const uint64_t x = wave_incl_scan(v);
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), 63));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x >> 32)), 63));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
 }  // namespace mmskv

@@ -63,6 +63,10 @@ struct SelectArgs {
     uint32_t* theta;           // [B, Hkv, G] cut mass (fp32 bits)
     int32_t* tcut;             // [B, Hkv, G] last admitted index among equals
     uint64_t* keys;            // [B, Hkv, T] score bits (fp64, non-negative)
+    uint32_t* planes;          // [B, Hkv, G, ceil(T/32)] tau-set membership, bit j of word (g, w): key 32w+j in S_g
+    uint32_t* hist0;           // [B, Hkv, 2048] pool keys per top digit (bits 63..53) of the score key
+    int kpt;                   // keys per top-k thread (register path), 0 for the sweep path
+    int key_stride;            // per-head stride of `keys`: kpt * 1024 (key t at (t % kpt) * 1024 + t / kpt), else T
     int32_t* idx;              // [B, Hkv, c_max]
     int32_t* counts;           // [B, Hkv]
     uint8_t* votes;            // [B, Hkv, T] or null
@@ -152,6 +156,13 @@ hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s);
 hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s);
 hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+// Keys per thread of the register-resident top-k for T keys (0: the sweep
+// kernel), and the per-head stride of the score keys it implies.
+int select_kpt(int T);
+inline int select_key_stride(int T) {
+    const int k = select_kpt(T);
+    return k > 0 ? k * 1024 : T;
+}
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 hipError_t launch_hidden_stats(const HiddenArgs& a, hipStream_t s);
 hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s);

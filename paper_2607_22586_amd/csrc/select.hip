@@ -7,13 +7,16 @@
 //           finds the cut mass theta and, among keys whose mass equals theta,
 //           the last admitted index, such that
 //           {mass > theta} u {mass == theta, index <= tcut} is the shortest
-//           (mass desc, index asc) prefix whose mass reaches tau * total;
-//           the passes stop early once the crossing bucket holds one key.
+//           (mass desc, index asc) prefix whose mass reaches tau * total.
 //           Masses are summed as integers in units of 2^-S (converted from
 //           the float bits exactly), so every decision is independent of
-//           summation order.
-// vote      one thread per 4 keys: vote = #groups whose set holds the key;
-//           score = vote + lambda*anchor (fp64) or the total mass.
+//           summation order.  The register-resident variant (T <= 16384)
+//           stops its passes early once the crossing bucket holds one key;
+//           the sweep variant always runs all three.  Both end by writing
+//           the group's membership plane: one bit per key, 32 keys a word.
+// vote      one wave per two membership words at a time: vote = #groups
+//           whose set holds the key, counted with one ballot per bit position;
+//           score = vote + lambda*anchor (fp64), or the total mass.
 // topk      one workgroup per (b, c): radix select (11-bit digits, stopping
 //           early once a bucket is taken whole) of the (C-1)-th largest score
 //           key over [0, T-1) (or the C-th over [0, T)), then an
@@ -61,7 +64,7 @@ __device__ __forceinline__ void hist_add(bool active, uint32_t digit, uint64_t f
             break;
         }
         const int leader = __ffsll(static_cast<unsigned long long>(pending)) - 1;
-        const uint32_t d0 = __shfl(digit, leader, kWave);
+        const uint32_t d0 = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(digit), leader));
         const bool mine = active && digit == d0;
         const uint64_t m = __ballot(mine);
         if (sum) {
@@ -101,16 +104,7 @@ template <typename U, int NT = kSelThreads>
 __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
     constexpr int kW = NT / kWave;
     const int lane = lane_id(), wave = static_cast<int>(threadIdx.x) / kWave;
-    U x = v;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        U y;
-        if constexpr (sizeof(U) == 8)
-            y = shfl_u64(x, lane >= o ? lane - o : lane);
-        else
-            y = __shfl(x, lane >= o ? lane - o : lane, kWave);
-        if (lane >= o) x += y;
-    }
+    const U x = wave_incl_scan(v);
     if (lane == kWave - 1) wtot[wave] = x;
     __syncthreads();
     U before = 0, tot = 0;
@@ -129,7 +123,7 @@ __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
 // 2048/NT digits below 2048 - (2048/NT)*i: finds the digit whose bucket
 // takes the running total (from the top) to `need` (need >= 1, need <=
 // total).  Returns, through shared memory, the digit, `need` minus the total
-// of higher buckets, and the bucket's count.
+// of higher buckets, and the bucket's count (when `cnt` is given).
 template <typename U, int NT = kSelThreads>
 __device__ __forceinline__ void descending_crossing(const U* val, const uint32_t* cnt, U need, U* wtot,
                                                     uint32_t* s_digit, U* s_rem, uint32_t* s_cnt) {
@@ -150,7 +144,7 @@ __device__ __forceinline__ void descending_crossing(const U* val, const uint32_t
             if (excl < need && need <= excl + v[k]) {
                 *s_digit = top - k;
                 *s_rem = need - excl;
-                *s_cnt = cnt[top - k];
+                if (cnt != nullptr) *s_cnt = cnt[top - k];
             }
             excl += v[k];
         }
@@ -177,6 +171,36 @@ __device__ __forceinline__ uint32_t tau_mask(int pass) { return pass == 0 ? 0u :
 __device__ __forceinline__ uint32_t tau_digit(uint32_t bits, int pass) {
     return (bits >> tau_shift(pass)) & (pass == 2 ? 0x1FFu : 0x7FFu);
 }
+// bits fixed once pass `pass` has chosen its digit
+__device__ __forceinline__ uint32_t tau_fixed(int pass) {
+    return pass == 0 ? 0xFFF00000u : pass == 1 ? 0xFFFFFE00u : 0xFFFFFFFFu;
+}
+
+// tau-set membership of key t for cut (theta, tcut): mass above the cut, or
+// equal to it at an index up to tcut
+__device__ __forceinline__ bool in_tau_set(uint32_t bits, int t, uint32_t theta, int32_t tcut) {
+    return bits > theta || (bits == theta && t <= tcut);
+}
+
+// Position of score key t of a head in `keys`: thread-major for the
+// register-resident top-k (thread i owns keys i*kpt .. i*kpt + kpt - 1 and
+// reads its j-th at j*1024 + i, so the reads are contiguous), else t.
+__device__ __forceinline__ int key_pos(const SelectArgs& a, int t) {
+    return a.kpt > 0 ? (t % a.kpt) * 1024 + t / a.kpt : t;
+}
+
+// Group g's share of clearing the first-digit histogram of head hc (the
+// vote kernel fills it).
+__device__ __forceinline__ void clear_hist0_share(const SelectArgs& a, int64_t hc, int g) {
+    const int lo = static_cast<int>((2048L * g) / a.G), hi = static_cast<int>((2048L * (g + 1)) / a.G);
+    for (int i = lo + static_cast<int>(threadIdx.x); i < hi; i += static_cast<int>(blockDim.x)) a.hist0[hc * 2048 + i] = 0u;
+}
+
+// Word w of group g's membership plane of head hc.
+__device__ __forceinline__ uint32_t* plane_word(const SelectArgs& a, int64_t hc, int g, int w) {
+    const int nw = (a.T + 31) / 32;
+    return a.planes + (hc * a.G + g) * nw + w;
+}
 
 // ---------------------------------------------------------------- tau cut
 __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
@@ -189,138 +213,141 @@ __global__ void __launch_bounds__(kSelThreads) tau_cut_kernel(SelectArgs a) {
     __shared__ int32_t s_tcut;
 
     const int g = blockIdx.x, c = blockIdx.y, b = blockIdx.z;
-    const int64_t hcg = (static_cast<int64_t>(b) * a.Hkv + c) * a.G + g;
+    const int64_t hc = static_cast<int64_t>(b) * a.Hkv + c;
+    const int64_t hcg = hc * a.G + g;
     const uint32_t* m = reinterpret_cast<const uint32_t*>(a.group_mass) + hcg * a.T;
     const int tid = threadIdx.x;
     const int S = a.fix_shift;
+    clear_hist0_share(a, hc, g);
 
     uint64_t local = 0;
     for (int t = tid; t < a.T; t += kSelThreads) local += fixed_of(m[t], S);
     const uint64_t total = block_sum_u64(local, wtot64);
-    if (total == 0) {
-        // every mass is below the fixed-point resolution: empty set
-        if (tid == 0) { a.theta[hcg] = 0xFFFFFFFFu; a.tcut[hcg] = -1; }
-        return;
-    }
-    unsigned long long need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(total)));
-    if (need < 1) need = 1;
-    if (need > total) need = total;
+    // every mass below the fixed-point resolution: empty set
+    uint32_t theta = 0xFFFFFFFFu;
+    int32_t tcut = -1;
+    if (total != 0) {
+        unsigned long long need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(total)));
+        if (need < 1) need = 1;
+        if (need > total) need = total;
 
-    uint32_t prefix = 0;
-    for (int pass = 0; pass < 3; ++pass) {
-        const uint32_t mask = tau_mask(pass);
-        for (int i = tid; i < 2048; i += kSelThreads) { cnt[i] = 0; sum[i] = 0; }
-        __syncthreads();
-        // uniform trip count: hist_add needs every lane of the wave
-        for (int base = 0; base < a.T; base += kSelThreads) {
-            const int t = base + tid;
-            const uint32_t bits = t < a.T ? m[t] : 0u;
-            const bool in = t < a.T && (bits & mask) == prefix;
-            hist_add(in, tau_digit(bits, pass), in ? fixed_of(bits, S) : 0ull, cnt, sum);
+        uint32_t prefix = 0;
+        for (int pass = 0; pass < 3; ++pass) {
+            const uint32_t mask = tau_mask(pass);
+            for (int i = tid; i < 2048; i += kSelThreads) { cnt[i] = 0; sum[i] = 0; }
+            __syncthreads();
+            // uniform trip count: hist_add needs every lane of the wave
+            for (int base = 0; base < a.T; base += kSelThreads) {
+                const int t = base + tid;
+                const uint32_t bits = t < a.T ? m[t] : 0u;
+                const bool in = t < a.T && (bits & mask) == prefix;
+                hist_add(in, tau_digit(bits, pass), in ? fixed_of(bits, S) : 0ull, cnt, sum);
+            }
+            __syncthreads();
+            descending_crossing<unsigned long long>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
+            prefix |= s_digit << tau_shift(pass);
+            need = s_rem;
         }
-        __syncthreads();
-        descending_crossing<unsigned long long>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
-        prefix |= s_digit << tau_shift(pass);
-        need = s_rem;
+        // keys with mass == theta each carry f_theta; the first k_eq by index
+        // enter the set (all of them when k_eq covers the bucket)
+        theta = prefix;
+        const uint64_t f_theta = fixed_of(prefix, S);
+        const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
+        if (k_eq >= s_cnt) {
+            tcut = a.T;
+        } else {
+            if (tid == 0) s_tcut = a.T - 1;
+            __syncthreads();
+            uint64_t seen = 0;
+            for (int base = 0; base < a.T; base += kSelThreads) {
+                const int t = base + tid;
+                const bool eq = t < a.T && m[t] == prefix;
+                uint32_t tot;
+                const uint32_t before = block_excl_count(eq, wtot, tot);
+                if (eq && seen + before + 1 == k_eq) s_tcut = t;
+                seen += tot;
+                if (seen >= k_eq) break;
+            }
+            __syncthreads();
+            tcut = s_tcut;
+        }
     }
-    // keys with mass == theta each carry f_theta; the first k_eq by index
-    // enter the set (all of them when k_eq covers the bucket)
-    const uint64_t f_theta = fixed_of(prefix, S);
-    const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
-    if (k_eq >= s_cnt) {
-        if (tid == 0) { a.theta[hcg] = prefix; a.tcut[hcg] = a.T; }
-        return;
+    if (tid == 0) {
+        a.theta[hcg] = theta;
+        a.tcut[hcg] = tcut;
     }
-    if (tid == 0) s_tcut = a.T - 1;
-    __syncthreads();
-    uint64_t seen = 0;
+    // membership plane: each wave's 64 keys of a sweep step are two words
+    const int lane = lane_id();
     for (int base = 0; base < a.T; base += kSelThreads) {
         const int t = base + tid;
-        const bool eq = t < a.T && m[t] == prefix;
-        uint32_t tot;
-        const uint32_t before = block_excl_count(eq, wtot, tot);
-        if (eq && seen + before + 1 == k_eq) s_tcut = t;
-        seen += tot;
-        if (seen >= k_eq) break;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        a.theta[hcg] = prefix;
-        a.tcut[hcg] = s_tcut;
+        const uint64_t mb = __ballot(t < a.T && in_tau_set(m[t], t, theta, tcut));
+        const int w = (base + (tid & ~(kWave - 1))) / 32 + lane;
+        if (lane < 2 && 32 * w < a.T) *plane_word(a, hc, g, w) = static_cast<uint32_t>(mb >> (32 * lane));
     }
 }
 
 // ---------------------------------------------------------------- vote + score
-// VEC consecutive keys per thread (VEC = 4 needs T % 4 == 0, so every group
-// row starts on a 16-byte boundary); the G group masses of a key are fetched
-// kVoteBatch groups at a time so their latencies overlap.
-constexpr int kVoteBatch = 8;
+// One workgroup per 32 membership words (128-byte lines of every group's
+// plane) of one head, each wave two words at a time: in each half-wave,
+// lane l reads the word of group l (32 groups at a time), and one ballot per
+// bit position j counts, for both words at once, the groups whose set holds
+// key j; lane j of each half keeps its own key's count.
+constexpr int kVoteThreads = 256;
+constexpr int kVoteWords = 32;                          // words per workgroup
+constexpr int kVoteSteps = kVoteWords * kWave / (2 * kVoteThreads);
 
-template <int VEC>
-__global__ void __launch_bounds__(256) vote_score_kernel(SelectArgs a) {
-    __shared__ uint32_t th[256];
-    __shared__ int32_t tc[256];
+__global__ void __launch_bounds__(kVoteThreads) vote_score_kernel(SelectArgs a) {
+    __shared__ uint32_t lh[2048];            // this workgroup's first-digit counts
     const int c = blockIdx.y, b = blockIdx.z;
     const int64_t hc = static_cast<int64_t>(b) * a.Hkv + c;
-    const bool vote_mode = a.mode == 0;
-    if (vote_mode) {
-        for (int i = threadIdx.x; i < a.G; i += 256) {
-            th[i] = a.theta[hc * a.G + i];
-            tc[i] = a.tcut[hc * a.G + i];
+    const int lane = lane_id(), half = lane >> 5, j0 = lane & 31;
+    const int nw = (a.T + 31) / 32;
+    const int pool = a.keep_last ? a.T - 1 : a.T;
+    const int wbase = static_cast<int>(blockIdx.x) * kVoteWords + 2 * kVoteSteps * (static_cast<int>(threadIdx.x) / kWave);
+    for (int i = threadIdx.x; i < 2048; i += kVoteThreads) lh[i] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int step = 0; step < kVoteSteps; ++step) {
+        const int w = wbase + 2 * step + half;
+        const int t = 32 * w + j0;
+        double score = 0.0;
+        if (a.mode == 0) {
+            uint32_t vote = 0;
+            for (int g0 = 0; g0 < a.G; g0 += 32) {
+                const int g = g0 + j0;
+                const uint32_t word = (w < nw && g < a.G) ? *plane_word(a, hc, g, w) : 0u;
+#pragma unroll
+                for (int j = 0; j < 32; ++j) {
+                    const uint64_t m = __ballot((word >> j) & 1u);
+                    const uint32_t n0 = static_cast<uint32_t>(__popcll(m & 0xFFFFFFFFull));
+                    const uint32_t n1 = static_cast<uint32_t>(__popcll(m >> 32));
+                    if (j0 == j) vote += half ? n1 : n0;
+                }
+            }
+            if (t < a.T) {
+                score = static_cast<double>(vote) + a.lambda * static_cast<double>(a.anchor[hc * a.T + t]);
+                if (a.votes != nullptr) a.votes[hc * a.T + t] = static_cast<uint8_t>(vote);
+            }
+        } else if (t < a.T) {
+            score = static_cast<double>(a.mass[hc * a.T + t]);
+        }
+        if (t < a.T) {
+            const uint64_t key = static_cast<uint64_t>(__double_as_longlong(score));
+            a.keys[hc * a.key_stride + key_pos(a, t)] = key;
+            if (t < pool) atomicAdd(&lh[static_cast<uint32_t>(key >> 53) & 2047u], 1u);
         }
     }
     __syncthreads();
-    const int t0 = (static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x)) * VEC;
-    if (t0 >= a.T) return;
-    double score[VEC];
-    if (vote_mode) {
-        int vote[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) vote[e] = 0;
-        const uint32_t* gm = reinterpret_cast<const uint32_t*>(a.group_mass) + hc * a.G * static_cast<int64_t>(a.T) + t0;
-        for (int g0 = 0; g0 < a.G; g0 += kVoteBatch) {
-            uint32_t v[kVoteBatch][VEC];
-#pragma unroll
-            for (int j = 0; j < kVoteBatch; ++j) {
-                const int g = g0 + j;
-                if (VEC == 4) {
-                    u32x4 x = {0u, 0u, 0u, 0u};
-                    if (g < a.G) x = *reinterpret_cast<const u32x4*>(gm + static_cast<int64_t>(g) * a.T);
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) v[j][e] = x[e];
-                } else {
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e)
-                        v[j][e] = (g < a.G && t0 + e < a.T) ? gm[static_cast<int64_t>(g) * a.T + e] : 0u;
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < kVoteBatch; ++j) {
-                const int g = g0 + j;
-                if (g < a.G) {
-                    const uint32_t tg = th[g];
-                    const int cg = tc[g];
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e)
-                        vote[e] += (v[j][e] > tg || (v[j][e] == tg && t0 + e <= cg)) ? 1 : 0;
-                }
-            }
-        }
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-            if (t0 + e < a.T) {
-                score[e] = static_cast<double>(vote[e]) + a.lambda * static_cast<double>(a.anchor[hc * a.T + t0 + e]);
-                if (a.votes != nullptr) a.votes[hc * a.T + t0 + e] = static_cast<uint8_t>(vote[e]);
-            }
-        }
-    } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e)
-            if (t0 + e < a.T) score[e] = static_cast<double>(a.mass[hc * a.T + t0 + e]);
-    }
-#pragma unroll
-    for (int e = 0; e < VEC; ++e)
-        if (t0 + e < a.T) a.keys[hc * a.T + t0 + e] = static_cast<uint64_t>(__double_as_longlong(score[e]));
+    for (int i = threadIdx.x; i < 2048; i += kVoteThreads)
+        if (lh[i] != 0u) atomicAdd(&a.hist0[hc * 2048 + i], lh[i]);
+}
+
+// Clears the first-digit histograms where no tau cut runs before the vote
+// kernel (MASS mode).
+__global__ void __launch_bounds__(256) clear_hist0_kernel(SelectArgs a) {
+    const int64_t n = static_cast<int64_t>(a.B) * a.Hkv * 2048;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += static_cast<int64_t>(gridDim.x) * 256)
+        a.hist0[i] = 0u;
 }
 
 // ---------------------------------------------------------------- top-k
@@ -329,7 +356,8 @@ __global__ void __launch_bounds__(256) vote_score_kernel(SelectArgs a) {
 // once the crossing bucket is taken whole.  `each(f)` calls f(key, ok) with
 // the same trip count on every thread, ok marking the pool keys this thread
 // owns.  On return, the selected keys are {key > theta} plus the first k_eq
-// keys (by index) with key == theta.  Requires 1 <= want < pool size.
+// keys (by index) with key == theta.  Requires 1 <= want < pool size.  The
+// first pass takes its counts from h0 (all pool keys by bits 63..53).
 struct TopkShared {
     uint32_t cnt[2048];
     uint32_t wtot[kSelWaves];
@@ -337,20 +365,24 @@ struct TopkShared {
 };
 
 template <typename Each>
-__device__ __forceinline__ void topk_threshold(uint32_t want, Each each, TopkShared& sh, uint64_t& theta,
-                                               uint32_t& k_eq) {
+__device__ __forceinline__ void topk_threshold(uint32_t want, Each each, const uint32_t* h0, TopkShared& sh,
+                                               uint64_t& theta, uint32_t& k_eq) {
     const int tid = threadIdx.x;
     uint64_t prefix = 0, mask = 0;
     uint32_t need = want;
     for (int pass = 0; pass < 6; ++pass) {
         const int shift = pass == 5 ? 0 : 53 - 11 * pass;
-        for (int i = tid; i < 2048; i += kSelThreads) sh.cnt[i] = 0;
-        __syncthreads();
-        // plain LDS atomics: same-digit lanes of a wave serialise in the LDS
-        // unit, which is cheaper than combining them with wave operations
-        each([&](uint64_t kv, bool ok) {
-            if (ok && (kv & mask) == prefix) atomicAdd(&sh.cnt[static_cast<uint32_t>(kv >> shift) & 2047u], 1u);
-        });
+        if (pass == 0) {
+            // the first digit's counts, made by the vote kernel
+            for (int i = tid; i < 2048; i += kSelThreads) sh.cnt[i] = h0[i];
+        } else {
+            for (int i = tid; i < 2048; i += kSelThreads) sh.cnt[i] = 0;
+            __syncthreads();
+            // plain LDS atomics over the keys left in the crossing bucket
+            each([&](uint64_t kv, bool ok) {
+                if (ok && (kv & mask) == prefix) atomicAdd(&sh.cnt[static_cast<uint32_t>(kv >> shift) & 2047u], 1u);
+            });
+        }
         __syncthreads();
         descending_crossing<uint32_t>(sh.cnt, sh.cnt, need, sh.wtot, &sh.s_digit, &sh.s_rem, &sh.s_cnt);
         prefix |= static_cast<uint64_t>(sh.s_digit) << shift;
@@ -385,7 +417,7 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
     }
     const int pool = a.keep_last ? a.T - 1 : a.T;
     const uint32_t want = static_cast<uint32_t>(a.keep_last ? budget - 1 : budget);
-    const uint64_t* key = a.keys + hc * a.T;
+    const uint64_t* key = a.keys + hc * a.key_stride;
 
     uint64_t theta = 0;
     uint32_t k_eq = 0;
@@ -395,7 +427,7 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
                 const int t = base + tid;
                 f(t < pool ? key[t] : 0ull, t < pool);
             }
-        }, sh, theta, k_eq);
+        }, a.hist0 + hc * 2048, sh, theta, k_eq);
     }
     uint32_t eq_seen = 0, written = 0;
     for (int base = 0; base < pool; base += kSelThreads) {
@@ -429,9 +461,15 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
 
 // tau cut of one (b, c, group); same result as tau_cut_kernel.  512 threads
 // of at most 128 VGPRs, so two workgroups share a CU and a whole launch of
-// 512 workgroups is resident at once.
+// 512 workgroups is resident at once.  Thread i holds keys
+// 2048 q + 4 i + e (q < KPT / 4, e < 4), so every load is one contiguous
+// 16-byte piece per lane; the index-ordered steps (ties, the plane) go
+// through the 2048-key chunks q in order.
 template <int KPT>
 __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) {
+    static_assert(KPT % 4 == 0, "whole 4-key pieces per thread");
+    constexpr int kQ = KPT / 4;
+    constexpr int kChunk = 4 * kTauThreads;
     __shared__ uint32_t cnt[2048];
     __shared__ unsigned long long sum[2048];
     __shared__ unsigned long long wtot64[kTauWaves];
@@ -442,95 +480,119 @@ __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) 
     __shared__ uint32_t s_theta;
 
     const int g = blockIdx.x, c = blockIdx.y, b = blockIdx.z;
-    const int64_t hcg = (static_cast<int64_t>(b) * a.Hkv + c) * a.G + g;
+    const int64_t hc = static_cast<int64_t>(b) * a.Hkv + c;
+    const int64_t hcg = hc * a.G + g;
     const uint32_t* m = reinterpret_cast<const uint32_t*>(a.group_mass) + hcg * a.T;
-    const int tid = threadIdx.x;
-    const int t0 = tid * KPT;
+    const int tid = threadIdx.x, lane = lane_id();
     const int S = a.fix_shift;
+    clear_hist0_share(a, hc, g);
+    auto key_of = [&](int q, int e) { return kChunk * q + 4 * tid + e; };
 
     // masses (bits), held for all passes (their fixed-point values are
     // recomputed where needed); keys past T read as mass 0
     uint32_t mb[KPT];
-    if (t0 + KPT <= a.T && (reinterpret_cast<uintptr_t>(m + t0) & 15u) == 0) {
+    if ((a.T & 3) == 0 && (reinterpret_cast<uintptr_t>(m) & 15u) == 0) {
 #pragma unroll
-        for (int j = 0; j < KPT; j += 4) {
-            const u32x4 x = *reinterpret_cast<const u32x4*>(m + t0 + j);
-            mb[j] = x[0]; mb[j + 1] = x[1]; mb[j + 2] = x[2]; mb[j + 3] = x[3];
+        for (int q = 0; q < kQ; ++q) {
+            u32x4 x = {0u, 0u, 0u, 0u};
+            if (key_of(q, 0) < a.T) x = *reinterpret_cast<const u32x4*>(m + key_of(q, 0));
+            mb[4 * q] = x[0]; mb[4 * q + 1] = x[1]; mb[4 * q + 2] = x[2]; mb[4 * q + 3] = x[3];
         }
     } else {
 #pragma unroll
-        for (int j = 0; j < KPT; ++j) mb[j] = (t0 + j < a.T) ? m[t0 + j] : 0u;
+        for (int q = 0; q < kQ; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) mb[4 * q + e] = key_of(q, e) < a.T ? m[key_of(q, e)] : 0u;
     }
     uint64_t local = 0;
 #pragma unroll
     for (int j = 0; j < KPT; ++j) local += fixed_of(mb[j], S);
     const uint64_t total = block_sum_u64<kTauThreads>(local, wtot64);
-    if (total == 0) {
-        if (tid == 0) { a.theta[hcg] = 0xFFFFFFFFu; a.tcut[hcg] = -1; }
-        return;
-    }
-    unsigned long long need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(total)));
-    if (need < 1) need = 1;
-    if (need > total) need = total;
+    // every mass below the fixed-point resolution: empty set
+    uint32_t theta = 0xFFFFFFFFu;
+    int32_t tcut = -1;
+    if (total != 0) {
+        unsigned long long need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(total)));
+        if (need < 1) need = 1;
+        if (need > total) need = total;
 
-    uint32_t prefix = 0;
+        uint32_t prefix = 0;
 #pragma nounroll
-    for (int pass = 0; pass < 3; ++pass) {
-        const uint32_t mask = tau_mask(pass);
-        for (int i = tid; i < 2048; i += kTauThreads) { cnt[i] = 0; sum[i] = 0; }
-        __syncthreads();
-#pragma unroll
-        for (int j = 0; j < KPT; ++j) {
-            // opaque inside the pass loop, so the fixed-point values are not
-            // hoisted out of it and kept live
-            asm volatile("" : "+v"(mb[j]));
-            if (t0 + j < a.T && (mb[j] & mask) == prefix) {
-                const uint32_t dg = tau_digit(mb[j], pass);
-                atomicAdd(&cnt[dg], 1u);
-                atomicAdd(&sum[dg], static_cast<unsigned long long>(fixed_of(mb[j], S)));
-            }
-        }
-        __syncthreads();
-        descending_crossing<unsigned long long, kTauThreads>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
-        prefix |= s_digit << tau_shift(pass);
-        need = s_rem;
-        if (pass < 2 && s_cnt == 1u) {
-            // one key left in the crossing bucket: its mass is theta, and the
-            // remaining passes would only spell out its low bits
-            const uint32_t fixed = tau_mask(pass + 1);
-#pragma unroll
-            for (int j = 0; j < KPT; ++j)
-                if (t0 + j < a.T && (mb[j] & fixed) == prefix) s_theta = mb[j];
+        for (int pass = 0; pass < 3; ++pass) {
+            const uint32_t mask = tau_mask(pass);
+            for (int i = tid; i < 2048; i += kTauThreads) { cnt[i] = 0; sum[i] = 0; }
             __syncthreads();
-            prefix = s_theta;
-            break;
-        }
-    }
-    const uint64_t f_theta = fixed_of(prefix, S);
-    const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
-    if (k_eq >= s_cnt) {
-        if (tid == 0) { a.theta[hcg] = prefix; a.tcut[hcg] = a.T; }
-        return;
-    }
-    // the k_eq-th key (by index) whose mass equals theta
-    uint32_t n_eq = 0;
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) n_eq += (t0 + j < a.T && mb[j] == prefix) ? 1u : 0u;
-    uint32_t eq_total;
-    const uint32_t eq_before = block_excl_scan<uint32_t, kTauThreads>(n_eq, wtot, eq_total);
-    if (eq_before < k_eq && k_eq <= eq_before + n_eq) {
-        uint32_t seen = eq_before;
+            for (int j = 0; j < KPT; ++j) {
+                // opaque inside the pass loop, so the fixed-point values are not
+                // hoisted out of it and kept live
+                asm volatile("" : "+v"(mb[j]));
+                if (key_of(j / 4, j % 4) < a.T && (mb[j] & mask) == prefix) {
+                    const uint32_t dg = tau_digit(mb[j], pass);
+                    atomicAdd(&cnt[dg], 1u);
+                    atomicAdd(&sum[dg], static_cast<unsigned long long>(fixed_of(mb[j], S)));
+                }
+            }
+            __syncthreads();
+            descending_crossing<unsigned long long, kTauThreads>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
+            prefix |= s_digit << tau_shift(pass);
+            need = s_rem;
+            if (pass < 2 && s_cnt == 1u) {
+                // one key left in the crossing bucket: its mass is theta, and the
+                // remaining passes would only spell out its low bits
 #pragma unroll
-        for (int j = 0; j < KPT; ++j) {
-            if (t0 + j < a.T && mb[j] == prefix) {
-                if (++seen == k_eq) s_tcut = t0 + j;
+                for (int j = 0; j < KPT; ++j)
+                    if (key_of(j / 4, j % 4) < a.T && (mb[j] & tau_fixed(pass)) == prefix) s_theta = mb[j];
+                __syncthreads();
+                prefix = s_theta;
+                break;
             }
         }
+        theta = prefix;
+        const uint64_t f_theta = fixed_of(prefix, S);
+        const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
+        if (k_eq >= s_cnt) {
+            tcut = a.T;
+        } else {
+            // the k_eq-th key (by index) whose mass equals theta, chunk by chunk
+            if (tid == 0) s_tcut = a.T - 1;
+            uint64_t seen = 0;
+#pragma nounroll
+            for (int q = 0; q < kQ; ++q) {
+                uint32_t n_eq = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) n_eq += (key_of(q, e) < a.T && mb[4 * q + e] == prefix) ? 1u : 0u;
+                uint32_t tot;
+                const uint32_t before = block_excl_scan<uint32_t, kTauThreads>(n_eq, wtot, tot);
+                if (seen + before < k_eq && k_eq <= seen + before + n_eq) {
+                    uint64_t at = seen + before;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (key_of(q, e) < a.T && mb[4 * q + e] == prefix && ++at == k_eq) s_tcut = key_of(q, e);
+                }
+                seen += tot;
+                if (seen >= k_eq) break;
+            }
+            __syncthreads();
+            tcut = s_tcut;
+        }
     }
-    __syncthreads();
     if (tid == 0) {
-        a.theta[hcg] = prefix;
-        a.tcut[hcg] = s_tcut;
+        a.theta[hcg] = theta;
+        a.tcut[hcg] = tcut;
+    }
+    // membership plane: each lane's 4 bits, merged over the 8 lanes of a word
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+        uint32_t word = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int t = key_of(q, e);
+            word |= (t < a.T && in_tau_set(mb[4 * q + e], t, theta, tcut)) ? 1u << (4 * (lane & 7) + e) : 0u;
+        }
+#pragma unroll
+        for (int o = 1; o < 8; o <<= 1) word |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(word), o, kWave));
+        if ((lane & 7) == 0 && key_of(q, 0) < a.T) *plane_word(a, hc, g, key_of(q, 0) / 32) = word;
     }
 }
 
@@ -553,11 +615,11 @@ __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
     }
     const int pool = a.keep_last ? a.T - 1 : a.T;
     const uint32_t want = static_cast<uint32_t>(a.keep_last ? budget - 1 : budget);
-    const uint64_t* key = a.keys + hc * a.T;
+    const uint64_t* key = a.keys + hc * a.key_stride;
     const int t0 = tid * KPT;
     uint64_t kv[KPT];
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) kv[j] = (t0 + j < pool) ? key[t0 + j] : 0ull;
+    for (int j = 0; j < KPT; ++j) kv[j] = (t0 + j < pool) ? key[j * kSelThreads + tid] : 0ull;
 
     uint64_t theta = 0;
     uint32_t k_eq = 0;
@@ -565,7 +627,7 @@ __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
         topk_threshold(want, [&](auto&& f) {
 #pragma unroll
             for (int j = 0; j < KPT; ++j) f(kv[j], t0 + j < pool);
-        }, sh, theta, k_eq);
+        }, a.hist0 + hc * 2048, sh, theta, k_eq);
     }
     // index-ordered compaction: keys > theta, then the first k_eq equal keys
     uint32_t n_eq = 0;
@@ -605,12 +667,16 @@ __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
 
 }  // namespace
 
+int select_kpt(int T) {
+    // register-resident top-k while a row fits in 32 keys per thread of 1024
+    const int per = (T + kSelThreads - 1) / kSelThreads;
+    return per <= 4 ? 4 : per <= 8 ? 8 : per <= 16 ? 16 : per <= 32 ? 32 : 0;
+}
+
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-    // register-resident kernels while a row fits in 32 elements per thread
-    // (512 threads for the tau cut, 1024 for the top-k)
-    const int per = (a.T + kSelThreads - 1) / kSelThreads;
-    const int kpt = per <= 4 ? 4 : per <= 8 ? 8 : per <= 16 ? 16 : per <= 32 ? 32 : 0;
+    if (a.kpt != select_kpt(a.T) || a.key_stride != select_key_stride(a.T)) return hipErrorInvalidValue;
     if (a.mode == 0) {
+        // register-resident tau cut while a row fits in 32 masses per thread of 512
         dim3 g1(a.G, a.Hkv, a.B);
         const int tper = (a.T + kTauThreads - 1) / kTauThreads;
         const int tkpt = tper <= 8 ? 8 : tper <= 16 ? 16 : tper <= 32 ? 32 : 0;
@@ -620,20 +686,20 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
             case 32: hipLaunchKernelGGL(tau_cut_reg_kernel<32>, g1, dim3(kTauThreads), 0, s, a); break;
             default: hipLaunchKernelGGL(tau_cut_kernel, g1, dim3(kSelThreads), 0, s, a); break;
         }
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    if ((a.T & 3) == 0 && (reinterpret_cast<uintptr_t>(a.group_mass) & 15u) == 0) {
-        dim3 g2((a.T / 4 + 255) / 256, a.Hkv, a.B);
-        hipLaunchKernelGGL(vote_score_kernel<4>, g2, dim3(256), 0, s, a);
     } else {
-        dim3 g2((a.T + 255) / 256, a.Hkv, a.B);
-        hipLaunchKernelGGL(vote_score_kernel<1>, g2, dim3(256), 0, s, a);
+        const int64_t n = static_cast<int64_t>(a.B) * a.Hkv * 2048;
+        hipLaunchKernelGGL(clear_hist0_kernel, dim3(static_cast<unsigned>((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024)),
+                           dim3(256), 0, s, a);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    const int nw = (a.T + 31) / 32;
+    dim3 g2((nw + kVoteWords - 1) / kVoteWords, a.Hkv, a.B);
+    hipLaunchKernelGGL(vote_score_kernel, g2, dim3(kVoteThreads), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
     dim3 g3(a.Hkv, a.B);
-    switch (kpt) {
+    switch (a.kpt) {
         case 4: hipLaunchKernelGGL(topk_reg_kernel<4>, g3, dim3(kSelThreads), 0, s, a); break;
         case 8: hipLaunchKernelGGL(topk_reg_kernel<8>, g3, dim3(kSelThreads), 0, s, a); break;
         case 16: hipLaunchKernelGGL(topk_reg_kernel<16>, g3, dim3(kSelThreads), 0, s, a); break;
