@@ -63,11 +63,32 @@ def measured_traffic(workload, kernel):
     if t.get("workload") != workload or t.get("score_hip_sha256") != src:
         return None
     # a pass is the kernels one C-ABI call launches
-    parts = {"score_lse": ("score_lse", "lse_combine")}.get(kernel, (kernel,))
+    parts = {"score_lse": ("anchor_rows", "score_lse", "lse_combine")}.get(kernel, (kernel,))
     ks = [t.get("kernels", {}).get(p) for p in parts]
     if any(k is None or k.get("hbm_bytes_per_launch") is None for k in ks):
         return None
     return sum(k["hbm_bytes_per_launch"] for k in ks)
+
+
+def measured_mfma_util(workload):
+    """MFMA busy fraction (and clock) of the two score kernels from the committed
+    counter summary, or None under the same conditions as measured_traffic."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        with open(SCORE_SRC, "rb") as f:
+            src = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if t.get("workload") != workload or t.get("score_hip_sha256") != src:
+        return None
+    k = t.get("kernels", {})
+    try:
+        return {p: {"mfma_busy": k[p]["mfma_busy"], "valu_busy": k[p]["valu_busy"], "clock_ghz": k[p]["clock_ghz"]}
+                for p in ("score_lse", "score_mass")} | {"source": "profiles/counters_score_qwen7b_16k_b4.md"}
+    except KeyError:
+        return None
 
 
 def calibrate_copy(nbytes=1 << 30, reps=5):
@@ -103,8 +124,21 @@ def cpu_baseline(w, cfg, layer_inputs, heads=1):
     dt = time.perf_counter() - t0
     keys = heads / w.Hkv * w.T          # one KV head covers 1/Hkv of a sequence-layer's keys
     return {"value": keys / dt, "unit": "prompt keys/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "nproc": os.cpu_count(), "cpu_model": cpu_model(),
             "sample": "%d (batch row, KV head) pair(s) of layer 0, T=%d, all steps; %.1f s"
                       % (heads, w.T, dt)}
+
+
+def cpu_model():
+    """The host CPU's model name (first entry of /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def decode_check_bench(args):
@@ -497,11 +531,63 @@ def main():
     mass_ms = sum(ev[s][l][1].elapsed_time(ev[s][l][2]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
     log("kernel timing on one stream: score_lse %.1f us, score_mass %.1f us per layer" % (lse_ms * 1e3, mass_ms * 1e3))
 
+    # the other stages: each C-ABI call repeated back to back on one stream
+    # (layer 0's inputs, the buffers of stream 0), so the time per call is
+    # its kernels plus the launch gaps between calls
+    x, c, bf = layers[0], cfgs[0], bufs[0]
+    sel_args = (bf["sc"], c, w.budget, w.budget, None, Hq, W)
+    calls = {
+        "build_proxies": lambda: bd.build_proxies(x["q_win"], c, T, Hkv, out=(bf["prox"], bf["qlast"])),
+        "select_tau": lambda: bd.select_topk(*sel_args, out=bf["sel"], workspace=bf["ws_sel"], stage="tau"),
+        "select_vote": lambda: bd.select_topk(*sel_args, out=bf["sel"], workspace=bf["ws_sel"], stage="vote"),
+        "select_pick": lambda: bd.select_topk(*sel_args, out=bf["sel"], workspace=bf["ws_sel"], stage="pick"),
+        "gather": lambda: bd.gather_kv(x["k"], x["v"], bf["sel"], out=kv_out[0]),
+    }
+    reps = 20
+    stage_ms = {}
+    with torch.cuda.stream(stream):
+        for name, fn in calls.items():
+            if name == "select_pick":
+                # the vote repetitions added to the first-digit counts: one
+                # tau + vote pair restores the state the pick reads
+                calls["select_tau"]()
+                calls["select_vote"]()
+            fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            stage_ms[name] = e0.elapsed_time(e1) / reps
+        # leave layer 0's selection as a whole call made it
+        bd.select_topk(*sel_args, out=bf["sel"], workspace=bf["ws_sel"])
+        torch.cuda.synchronize()
+    stage_ms = {"build_proxies": stage_ms["build_proxies"], "score_lse": lse_ms, "score_mass": mass_ms,
+                **{k: v for k, v in stage_ms.items() if k != "build_proxies"}}
+    log("per call (us): " + ", ".join("%s %.1f" % (k, v * 1e3) for k, v in stage_ms.items()))
+
     # algorithmic MFMA work of one scoring launch: 2*Gh*P*d flops per prompt
     # key per KV head (one proxy-by-key contraction), times B*Hkv*T keys
     flops = 2.0 * w.Gh * cfg.P * d * B * Hkv * T
     # one launch = one C-ABI pass call: score_lse = score_lse_kernel + lse_combine_kernel,
     # score_mass = score_mass_kernel
+    # algorithmic HBM bytes of the memory-bound stages, per layer (all heads)
+    heads = B * Hkv
+    eb = layers[0]["k"].element_size()
+    words = (T + 31) // 32
+    vote_mode = mode == bd.MMSKV_VOTE
+    stage_bytes = {
+        # masses read, membership planes written
+        "select_tau": heads * (cfg.G * T * 4 + cfg.G * words * 4) if vote_mode else 0,
+        # planes and anchor (or masses) read, fp64 score keys written
+        "select_vote": heads * ((cfg.G * words * 4 + T * 4) if vote_mode else T * 4) + heads * T * 8,
+        # score keys and first-digit counts read, indices written
+        "select_pick": heads * (T * 8 + 2048 * 4 + w.budget * 4 + 4),
+        # selected K and V rows read and written
+        "gather": heads * w.budget * d * eb * 4,
+    }
+    stage_bytes = {k: v for k, v in stage_bytes.items() if v > 0}
     dom = "score_mass" if mass_ms >= lse_ms else "score_lse"
     dom_ms = max(mass_ms, lse_ms)
     achieved = flops / (dom_ms * 1e-3) / 1e12
@@ -523,11 +609,16 @@ def main():
         "config": {"workload": w.name, "layers": L, "batch": B, "T": T, "Hq": Hq, "Hkv": Hkv, "d": d, "W": W,
                    "budget": w.budget, "P": cfg.P, "G": cfg.G, "gamma": cfg.gamma, "tau": cfg.tau,
                    "lambda": cfg.lam, "mode": args.mode, "streams": n_streams},
-        "stages_us_per_layer": {"score_lse": lse_ms * 1e3, "score_mass": mass_ms * 1e3},
+        "stages_us_per_layer": {k: v * 1e3 for k, v in stage_ms.items()},
+        "stages_timing": "score passes: events around them in %d steps on one stream; the rest: %d back-to-back "
+                         "calls of one stage on one stream (kernels + launch gaps)" % (args.steps, reps),
+        "non_score_us_per_layer": sum(v for k, v in stage_ms.items() if not k.startswith("score_")) * 1e3,
+        "stage_hbm_frac": {k: stage_bytes[k] / (stage_ms[k] * 1e-3) / 1e9 / PEAK_HBM_GBS for k in stage_bytes},
         "roofline": {"kernel": dom + " pass", "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(w.name, dom),
                      "timing": "%d steps on one stream after the throughput steps" % args.steps},
+        "mfma_util_counter": measured_mfma_util(w.name),
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on %d head(s)" % args.cpu_heads)

@@ -204,6 +204,26 @@ int mmshiftkv_select_topk(const mmskv_shape *shape, const mmskv_params *params,
                           int32_t *idx, int32_t *counts, uint8_t *votes,
                           void *workspace, size_t workspace_bytes, void *stream);
 
+/* The three stages of mmshiftkv_select_topk as separate calls (same
+ * arguments, same workspace), for callers that schedule or time them
+ * separately; called in this order on one stream they are
+ * mmshiftkv_select_topk.  Each keeps its state in the workspace for the
+ * next, so nothing else may write the workspace between them.
+ * mmshiftkv_select_tau: VOTE mode, the tau cut of every group (reads
+ * group_mass); MASS mode, only clears the workspace's digit counts.
+ * mmshiftkv_select_vote: votes (VOTE; `votes` out or NULL) and the score of
+ * every key (reads anchor in VOTE mode, mass in MASS mode).
+ * mmshiftkv_select_pick: the budgeted top-k into idx and counts.
+ * Each checks the arguments it reads as mmshiftkv_select_topk does. */
+int mmshiftkv_select_tau(const mmskv_shape *shape, const mmskv_params *params, const float *group_mass,
+                         void *workspace, size_t workspace_bytes, void *stream);
+int mmshiftkv_select_vote(const mmskv_shape *shape, const mmskv_params *params, const float *mass,
+                          const float *anchor, uint8_t *votes, void *workspace, size_t workspace_bytes,
+                          void *stream);
+int mmshiftkv_select_pick(const mmskv_shape *shape, const mmskv_params *params, const int32_t *budgets,
+                          int32_t budget, int32_t c_max, int32_t *idx, int32_t *counts,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
 /* Step 4 -- compacted cache (Appendix B: retained tokens in temporal order,
  * inserted through the standard cache update).  For j < counts[b,c]:
  *   k_out[b,c,j,:] = k[b,c,idx[b,c,j],:], v_out likewise (byte copies);

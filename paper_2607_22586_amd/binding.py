@@ -23,7 +23,8 @@ MMSKV_VOTE, MMSKV_MASS = 0, 1
 
 EXPORTED = ("mmshiftkv_build_proxies", "mmshiftkv_score_workspace", "mmshiftkv_score",
             "mmshiftkv_score_lse", "mmshiftkv_score_mass", "mmshiftkv_select_workspace",
-            "mmshiftkv_select_topk", "mmshiftkv_gather_kv", "mmshiftkv_status_string",
+            "mmshiftkv_select_topk", "mmshiftkv_select_tau", "mmshiftkv_select_vote", "mmshiftkv_select_pick",
+            "mmshiftkv_gather_kv", "mmshiftkv_status_string",
             "mmshiftkv_version", "mmshiftkv_hidden_stats_workspace", "mmshiftkv_hidden_stats",
             "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies", "mmshiftkv_decode_workspace",
             "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores",
@@ -81,6 +82,9 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_select_workspace.argtypes = [PS, PP]
     lib.mmshiftkv_select_workspace.restype = SZ
     lib.mmshiftkv_select_topk.argtypes = [PS, PP, V, V, V, V, I32, I32, V, V, V, V, SZ, V]
+    lib.mmshiftkv_select_tau.argtypes = [PS, PP, V, V, SZ, V]
+    lib.mmshiftkv_select_vote.argtypes = [PS, PP, V, V, V, V, SZ, V]
+    lib.mmshiftkv_select_pick.argtypes = [PS, PP, V, I32, I32, V, V, V, SZ, V]
     lib.mmshiftkv_gather_kv.argtypes = [PS, V, V, I32, PT, PT, V, V, I32, V, V, V]
     PH = ctypes.POINTER(HShape)
     lib.mmshiftkv_hidden_stats_workspace.argtypes = [PH]
@@ -97,7 +101,8 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_status_string.restype = ctypes.c_char_p
     lib.mmshiftkv_version.restype = ctypes.c_int
     for name in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_score_lse",
-                 "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_gather_kv",
+                 "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_select_tau",
+                 "mmshiftkv_select_vote", "mmshiftkv_select_pick", "mmshiftkv_gather_kv",
                  "mmshiftkv_hidden_stats", "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies",
                  "mmshiftkv_decode_check", "mmshiftkv_window_rows", "mmshiftkv_shape_scores",
             "mmshiftkv_score_noalloc"):
@@ -377,8 +382,10 @@ class Selected:
 def select_topk(s: ScoreOut, cfg: SelectionConfig, budget: int, c_max: int | None = None,
                 budgets: torch.Tensor | None = None, Hq: int | None = None, W: int = 1,
                 want_votes: bool = False, out: Selected | None = None,
-                workspace: torch.Tensor | None = None) -> Selected:
-    """mmshiftkv_select_topk: tau-sets, votes, score and budgeted top-k."""
+                workspace: torch.Tensor | None = None, stage: str | None = None) -> Selected:
+    """mmshiftkv_select_topk: tau-sets, votes, score and budgeted top-k; with
+    stage "tau", "vote" or "pick" only that stage's call (mmshiftkv_select_tau /
+    _vote / _pick), which must run in that order on one workspace."""
     dev = _dev(s.mass)
     B, Hkv, T = s.mass.shape
     Hq = Hkv if Hq is None else Hq
@@ -394,12 +401,28 @@ def select_topk(s: ScoreOut, cfg: SelectionConfig, budget: int, c_max: int | Non
                        torch.empty((B, Hkv, T), dtype=torch.uint8, device=dev) if want_votes else None)
     if budgets is not None:
         budgets = budgets.to(device=dev, dtype=torch.int32).contiguous()
+    nbytes = ws.numel() * ws.element_size()
+    S, Pm = ctypes.byref(shape), ctypes.byref(prm)
     with torch.cuda.device(dev):
-        rc = lib.mmshiftkv_select_topk(ctypes.byref(shape), ctypes.byref(prm), _p(s.group_mass), _p(s.mass),
-                                       _p(s.anchor), _p(budgets), int(budget), c_max, _p(out.idx),
-                                       _p(out.counts), _p(out.votes), _p(ws),
-                                       ws.numel() * ws.element_size(), _stream(dev))
-    _check("mmshiftkv_select_topk", rc)
+        if stage is None:
+            name = "mmshiftkv_select_topk"
+            rc = lib.mmshiftkv_select_topk(S, Pm, _p(s.group_mass), _p(s.mass), _p(s.anchor), _p(budgets),
+                                           int(budget), c_max, _p(out.idx), _p(out.counts), _p(out.votes),
+                                           _p(ws), nbytes, _stream(dev))
+        elif stage == "tau":
+            name = "mmshiftkv_select_tau"
+            rc = lib.mmshiftkv_select_tau(S, Pm, _p(s.group_mass), _p(ws), nbytes, _stream(dev))
+        elif stage == "vote":
+            name = "mmshiftkv_select_vote"
+            rc = lib.mmshiftkv_select_vote(S, Pm, _p(s.mass), _p(s.anchor), _p(out.votes), _p(ws), nbytes,
+                                           _stream(dev))
+        elif stage == "pick":
+            name = "mmshiftkv_select_pick"
+            rc = lib.mmshiftkv_select_pick(S, Pm, _p(budgets), int(budget), c_max, _p(out.idx), _p(out.counts),
+                                           _p(ws), nbytes, _stream(dev))
+        else:
+            raise ValueError("stage must be None, 'tau', 'vote' or 'pick'")
+    _check(name, rc)
     return out
 
 

@@ -365,20 +365,29 @@ size_t mmshiftkv_select_workspace(const mmskv_shape* shape, const mmskv_params* 
     return select_layout(shape, params).total;
 }
 
-int mmshiftkv_select_topk(const mmskv_shape* shape, const mmskv_params* params, const float* group_mass,
-                          const float* mass, const float* anchor, const int32_t* budgets, int32_t budget,
-                          int32_t c_max, int32_t* idx, int32_t* counts, uint8_t* votes, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+namespace {
+
+// Validation and argument packing of the selection calls; `stages` is a mask
+// of kSelectTau, kSelectVote, kSelectPick, each stage checking the
+// arguments it reads.
+int select_call(const mmskv_shape* shape, const mmskv_params* params, const float* group_mass, const float* mass,
+                const float* anchor, const int32_t* budgets, int32_t budget, int32_t c_max, int32_t* idx,
+                int32_t* counts, uint8_t* votes, void* workspace, size_t workspace_bytes, void* stream, int stages) {
     int rc = check_heads(shape);
     if (rc) return rc;
     rc = check_method(params);
     if (rc) return rc;
-    if (idx == nullptr || counts == nullptr || c_max < 1) return MMSKV_EINVAL;
-    if (budgets == nullptr && (budget < 1 || c_max < (budget < shape->T ? budget : shape->T)))
-        return MMSKV_EINVAL;
-    if (params->mode == MMSKV_VOTE && (group_mass == nullptr || anchor == nullptr)) return MMSKV_EINVAL;
-    if (params->mode == MMSKV_MASS && mass == nullptr) return MMSKV_EINVAL;
-    if (params->mode == MMSKV_MASS && votes != nullptr) return MMSKV_EINVAL;
+    const bool vote = params->mode == MMSKV_VOTE;
+    if ((stages & kSelectTau) && vote && group_mass == nullptr) return MMSKV_EINVAL;
+    if (stages & kSelectVote) {
+        if (vote && anchor == nullptr) return MMSKV_EINVAL;
+        if (!vote && (mass == nullptr || votes != nullptr)) return MMSKV_EINVAL;
+    }
+    if (stages & kSelectPick) {
+        if (idx == nullptr || counts == nullptr || c_max < 1) return MMSKV_EINVAL;
+        if (budgets == nullptr && (budget < 1 || c_max < (budget < shape->T ? budget : shape->T)))
+            return MMSKV_EINVAL;
+    }
     const SelectLayout l = select_layout(shape, params);
     if (workspace == nullptr || !aligned(workspace, kAlign) || workspace_bytes < l.total)
         return MMSKV_EWORKSPACE;
@@ -416,7 +425,37 @@ int mmshiftkv_select_topk(const mmskv_shape* shape, const mmskv_params* params, 
     a.idx = idx;
     a.counts = counts;
     a.votes = votes;
-    return status_of(launch_select(a, static_cast<hipStream_t>(stream)));
+    return status_of(launch_select(a, stages, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+int mmshiftkv_select_topk(const mmskv_shape* shape, const mmskv_params* params, const float* group_mass,
+                          const float* mass, const float* anchor, const int32_t* budgets, int32_t budget,
+                          int32_t c_max, int32_t* idx, int32_t* counts, uint8_t* votes, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    return select_call(shape, params, group_mass, mass, anchor, budgets, budget, c_max, idx, counts, votes,
+                       workspace, workspace_bytes, stream, kSelectTau | kSelectVote | kSelectPick);
+}
+
+int mmshiftkv_select_tau(const mmskv_shape* shape, const mmskv_params* params, const float* group_mass,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+    return select_call(shape, params, group_mass, nullptr, nullptr, nullptr, 0, 0, nullptr, nullptr, nullptr,
+                       workspace, workspace_bytes, stream, kSelectTau);
+}
+
+int mmshiftkv_select_vote(const mmskv_shape* shape, const mmskv_params* params, const float* mass,
+                          const float* anchor, uint8_t* votes, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+    return select_call(shape, params, nullptr, mass, anchor, nullptr, 0, 0, nullptr, nullptr, votes, workspace,
+                       workspace_bytes, stream, kSelectVote);
+}
+
+int mmshiftkv_select_pick(const mmskv_shape* shape, const mmskv_params* params, const int32_t* budgets,
+                          int32_t budget, int32_t c_max, int32_t* idx, int32_t* counts, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    return select_call(shape, params, nullptr, nullptr, nullptr, budgets, budget, c_max, idx, counts, nullptr,
+                       workspace, workspace_bytes, stream, kSelectPick);
 }
 
 int mmshiftkv_gather_kv(const mmskv_shape* shape, const void* k, const void* v, int32_t dtype,

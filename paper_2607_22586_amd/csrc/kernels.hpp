@@ -155,7 +155,10 @@ int decode_max_compact();
 hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s);
 hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s);
 hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s);
-hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+// Selection stages: tau cuts and membership planes (VOTE) or clearing the
+// first-digit counts (MASS); votes, scores and first-digit counts; top-k.
+constexpr int kSelectTau = 1, kSelectVote = 2, kSelectPick = 4;
+hipError_t launch_select(const SelectArgs& a, int stages, hipStream_t s);
 // Keys per thread of the register-resident top-k for T keys (0: the sweep
 // kernel), and the per-head stride of the score keys it implies.
 int select_kpt(int T);

@@ -673,40 +673,48 @@ int select_kpt(int T) {
     return per <= 4 ? 4 : per <= 8 ? 8 : per <= 16 ? 16 : per <= 32 ? 32 : 0;
 }
 
-hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+hipError_t launch_select(const SelectArgs& a, int stages, hipStream_t s) {
     if (a.kpt != select_kpt(a.T) || a.key_stride != select_key_stride(a.T)) return hipErrorInvalidValue;
-    if (a.mode == 0) {
-        // register-resident tau cut while a row fits in 32 masses per thread of 512
-        dim3 g1(a.G, a.Hkv, a.B);
-        const int tper = (a.T + kTauThreads - 1) / kTauThreads;
-        const int tkpt = tper <= 8 ? 8 : tper <= 16 ? 16 : tper <= 32 ? 32 : 0;
-        switch (tkpt) {
-            case 8: hipLaunchKernelGGL(tau_cut_reg_kernel<8>, g1, dim3(kTauThreads), 0, s, a); break;
-            case 16: hipLaunchKernelGGL(tau_cut_reg_kernel<16>, g1, dim3(kTauThreads), 0, s, a); break;
-            case 32: hipLaunchKernelGGL(tau_cut_reg_kernel<32>, g1, dim3(kTauThreads), 0, s, a); break;
-            default: hipLaunchKernelGGL(tau_cut_kernel, g1, dim3(kSelThreads), 0, s, a); break;
+    hipError_t e = hipSuccess;
+    if (stages & kSelectTau) {
+        if (a.mode == 0) {
+            // register-resident tau cut while a row fits in 32 masses per thread of 512
+            dim3 g1(a.G, a.Hkv, a.B);
+            const int tper = (a.T + kTauThreads - 1) / kTauThreads;
+            const int tkpt = tper <= 8 ? 8 : tper <= 16 ? 16 : tper <= 32 ? 32 : 0;
+            switch (tkpt) {
+                case 8: hipLaunchKernelGGL(tau_cut_reg_kernel<8>, g1, dim3(kTauThreads), 0, s, a); break;
+                case 16: hipLaunchKernelGGL(tau_cut_reg_kernel<16>, g1, dim3(kTauThreads), 0, s, a); break;
+                case 32: hipLaunchKernelGGL(tau_cut_reg_kernel<32>, g1, dim3(kTauThreads), 0, s, a); break;
+                default: hipLaunchKernelGGL(tau_cut_kernel, g1, dim3(kSelThreads), 0, s, a); break;
+            }
+        } else {
+            const int64_t n = static_cast<int64_t>(a.B) * a.Hkv * 2048;
+            const int64_t blocks = (n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024;
+            hipLaunchKernelGGL(clear_hist0_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
         }
-    } else {
-        const int64_t n = static_cast<int64_t>(a.B) * a.Hkv * 2048;
-        hipLaunchKernelGGL(clear_hist0_kernel, dim3(static_cast<unsigned>((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024)),
-                           dim3(256), 0, s, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int nw = (a.T + 31) / 32;
-    dim3 g2((nw + kVoteWords - 1) / kVoteWords, a.Hkv, a.B);
-    hipLaunchKernelGGL(vote_score_kernel, g2, dim3(kVoteThreads), 0, s, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    dim3 g3(a.Hkv, a.B);
-    switch (a.kpt) {
-        case 4: hipLaunchKernelGGL(topk_reg_kernel<4>, g3, dim3(kSelThreads), 0, s, a); break;
-        case 8: hipLaunchKernelGGL(topk_reg_kernel<8>, g3, dim3(kSelThreads), 0, s, a); break;
-        case 16: hipLaunchKernelGGL(topk_reg_kernel<16>, g3, dim3(kSelThreads), 0, s, a); break;
-        case 32: hipLaunchKernelGGL(topk_reg_kernel<32>, g3, dim3(kSelThreads), 0, s, a); break;
-        default: hipLaunchKernelGGL(topk_kernel, g3, dim3(kSelThreads), 0, s, a); break;
+    if (stages & kSelectVote) {
+        const int nw = (a.T + 31) / 32;
+        dim3 g2((nw + kVoteWords - 1) / kVoteWords, a.Hkv, a.B);
+        hipLaunchKernelGGL(vote_score_kernel, g2, dim3(kVoteThreads), 0, s, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    return hipGetLastError();
+    if (stages & kSelectPick) {
+        dim3 g3(a.Hkv, a.B);
+        switch (a.kpt) {
+            case 4: hipLaunchKernelGGL(topk_reg_kernel<4>, g3, dim3(kSelThreads), 0, s, a); break;
+            case 8: hipLaunchKernelGGL(topk_reg_kernel<8>, g3, dim3(kSelThreads), 0, s, a); break;
+            case 16: hipLaunchKernelGGL(topk_reg_kernel<16>, g3, dim3(kSelThreads), 0, s, a); break;
+            case 32: hipLaunchKernelGGL(topk_reg_kernel<32>, g3, dim3(kSelThreads), 0, s, a); break;
+            default: hipLaunchKernelGGL(topk_kernel, g3, dim3(kSelThreads), 0, s, a); break;
+        }
+        e = hipGetLastError();
+    }
+    return e;
 }
 
 }  // namespace mmskv

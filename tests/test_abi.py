@@ -173,6 +173,26 @@ def test_select_rejects(lib):
     assert call(64, 64, votes=FAKE, prm=_params(mode=bd.MMSKV_MASS)) == bd.MMSKV_EINVAL
 
 
+def test_select_stages_reject(lib):
+    """Each stage call checks the arguments it reads (and only those): the
+    calls below stop at argument or workspace checks, before any launch."""
+    s, p = _shape(), _params()
+    pm = _params(mode=bd.MMSKV_MASS)
+    need = lib.mmshiftkv_select_workspace(ctypes.byref(s), ctypes.byref(p))
+    S, P, PM = ctypes.byref(s), ctypes.byref(p), ctypes.byref(pm)
+    assert lib.mmshiftkv_select_tau(S, P, None, FAKE, need, None) == bd.MMSKV_EINVAL          # VOTE needs masses
+    assert lib.mmshiftkv_select_tau(S, P, FAKE, FAKE, need - 8, None) == bd.MMSKV_EWORKSPACE
+    assert lib.mmshiftkv_select_tau(S, PM, None, None, need, None) == bd.MMSKV_EWORKSPACE     # MASS: none read
+    assert lib.mmshiftkv_select_vote(S, P, FAKE, None, None, FAKE, need, None) == bd.MMSKV_EINVAL   # no anchor
+    assert lib.mmshiftkv_select_vote(S, PM, None, FAKE, None, FAKE, need, None) == bd.MMSKV_EINVAL  # no mass
+    assert lib.mmshiftkv_select_vote(S, PM, FAKE, None, FAKE, FAKE, need, None) == bd.MMSKV_EINVAL  # votes
+    assert lib.mmshiftkv_select_vote(S, P, None, FAKE, FAKE, FAKE, need - 8, None) == bd.MMSKV_EWORKSPACE
+    assert lib.mmshiftkv_select_pick(S, P, None, 0, 64, FAKE, FAKE, FAKE, need, None) == bd.MMSKV_EINVAL
+    assert lib.mmshiftkv_select_pick(S, P, None, 64, 63, FAKE, FAKE, FAKE, need, None) == bd.MMSKV_EINVAL
+    assert lib.mmshiftkv_select_pick(S, P, None, 64, 64, None, FAKE, FAKE, need, None) == bd.MMSKV_EINVAL
+    assert lib.mmshiftkv_select_pick(S, P, None, 64, 64, FAKE, FAKE, FAKE, need - 8, None) == bd.MMSKV_EWORKSPACE
+
+
 def test_select_ignores_window_and_head_dim(lib):
     """The selection reads B, Hq, Hkv, T and the method parameters only: W = 0,
     d = 0 and a gamma / ddof the proxy call would refuse still pass its

@@ -170,3 +170,31 @@ def test_dense_wq_hidden_path_scores_and_selection():
                     else val[b:b + 1, c * Gh:(c + 1) * Gh]) for key, val in g.items()}
         rep = parity.check_layer(gh, ref, cfg, w.budget, k1, v1)
         print("dense W_Q", (b, c), rep, flush=True)
+
+
+@pytest.mark.parametrize("mode", ["vote", "mass"])
+@pytest.mark.parametrize("T", [16384, 3001, 40000])
+def test_select_stage_calls_equal_whole_call(T, mode):
+    """mmshiftkv_select_tau, _vote and _pick in order give exactly what
+    mmshiftkv_select_topk gives (register and sweep paths, both modes)."""
+    print("case select stages", T, mode, flush=True)
+    dev = torch.device(DEV)
+    m = bd.MMSKV_MASS if mode == "mass" else bd.MMSKV_VOTE
+    cfg = bd.SelectionConfig(P=64, G=4, seed=T + m, mode=m)
+    B, Hkv, Gh, d, W = 2, 2, 2, 64, 16
+    torch.manual_seed(T)
+    q = torch.randn(B, Hkv * Gh, W, d, device=dev).to(torch.bfloat16)
+    k = torch.randn(B, Hkv, T, d, device=dev).to(torch.bfloat16)
+    prox, ql = bd.build_proxies(q, cfg, T, Hkv)
+    sc = bd.score(prox, ql, k, cfg, W)
+    whole = bd.select_topk(sc, cfg, 200, Hq=Hkv * Gh, W=W, want_votes=(m == bd.MMSKV_VOTE))
+    ws = torch.empty(bd.select_workspace(B, Hkv * Gh, Hkv, T, W, d, cfg), dtype=torch.uint8, device=dev)
+    out = bd.Selected(torch.full_like(whole.idx, -7), torch.full_like(whole.counts, -7),
+                      None if whole.votes is None else torch.full_like(whole.votes, 99))
+    for stg in ("tau", "vote", "pick"):
+        bd.select_topk(sc, cfg, 200, Hq=Hkv * Gh, W=W, out=out, workspace=ws, stage=stg)
+    torch.cuda.synchronize()
+    assert torch.equal(out.idx, whole.idx)
+    assert torch.equal(out.counts, whole.counts)
+    if whole.votes is not None:
+        assert torch.equal(out.votes, whole.votes)
