@@ -39,6 +39,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+SPIN_CYCLES = 20_000_000      # GPU spin ahead of the stage timings (several ms)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_score_qwen7b_16k_b4.json")
 SCORE_SRC = os.path.join(ROOT, "paper_2607_22586_amd", "csrc", "score.hip")
 
@@ -532,8 +533,9 @@ def main():
     log("kernel timing on one stream: score_lse %.1f us, score_mass %.1f us per layer" % (lse_ms * 1e3, mass_ms * 1e3))
 
     # the other stages: each C-ABI call repeated back to back on one stream
-    # (layer 0's inputs, the buffers of stream 0), so the time per call is
-    # its kernels plus the launch gaps between calls
+    # (layer 0's inputs, the buffers of stream 0) behind a GPU-side spin long
+    # enough for the host to queue all of them, so the time per call is its
+    # kernels plus the launch gaps between them (not the host's call cost)
     x, c, bf = layers[0], cfgs[0], bufs[0]
     sel_args = (bf["sc"], c, w.budget, w.budget, None, Hq, W)
     calls = {
@@ -554,11 +556,20 @@ def main():
                 calls["select_vote"]()
             fn()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            es = torch.cuda.Event(enable_timing=True)
+            es.record(stream)
+            torch.cuda._sleep(SPIN_CYCLES)
             e0.record(stream)
+            h0 = time.perf_counter()
             for _ in range(reps):
                 fn()
+            host_ms = (time.perf_counter() - h0) * 1e3
             e1.record(stream)
             torch.cuda.synchronize()
+            spin_ms = es.elapsed_time(e0)
+            if host_ms > spin_ms:
+                log("warning: queuing %s took %.2f ms, longer than the %.2f ms spin: its time includes host "
+                    "call cost" % (name, host_ms, spin_ms))
             stage_ms[name] = e0.elapsed_time(e1) / reps
         # leave layer 0's selection as a whole call made it
         bd.select_topk(*sel_args, out=bf["sel"], workspace=bf["ws_sel"])
@@ -611,7 +622,8 @@ def main():
                    "lambda": cfg.lam, "mode": args.mode, "streams": n_streams},
         "stages_us_per_layer": {k: v * 1e3 for k, v in stage_ms.items()},
         "stages_timing": "score passes: events around them in %d steps on one stream; the rest: %d back-to-back "
-                         "calls of one stage on one stream (kernels + launch gaps)" % (args.steps, reps),
+                         "calls of one stage on one stream, queued behind a GPU spin (kernels + launch gaps)"
+                         % (args.steps, reps),
         "non_score_us_per_layer": sum(v for k, v in stage_ms.items() if not k.startswith("score_")) * 1e3,
         "stage_hbm_frac": {k: stage_bytes[k] / (stage_ms[k] * 1e-3) / 1e9 / PEAK_HBM_GBS for k in stage_bytes},
         "roofline": {"kernel": dom + " pass", "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,

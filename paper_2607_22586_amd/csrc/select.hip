@@ -10,7 +10,7 @@
 //           (mass desc, index asc) prefix whose mass reaches tau * total.
 //           Masses are summed as integers in units of 2^-S (converted from
 //           the float bits exactly), so every decision is independent of
-//           summation order.  The register-resident variant (T <= 16384)
+//           summation order.  The register-resident variant (T <= 32768)
 //           stops its passes early once the crossing bucket holds one key;
 //           the sweep variant always runs all three.  Both end by writing
 //           the group's membership plane: one bit per key, 32 keys a word.
@@ -33,7 +33,6 @@ namespace {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kTauThreads = 512;                 // register-resident tau cut
-constexpr int kTauWaves = kTauThreads / kWave;
 
 // floor(m * 2^S) for the finite, non-negative float with bit pattern `bits`,
 // computed exactly from the significand and exponent (the product m * 2^S
@@ -459,21 +458,23 @@ __global__ void __launch_bounds__(kSelThreads) topk_kernel(SelectArgs a) {
 // is read from memory once and every index-ordered step (ties, compaction)
 // needs one block scan instead of a sweep.
 
-// tau cut of one (b, c, group); same result as tau_cut_kernel.  512 threads
-// of at most 128 VGPRs, so two workgroups share a CU and a whole launch of
-// 512 workgroups is resident at once.  Thread i holds keys
+// tau cut of one (b, c, group); same result as tau_cut_kernel.  NT threads
+// (512 up to T = 16384, so two workgroups share a CU and a launch of 512
+// workgroups is resident at once; 1024 up to T = 32768) of at most 128
+// VGPRs.  Thread i holds keys
 // 2048 q + 4 i + e (q < KPT / 4, e < 4), so every load is one contiguous
 // 16-byte piece per lane; the index-ordered steps (ties, the plane) go
 // through the 2048-key chunks q in order.
-template <int KPT>
-__global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) {
+template <int KPT, int NT>
+__global__ void __launch_bounds__(NT) tau_cut_reg_kernel(SelectArgs a) {
     static_assert(KPT % 4 == 0, "whole 4-key pieces per thread");
     constexpr int kQ = KPT / 4;
-    constexpr int kChunk = 4 * kTauThreads;
+    constexpr int kChunk = 4 * NT;
+    constexpr int kW = NT / kWave;
     __shared__ uint32_t cnt[2048];
     __shared__ unsigned long long sum[2048];
-    __shared__ unsigned long long wtot64[kTauWaves];
-    __shared__ uint32_t wtot[kTauWaves];
+    __shared__ unsigned long long wtot64[kW];
+    __shared__ uint32_t wtot[kW];
     __shared__ uint32_t s_digit, s_cnt;
     __shared__ unsigned long long s_rem;
     __shared__ int32_t s_tcut;
@@ -507,7 +508,7 @@ __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) 
     uint64_t local = 0;
 #pragma unroll
     for (int j = 0; j < KPT; ++j) local += fixed_of(mb[j], S);
-    const uint64_t total = block_sum_u64<kTauThreads>(local, wtot64);
+    const uint64_t total = block_sum_u64<NT>(local, wtot64);
     // every mass below the fixed-point resolution: empty set
     uint32_t theta = 0xFFFFFFFFu;
     int32_t tcut = -1;
@@ -520,7 +521,7 @@ __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) 
 #pragma nounroll
         for (int pass = 0; pass < 3; ++pass) {
             const uint32_t mask = tau_mask(pass);
-            for (int i = tid; i < 2048; i += kTauThreads) { cnt[i] = 0; sum[i] = 0; }
+            for (int i = tid; i < 2048; i += NT) { cnt[i] = 0; sum[i] = 0; }
             __syncthreads();
 #pragma unroll
             for (int j = 0; j < KPT; ++j) {
@@ -534,7 +535,7 @@ __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) 
                 }
             }
             __syncthreads();
-            descending_crossing<unsigned long long, kTauThreads>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
+            descending_crossing<unsigned long long, NT>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
             prefix |= s_digit << tau_shift(pass);
             need = s_rem;
             if (pass < 2 && s_cnt == 1u) {
@@ -563,7 +564,7 @@ __global__ void __launch_bounds__(kTauThreads) tau_cut_reg_kernel(SelectArgs a) 
 #pragma unroll
                 for (int e = 0; e < 4; ++e) n_eq += (key_of(q, e) < a.T && mb[4 * q + e] == prefix) ? 1u : 0u;
                 uint32_t tot;
-                const uint32_t before = block_excl_scan<uint32_t, kTauThreads>(n_eq, wtot, tot);
+                const uint32_t before = block_excl_scan<uint32_t, NT>(n_eq, wtot, tot);
                 if (seen + before < k_eq && k_eq <= seen + before + n_eq) {
                     uint64_t at = seen + before;
 #pragma unroll
@@ -678,14 +679,16 @@ hipError_t launch_select(const SelectArgs& a, int stages, hipStream_t s) {
     hipError_t e = hipSuccess;
     if (stages & kSelectTau) {
         if (a.mode == 0) {
-            // register-resident tau cut while a row fits in 32 masses per thread of 512
+            // register-resident tau cut while a row fits in 32 masses per
+            // thread of 512, then of 1024; the sweep kernel beyond
             dim3 g1(a.G, a.Hkv, a.B);
             const int tper = (a.T + kTauThreads - 1) / kTauThreads;
-            const int tkpt = tper <= 8 ? 8 : tper <= 16 ? 16 : tper <= 32 ? 32 : 0;
+            const int tkpt = tper <= 8 ? 8 : tper <= 16 ? 16 : tper <= 32 ? 32 : tper <= 64 ? 64 : 0;
             switch (tkpt) {
-                case 8: hipLaunchKernelGGL(tau_cut_reg_kernel<8>, g1, dim3(kTauThreads), 0, s, a); break;
-                case 16: hipLaunchKernelGGL(tau_cut_reg_kernel<16>, g1, dim3(kTauThreads), 0, s, a); break;
-                case 32: hipLaunchKernelGGL(tau_cut_reg_kernel<32>, g1, dim3(kTauThreads), 0, s, a); break;
+                case 8: hipLaunchKernelGGL((tau_cut_reg_kernel<8, kTauThreads>), g1, dim3(kTauThreads), 0, s, a); break;
+                case 16: hipLaunchKernelGGL((tau_cut_reg_kernel<16, kTauThreads>), g1, dim3(kTauThreads), 0, s, a); break;
+                case 32: hipLaunchKernelGGL((tau_cut_reg_kernel<32, kTauThreads>), g1, dim3(kTauThreads), 0, s, a); break;
+                case 64: hipLaunchKernelGGL((tau_cut_reg_kernel<32, kSelThreads>), g1, dim3(kSelThreads), 0, s, a); break;
                 default: hipLaunchKernelGGL(tau_cut_kernel, g1, dim3(kSelThreads), 0, s, a); break;
             }
         } else {

@@ -61,10 +61,12 @@ def oracle_layer(x, cfg, budget):
     return ref, k, v
 
 
-@pytest.mark.parametrize("T,Hq,budget,mode", [(20001, 4, 300, bd.MMSKV_VOTE), (40000, 2, 500, bd.MMSKV_VOTE),
-                                              (40000, 2, 123, bd.MMSKV_MASS)])
+@pytest.mark.parametrize("T,Hq,budget,mode", [(20001, 4, 300, bd.MMSKV_VOTE), (32768, 2, 700, bd.MMSKV_VOTE),
+                                              (40000, 2, 500, bd.MMSKV_VOTE), (40000, 2, 123, bd.MMSKV_MASS)])
 def test_long_rows_sweep_paths(T, Hq, budget, mode):
-    """T > 16384 takes the sweep tau cut, T > 32768 the global top-k."""
+    """16384 < T <= 32768 takes the 1024-thread register tau cut (ragged at
+    T = 20001, full at 32768), T > 32768 the sweep tau cut and the global
+    top-k."""
     print("case long rows", T, Hq, budget, mode, flush=True)
     x = wl.custom_layer(1, Hq, 1, T, 8, 64, seed=T + budget)
     cfg = bd.SelectionConfig(P=64, G=4, seed=T, mode=mode)
