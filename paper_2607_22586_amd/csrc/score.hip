@@ -2,21 +2,23 @@
 // Sec. 3.2.3 Eq. 11 anchor, Appendix B GQA aggregation) on gfx950.
 //
 // Work decomposition.  A workgroup of WAVES waves owns one (batch row b,
-// KV head c) and a block of 64*WAVES prompt keys; each wave keeps its 64 keys
-// resident in registers as bf16 MFMA fragments for the whole kernel.  Every
-// proxy row of the Gh query heads that share KV head c (then the anchor
-// rows) streams past those keys in 32-row tiles: the workgroup stages each
-// tile once in LDS (double buffered, XOR-swizzled 16-byte chunks so the
-// fragment reads are bank-conflict free) and every wave multiplies it with
-// v_mfma_f32_32x32x16_bf16 (fp32 accumulation).  Within a wave the MFMAs of
-// tile t are issued alongside the exp/reduction VALU work of tile t-1, which
-// keeps both the matrix pipe and the VALU busy.  No logit reaches memory.
+// KV head c) and a block of prompt keys; each wave keeps its keys (32*NS in
+// pass 1, 64 in pass 2) resident in registers as bf16 MFMA fragments for
+// the whole kernel.  Every proxy row of the Gh query heads that share KV
+// head c (then the anchor rows) streams past those keys in 32-row tiles:
+// the workgroup stages each tile once in a 4-slot LDS ring (rows padded by
+// one 16-byte chunk so the fragment reads are bank-conflict free) and every
+// wave multiplies it with v_mfma_f32_32x32x16_bf16 (fp32 accumulation).
+// Within a wave the MFMAs of one tile (or chain) are issued alongside the
+// exp/reduction VALU work of the previous one, so the matrix pipe and the
+// VALU work side by side.  No logit reaches memory.
 //
 // An exact column mass needs every row's full normaliser, so the keys are
 // scored twice:
-//   score_lse:  D = K * P^T (keys as rows).  Per proxy row: max and
-//               sum 2^(s - max) over the wave's keys (in-lane, then one
-//               cross-lane step), merged over the waves through LDS into one
+//   score_lse:  D = K * P^T (keys as rows).  Per proxy row: the sum of 2^s
+//               over the wave's keys, relative to zero while it stays in a
+//               safe range and relative to the exact maximum otherwise,
+//               merged over the waves through LDS into one (max, sum)
 //               partial per (row, key block); lse_combine folds the partials
 //               into L_row = log2 sum_t 2^(s_t).
 //   score_mass: D = P * K^T (proxies as rows).  p = 2^(s - L_row);
