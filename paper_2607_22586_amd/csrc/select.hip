@@ -99,7 +99,7 @@ __device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* wtot, 
 
 // Block-wide exclusive prefix sum of `v` over the NT threads in thread
 // order; also returns the block total.
-template <typename U, int NT = kSelThreads>
+template <typename U, int NT = kSelThreads, bool kFence = true>
 __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
     constexpr int kW = NT / kWave;
     const int lane = lane_id(), wave = static_cast<int>(threadIdx.x) / kWave;
@@ -113,7 +113,8 @@ __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
         before += (w < wave) ? t : U(0);
         tot += t;
     }
-    __syncthreads();
+    // without kFence the caller puts a barrier before wtot is written again
+    if (kFence) __syncthreads();
     total = tot;
     return before + x - v;
 }
@@ -136,7 +137,7 @@ __device__ __forceinline__ void descending_crossing(const U* val, const uint32_t
         mine += v[k];
     }
     U total;
-    U excl = block_excl_scan<U, NT>(mine, wtot, total);
+    U excl = block_excl_scan<U, NT, false>(mine, wtot, total);   // the barrier below guards wtot
     if (excl < need && need <= excl + mine) {
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
@@ -358,7 +359,7 @@ __global__ void __launch_bounds__(256) clear_hist0_kernel(SelectArgs a) {
 // keys (by index) with key == theta.  Requires 1 <= want < pool size.  The
 // first pass takes its counts from h0 (all pool keys by bits 63..53).
 struct TopkShared {
-    uint32_t cnt[2048];
+    uint32_t cnt[2][2048];       // pass p counts into cnt[p % 2]
     uint32_t wtot[kSelWaves];
     uint32_t s_digit, s_cnt, s_rem;
 };
@@ -369,21 +370,27 @@ __device__ __forceinline__ void topk_threshold(uint32_t want, Each each, const u
     const int tid = threadIdx.x;
     uint64_t prefix = 0, mask = 0;
     uint32_t need = want;
+    // the first digit's counts, made by the vote kernel; the other buffer
+    // cleared for the second pass
+    for (int i = tid; i < 2048; i += kSelThreads) {
+        sh.cnt[0][i] = h0[i];
+        sh.cnt[1][i] = 0;
+    }
+    __syncthreads();
     for (int pass = 0; pass < 6; ++pass) {
         const int shift = pass == 5 ? 0 : 53 - 11 * pass;
-        if (pass == 0) {
-            // the first digit's counts, made by the vote kernel
-            for (int i = tid; i < 2048; i += kSelThreads) sh.cnt[i] = h0[i];
-        } else {
-            for (int i = tid; i < 2048; i += kSelThreads) sh.cnt[i] = 0;
-            __syncthreads();
+        uint32_t* cnt = sh.cnt[pass & 1];
+        if (pass > 0) {
             // plain LDS atomics over the keys left in the crossing bucket
             each([&](uint64_t kv, bool ok) {
-                if (ok && (kv & mask) == prefix) atomicAdd(&sh.cnt[static_cast<uint32_t>(kv >> shift) & 2047u], 1u);
+                if (ok && (kv & mask) == prefix) atomicAdd(&cnt[static_cast<uint32_t>(kv >> shift) & 2047u], 1u);
             });
+            __syncthreads();
         }
-        __syncthreads();
-        descending_crossing<uint32_t>(sh.cnt, sh.cnt, need, sh.wtot, &sh.s_digit, &sh.s_rem, &sh.s_cnt);
+        descending_crossing<uint32_t>(cnt, cnt, need, sh.wtot, &sh.s_digit, &sh.s_rem, &sh.s_cnt);
+        // every read of this buffer is done (the crossing ends with a
+        // barrier): clear it for pass + 2, two barriers away
+        for (int i = tid; i < 2048; i += kSelThreads) cnt[i] = 0;
         prefix |= static_cast<uint64_t>(sh.s_digit) << shift;
         mask |= (shift == 0 ? 0x1FFull : 0x7FFull) << shift;
         need = sh.s_rem;
@@ -634,8 +641,8 @@ __global__ void __launch_bounds__(kSelThreads) topk_reg_kernel(SelectArgs a) {
     uint32_t n_eq = 0;
 #pragma unroll
     for (int j = 0; j < KPT; ++j) n_eq += (want > 0 && k_eq > 0 && t0 + j < pool && kv[j] == theta) ? 1u : 0u;
-    uint32_t eq_total;
-    uint32_t eq_seen = block_excl_scan<uint32_t>(n_eq, sh.wtot, eq_total);
+    uint32_t eq_total = 0, eq_seen = 0;
+    if (want > 0 && k_eq > 0) eq_seen = block_excl_scan<uint32_t>(n_eq, sh.wtot, eq_total);
     uint32_t sel_mask = 0, n_sel = 0;
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
