@@ -47,6 +47,28 @@ __device__ __forceinline__ uint64_t fixed_of(uint32_t bits, int S) {
     return man >> (-sh);
 }
 
+// The fixed-point value floor(m * 2^S) of a non-negative float m = man *
+// 2^(e' - 150) (e' = max(e, 1), man with the implicit bit when e > 0) is
+// man << sh for sh = e' - 150 + S >= 0 and man >> -sh otherwise.  Every key
+// in one bucket of the tau-cut passes has the same exponent (the first digit
+// holds the exponent bits, the later passes keep them in the prefix), so a
+// bucket can sum mant_part(bits) = man >> max(-sh, 0) (under 2^24) and take
+// the common factor 2^max(sh, 0) once: bucket_fixed(sum, e) is then exactly
+// the sum of fixed_of over the bucket.
+__device__ __forceinline__ int fixed_shift(uint32_t e, int S) {
+    return (e != 0 ? static_cast<int>(e) : 1) - 150 + S;
+}
+__device__ __forceinline__ uint32_t mant_part(uint32_t bits, int S) {
+    const uint32_t e = bits >> 23;           // sign bit is 0
+    const uint32_t man = (bits & 0x7FFFFFu) | (e != 0 ? 0x800000u : 0u);
+    const int rs = -fixed_shift(e, S);
+    return rs <= 0 ? man : (rs >= 24 ? 0u : man >> rs);
+}
+__device__ __forceinline__ uint64_t bucket_fixed(uint64_t sum, uint32_t e, int S) {
+    const int sh = fixed_shift(e, S);
+    return sh > 0 ? sum << min(sh, 63) : sum;   // sh stays below 40 for any non-empty bucket
+}
+
 // Adds (count 1, value f) of every active lane to bucket `digit`, combining
 // lanes of the wave that share a digit (skewed digit distributions would
 // otherwise serialise on one LDS address).
@@ -120,24 +142,27 @@ __device__ __forceinline__ U block_excl_scan(U v, U* wtot, U& total) {
 }
 
 // Digits [0, 2048) visited in descending order, thread i of NT covering the
-// 2048/NT digits below 2048 - (2048/NT)*i: finds the digit whose bucket
-// takes the running total (from the top) to `need` (need >= 1, need <=
-// total).  Returns, through shared memory, the digit, `need` minus the total
-// of higher buckets, and the bucket's count (when `cnt` is given).
-template <typename U, int NT = kSelThreads>
-__device__ __forceinline__ void descending_crossing(const U* val, const uint32_t* cnt, U need, U* wtot,
-                                                    uint32_t* s_digit, U* s_rem, uint32_t* s_cnt) {
+// 2048/NT digits below 2048 - (2048/NT)*i, bucket d holding val_of(d): finds
+// the digit whose bucket takes the running total (from the top) to need =
+// need_of(total of all buckets) (1 <= need <= total; no digit when need is
+// 0).  Returns the total; writes, through shared memory, the digit, `need`
+// minus the total of higher buckets, and the bucket's count (when `cnt` is
+// given).
+template <typename U, int NT, typename ValOf, typename NeedOf>
+__device__ __forceinline__ U crossing_of(ValOf val_of, const uint32_t* cnt, NeedOf need_of, U* wtot,
+                                         uint32_t* s_digit, U* s_rem, uint32_t* s_cnt) {
     constexpr int kPer = 2048 / NT;
     const int top = 2047 - kPer * static_cast<int>(threadIdx.x);
     U v[kPer];
     U mine = 0;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-        v[k] = val[top - k];
+        v[k] = val_of(top - k);
         mine += v[k];
     }
     U total;
     U excl = block_excl_scan<U, NT, false>(mine, wtot, total);   // the barrier below guards wtot
+    const U need = need_of(total);
     if (excl < need && need <= excl + mine) {
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
@@ -150,6 +175,14 @@ __device__ __forceinline__ void descending_crossing(const U* val, const uint32_t
         }
     }
     __syncthreads();
+    return total;
+}
+
+template <typename U, int NT = kSelThreads>
+__device__ __forceinline__ void descending_crossing(const U* val, const uint32_t* cnt, U need, U* wtot,
+                                                    uint32_t* s_digit, U* s_rem, uint32_t* s_cnt) {
+    crossing_of<U, NT>([val](int d) { return val[d]; }, cnt, [need](U) { return need; }, wtot, s_digit, s_rem,
+                       s_cnt);
 }
 
 template <int NT = kSelThreads>
@@ -512,19 +545,13 @@ __global__ void __launch_bounds__(NT) tau_cut_reg_kernel(SelectArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) mb[4 * q + e] = key_of(q, e) < a.T ? m[key_of(q, e)] : 0u;
     }
-    uint64_t local = 0;
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) local += fixed_of(mb[j], S);
-    const uint64_t total = block_sum_u64<NT>(local, wtot64);
     // every mass below the fixed-point resolution: empty set
     uint32_t theta = 0xFFFFFFFFu;
     int32_t tcut = -1;
-    if (total != 0) {
-        unsigned long long need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(total)));
-        if (need < 1) need = 1;
-        if (need > total) need = total;
-
-        uint32_t prefix = 0;
+    unsigned long long need = 0;
+    uint32_t prefix = 0;
+    bool found = true;
+    {
 #pragma nounroll
         for (int pass = 0; pass < 3; ++pass) {
             const uint32_t mask = tau_mask(pass);
@@ -532,17 +559,39 @@ __global__ void __launch_bounds__(NT) tau_cut_reg_kernel(SelectArgs a) {
             __syncthreads();
 #pragma unroll
             for (int j = 0; j < KPT; ++j) {
-                // opaque inside the pass loop, so the fixed-point values are not
+                // opaque inside the pass loop, so the per-key values are not
                 // hoisted out of it and kept live
                 asm volatile("" : "+v"(mb[j]));
                 if (key_of(j / 4, j % 4) < a.T && (mb[j] & mask) == prefix) {
                     const uint32_t dg = tau_digit(mb[j], pass);
                     atomicAdd(&cnt[dg], 1u);
-                    atomicAdd(&sum[dg], static_cast<unsigned long long>(fixed_of(mb[j], S)));
+                    atomicAdd(&sum[dg], static_cast<unsigned long long>(mant_part(mb[j], S)));
                 }
             }
             __syncthreads();
-            descending_crossing<unsigned long long, NT>(sum, cnt, need, wtot64, &s_digit, &s_rem, &s_cnt);
+            // bucket d's exponent: the digit's top 8 bits in the first pass,
+            // the prefix's in the later ones
+            const uint32_t e_pre = prefix >> 23;
+            const unsigned long long total = crossing_of<unsigned long long, NT>(
+                [&](int d) {
+                    return static_cast<unsigned long long>(
+                        bucket_fixed(sum[d], pass == 0 ? static_cast<uint32_t>(d) >> 3 : e_pre, S));
+                },
+                cnt,
+                [&](unsigned long long tot) {
+                    if (pass == 0) {
+                        // the shortest prefix reaching tau * total (at least one key)
+                        need = static_cast<unsigned long long>(ceil(a.tau * static_cast<double>(tot)));
+                        if (need < 1) need = 1;
+                        if (need > tot) need = tot;
+                    }
+                    return need;
+                },
+                wtot64, &s_digit, &s_rem, &s_cnt);
+            if (pass == 0 && total == 0) {
+                found = false;
+                break;
+            }
             prefix |= s_digit << tau_shift(pass);
             need = s_rem;
             if (pass < 2 && s_cnt == 1u) {
@@ -556,6 +605,8 @@ __global__ void __launch_bounds__(NT) tau_cut_reg_kernel(SelectArgs a) {
                 break;
             }
         }
+    }
+    if (found) {
         theta = prefix;
         const uint64_t f_theta = fixed_of(prefix, S);
         const uint64_t k_eq = f_theta == 0 ? 1 : (need + f_theta - 1) / f_theta;
