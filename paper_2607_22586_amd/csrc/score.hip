@@ -621,7 +621,10 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     bf16x8 A[D / 16];
     read_frags<D>(stage[0], A, lane);
     TileCursor mm{0, 0, 0};                  // tile whose accumulator start is read next
-    floatx16 Cn = row_offsets(Llds + tile_row(mm), lane);
+    // accumulator starts of tiles t (set t % 2) and t + 1: read one tile ahead
+    // into the other set, so none is copied
+    floatx16 Cn[2];
+    Cn[0] = row_offsets(Llds + tile_row(mm), lane);
     mm.advance(a.Gh);
 
     const int64_t gm_base = static_cast<int64_t>(head) * a.G * a.T;
@@ -676,7 +679,6 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
         constexpr int cur = T4 & 1, prev = cur ^ 1;
         const u32x4* next = stage[(T4 + 1) % kRing];
         const bool mfma_on = FAST || t < n_prox;
-        floatx16 Cnext;
         float ev[kPer32];
         auto add_group = [&](int g) {
 #pragma unroll
@@ -697,7 +699,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
 #pragma unroll
             for (int s = 0; s < kSub; ++s) {
                 const int slot = kSub * kc + s;
-                if (mfma_on) acc[cur][s] = mfma32(A[kc], kf[s][kc], kc == 0 ? Cn : acc[cur][s]);
+                if (mfma_on) acc[cur][s] = mfma32(A[kc], kf[s][kc], kc == 0 ? Cn[cur] : acc[cur][s]);
                 if (PROBS) {
                     if (slot >= 1) add_group(slot - 1);
                     exp_group(slot);
@@ -707,8 +709,21 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
             if (mfma_on) A[kc] = lds_frag<D>(next, lane & 31, 2 * kc + (lane >> 5));
             if (kc == D / 32) {
                 // accumulator start of tile t+1 (a valid row block even past the end)
-                Cnext = row_offsets(Llds + ((FAST || mm.t < n_prox) ? tile_row(mm) : 0), lane);
+                Cn[prev] = row_offsets(Llds + ((FAST || mm.t < n_prox) ? tile_row(mm) : 0), lane);
                 mm.advance(a.Gh);
+            }
+            if (kc == D / 32 - 1) {
+                // tile t+3 (set (t+3) % 2) to LDS, then tile t+5 into the same
+                // set, halfway through the MFMAs so their latency is covered
+                constexpr int set = (T4 + 1) & 1;
+                if (FAST) {
+                    st[set].store(stage[(T4 + 3) % kRing]);
+                    load_tile(st[set], ld);
+                } else if (t + 3 < n_prox) {
+                    st[set].store(stage[(T4 + 3) % kRing]);
+                    if (ld.t < n_prox) load_tile(st[set], ld);
+                }
+                ld.advance(a.Gh);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -719,17 +734,6 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
 #pragma unroll
                 for (int q = 0; q < 2; ++q) asm volatile("" : "+v"(runA[s][q]), "+v"(runB[s][q]));
         }
-        // tile t+3 (set (t+3) % 2) to LDS, then tile t+5 into the same set
-        constexpr int set = (T4 + 1) & 1;
-        if (FAST) {
-            st[set].store(stage[(T4 + 3) % kRing]);
-            load_tile(st[set], ld);
-        } else if (t + 3 < n_prox) {
-            st[set].store(stage[(T4 + 3) % kRing]);
-            if (ld.t < n_prox) load_tile(st[set], ld);
-        }
-        ld.advance(a.Gh);
-        Cn = Cnext;
         if (PROBS) group_step();
         if ((T4 & 1) == 0) __syncthreads();
     };
