@@ -679,6 +679,14 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
         constexpr int cur = T4 & 1, prev = cur ^ 1;
         const u32x4* next = stage[(T4 + 1) % kRing];
         const bool mfma_on = FAST || t < n_prox;
+        // The two waves of a SIMD (w and w + WAVES/2) take turns at the
+        // higher issue priority, one tile each, so that neither runs ahead
+        // and waits at the barrier (the older wave would otherwise win every
+        // arbitration).
+        if ((((T4 & 1) ^ (wave / (WAVES / 2))) & 1) != 0)
+            __builtin_amdgcn_s_setprio(1);
+        else
+            __builtin_amdgcn_s_setprio(0);
         float ev[kPer32];
         auto add_group = [&](int g) {
 #pragma unroll
