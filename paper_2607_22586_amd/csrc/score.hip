@@ -366,6 +366,12 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         constexpr bool PREV = decltype(prev)::value != 0, MF = decltype(mf)::value != 0,
                        FAST = decltype(fast)::value != 0;
         const u32x4* next = stage[(T4 + 1) % kRing];
+        // the two waves of a SIMD (w and w + WAVES/2) take turns at the
+        // higher issue priority, one tile each (see pass 2)
+        if ((((T4 & 1) ^ (wave / (WAVES / 2))) & 1) != 0)
+            __builtin_amdgcn_s_setprio(1);
+        else
+            __builtin_amdgcn_s_setprio(0);
         auto chain = [&](auto si) {
             constexpr int S = decltype(si)::value;
             constexpr int CUR = S & 1, PRV = CUR ^ 1, SP = (S + NS - 1) % NS;
