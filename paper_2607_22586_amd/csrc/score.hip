@@ -418,20 +418,27 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
                 }
             }
         };
+        // tile t+3 to LDS and tile t+4 into the staging registers, between
+        // the chains so that their latency is covered by MFMAs
+        auto staging = [&]() {
+            if (FAST) {
+                st.store(stage[(T4 + 3) % kRing]);
+                st.load_block(pbase + static_cast<int64_t>(32 * (t + 4)) * D, off);
+            } else if (t + 3 < n_tiles) {
+                st.store(stage[(T4 + 3) % kRing]);
+                if (t + 4 < n_tiles) load_tile(t + 4);
+            }
+        };
         chain(Tag<0>{});
         if constexpr (MF) {
             chain(Tag<1>{});
+            staging();
             if constexpr (NS > 2) {
                 chain(Tag<2>{});
                 chain(Tag<3>{});
             }
-        }
-        if (FAST) {
-            st.store(stage[(T4 + 3) % kRing]);
-            st.load_block(pbase + static_cast<int64_t>(32 * (t + 4)) * D, off);
-        } else if (t + 3 < n_tiles) {
-            st.store(stage[(T4 + 3) % kRing]);
-            if (t + 4 < n_tiles) load_tile(t + 4);
+        } else {
+            staging();
         }
         if ((T4 & 1) == 0) __syncthreads();
     };
