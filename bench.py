@@ -11,7 +11,7 @@ lambda=1, vote mode).
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--streams N]
 
 The layers of a step are independent, so the throughput steps spread them
-over N HIP streams (layer l on stream l % N, default 3): the latency-bound
+over N HIP streams (layer l on stream l % N, default 4: one per hardware queue): the latency-bound
 selection kernels and the tails of one layer's score passes then overlap
 another layer's work.  The score-pass durations for the roofline come from
 K further steps on one stream, where no other kernel shares the GPU.
@@ -400,7 +400,7 @@ def main():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--mode", choices=["vote", "mass"], default="vote")
     ap.add_argument("--cpu-heads", type=int, default=12)
-    ap.add_argument("--streams", type=int, default=3,
+    ap.add_argument("--streams", type=int, default=4,
                     help="HIP streams the layers are spread over in the throughput steps "
                          "(layer l on stream l %% n); the kernel-timing steps use one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
