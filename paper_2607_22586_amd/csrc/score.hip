@@ -218,14 +218,14 @@ constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batc
 // two accumulator sets alternate between the chains.  The accumulators start
 // at zero, so the MFMA leaves the base-2 logit itself and every logit costs
 // one exp and one add (in a block with keys past T, a chain's accumulator
-// starts at -inf on their rows instead).  A chain's lane sum is kept
-// relative to zero while it
-// lies in [2^-60, H) with H = lane_sum_hi, the bound under which no partial
-// of a row's total can overflow; at 2^-60 or more the terms that underflow
-// (each below 2^-126) are negligible against the sum.  Otherwise the whole
-// wave takes that chain again relative to each lane's exact maximum while its
-// values are still in registers, and the lane's (max, sum) pair is merged by
-// the max-and-rescale rule.  Per tile, the two half-waves' sums of each
+// starts at -inf on their rows instead).  A lane's running sum over the
+// tile's chains is kept relative to zero while it lies in [2^-60, H) with
+// H = lane_sum_hi, the bound under which no partial of a row's total can
+// overflow; at 2^-60 or more the terms that underflow (each below 2^-126)
+// are negligible against the sum.  A chain that would take it out of that
+// range is taken again by the whole wave relative to each lane's exact
+// maximum while its values are still in registers, and the lane's
+// (max, sum) pair is merged by the max-and-rescale rule.  Per tile, the two half-waves' sums of each
 // column are combined and the waves' pairs are merged every kMergeTiles tiles
 // into one partial per (row, key block).  FULL: every key of the block is < T.
 template <int D, int WAVES, int NS, bool FULL>
@@ -295,20 +295,25 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
     for (int kc = 0; kc < KC; ++kc) A[0][kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
 
     floatx16 acc[2];
-    // per-lane pair of the tile being summed: fast part relative to zero,
-    // exact part (max, sum) from chains that left the fast range
+    // per-lane pair of the tile being summed: fast part relative to zero
+    // (the running sum over the tile's chains so far), exact part (max, sum)
+    // from chains that left the fast range; me and se are back at -inf and 0
+    // whenever exact_tile is false
     float sf = 0.f, me = -INFINITY, se = 0.f;
-    bool exact_tile = false;                   // wave-uniform
+    int exact_tile = 0;                        // wave-uniform flag
 
-    // finish chain (values in acc[SETP], sub-tile SP) after its exps: range
-    // check and, if needed, the exact form
-    auto finish_chain = [&](auto setp, auto sp, float lsum) {
+    // finish chain (values in acc[SETP], sub-tile SP) after its exps; nsf is
+    // the running sum with this chain's values added: range check and, if
+    // needed, the exact form
+    auto finish_chain = [&](auto setp, auto sp, float nsf) {
         constexpr int SETP = decltype(setp)::value, SP = decltype(sp)::value;
         // a lane whose keys are all past T has nothing to sum
-        const bool in_range = (lsum >= 0x1p-60f || (!FULL && n_keys(SP) <= 0)) && lsum < a.lane_sum_hi;
+        const bool in_range = (nsf >= 0x1p-60f || (!FULL && n_keys(SP) <= 0)) && nsf < a.lane_sum_hi;
         if (__ballot(!in_range) == 0) {
-            sf += lsum;
+            sf = nsf;
         } else {
+            // the tile's first chain starts the running sum
+            if (SP == 0) sf = 0.f;
             // (keys past T hold -inf and drop out of both)
             float mx = -INFINITY;
 #pragma unroll
@@ -321,14 +326,20 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
                 se = (me == -INFINITY ? 0.f : se * fast_exp2(me - mm)) + ls * fast_exp2(mx - mm);
                 me = mm;
             }
-            exact_tile = true;
+            // set here, inside the branch that the whole wave takes or
+            // skips (as a select on the ballot it would cost two VALU ops
+            // on the fast path)
+            exact_tile = 1;
+            asm volatile("" : "+s"(exact_tile));
         }
     };
     // column (max, sum) of tile tp from both half-waves, to LDS
     auto finish_tile = [&](int tp, bool merge_now) {
         float mrow = 0.f, l;
         if (!exact_tile) {
+            // every chain was in range, so in a full block l >= 2^-60
             l = pair_total(sf);
+            if (!FULL && !(l > 0.f)) mrow = -INFINITY;
         } else {
             // lane pair: fast part (max 0) and exact part
             float M = sf > 0.f ? fmaxf(0.f, me) : me;
@@ -342,16 +353,15 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
             l = 0.f;
             if (mrow != -INFINITY)
                 l = (m0 == -INFINITY ? 0.f : s0 * fast_exp2(m0 - mrow)) + (m1 == -INFINITY ? 0.f : s1 * fast_exp2(m1 - mrow));
+            // an empty sum (no valid key) carries no maximum, so it cannot
+            // outweigh the pairs it is merged with
+            if (!(l > 0.f)) mrow = -INFINITY;
+            me = -INFINITY;
+            se = 0.f;
+            exact_tile = 0;
         }
-        // an empty sum (no valid key) carries no maximum, so it cannot
-        // outweigh the pairs it is merged with
-        if (!(l > 0.f)) mrow = -INFINITY;
         if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(mrow, l);
         if (merge_now) merge_chunk((tp - kMergeTiles) / kMergeTiles);
-        sf = 0.f;
-        me = -INFINITY;
-        se = 0.f;
-        exact_tile = false;
     };
 
     // One pipeline iteration over tile t (LDS slot t % 4): chain s of tile t
@@ -377,7 +387,10 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
             constexpr int CUR = S & 1, PRV = CUR ^ 1, SP = (S + NS - 1) % NS;
             constexpr bool HAVE_PREV = S > 0 ? MF : PREV;
             constexpr int AS = T4 & 1, AN = AS ^ 1;    // fragment sets of tiles t and t+1
-            float l0 = 0.f, l1 = 0.f;
+            // the previous chain's values are added to the running sum (a
+            // tile's first chain, SP == 0, starts it from -0, the additive
+            // identity, so that first add is no instruction)
+            float l0 = SP == 0 ? -0.f : sf, l1 = -0.f;
             if (!FULL && MF) {
                 // keys past T start at -inf, so their 2^s is 0 (the mask is
                 // opaque here so that the start values are not kept live
