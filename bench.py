@@ -64,7 +64,7 @@ def measured_traffic(workload, kernel):
     if t.get("workload") != workload or t.get("score_hip_sha256") != src:
         return None
     # a pass is the kernels one C-ABI call launches
-    parts = {"score_lse": ("anchor_rows", "score_lse", "lse_combine")}.get(kernel, (kernel,))
+    parts = {"score_lse": ("score_lse", "lse_combine")}.get(kernel, (kernel,))
     ks = [t.get("kernels", {}).get(p) for p in parts]
     if any(k is None or k.get("hbm_bytes_per_launch") is None for k in ks):
         return None

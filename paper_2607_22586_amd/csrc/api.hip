@@ -87,7 +87,7 @@ int status_of(hipError_t e) { return e == hipSuccess ? MMSKV_OK : MMSKV_EHIP; }
 struct ScoreLayout {
     ScorePlan plan;
     int n_kb, block_keys, mass_n_kb, rows, rows_pad;
-    size_t part_bytes, lse_off, anchor_off, total;
+    size_t part_bytes, lse_off, total;
 };
 
 ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
@@ -103,8 +103,7 @@ ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
     const size_t heads = static_cast<size_t>(s->B) * s->Hkv;
     l.part_bytes = heads * l.n_kb * l.rows_pad * sizeof(float2);
     l.lse_off = align_up(l.part_bytes);
-    l.anchor_off = l.lse_off + align_up(heads * l.rows_pad * sizeof(float));
-    l.total = l.anchor_off + align_up(heads * (l.rows_pad - l.rows) * s->d * sizeof(uint16_t));
+    l.total = l.lse_off + align_up(heads * l.rows_pad * sizeof(float));
     return l;
 }
 
@@ -169,7 +168,6 @@ int prepare_score(const mmskv_shape* shape, const mmskv_params* params, const ui
     a->lane_sum_hi = lane_sum_limit(shape->T, 16);     // pass 1 sums 16 keys per lane and chain
     a->part = static_cast<float2*>(ws);
     a->lse = reinterpret_cast<float*>(static_cast<char*>(ws) + l.lse_off);
-    a->anchors = reinterpret_cast<const uint16_t*>(static_cast<char*>(ws) + l.anchor_off);
     a->group_mass = nullptr;
     a->mass = nullptr;
     a->anchor = nullptr;

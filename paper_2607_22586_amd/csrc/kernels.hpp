@@ -42,9 +42,8 @@ struct ScoreArgs {
     int mass_n_kb;             // pass-2 key blocks
     int rows;                  // Gh * P proxy rows per KV head
     int rows_pad;              // rows + 32 * ceil(Gh / 32) (anchor rows, padded)
-    double anchor_scale;       // log2(e) / sqrt(d), applied to the anchor rows
+    double anchor_scale;       // log2(e) / sqrt(d), applied to the anchor rows as they are staged
     float lane_sum_hi;         // pass 1 sums from zero while every lane sum is below this
-    const uint16_t* anchors;   // [B, Hkv, rows_pad - rows, d] scaled anchor rows (workspace)
     float2* part;              // [B, Hkv, n_kb, rows_pad]  (max, sum), base 2
     float* lse;                // [B, Hkv, rows_pad]        log2-domain
     float* group_mass;         // [B, Hkv, G, T] or null

@@ -86,12 +86,10 @@ __device__ __forceinline__ bf16x8 lds_frag(const u32x4* stage, int row, int chun
     return __builtin_bit_cast(bf16x8, stage[row * TileLds<D>::kRow + chunk]);
 }
 
-// The anchor rows of head (b, c) in the workspace: 32 * ceil(Gh / 32) rows of
-// D bf16 values, row h < Gh the scaled last window query of query head
-// c * Gh + h, the rest zero (written by anchor_rows_kernel before pass 1).
-template <int D>
-__device__ __forceinline__ const uint16_t* anchor_block(const ScoreArgs& a, int head) {
-    return a.anchors + static_cast<int64_t>(head) * (a.rows_pad - a.rows) * D;
+// bf16 bits of the anchor value v (bf16 bits) times log2(e)/sqrt(d): the
+// product in fp64, rounded fp64 -> fp32 -> bf16 like the proxies.
+__device__ __forceinline__ uint32_t scaled_anchor(uint32_t v, double scale) {
+    return f32_to_bf16_bits(static_cast<float>(static_cast<double>(__uint_as_float(v << 16)) * scale));
 }
 
 // Per-thread share of staging one tile: thread j moves 16-byte chunks
@@ -122,6 +120,26 @@ struct Stager {
 #pragma unroll
         for (int k = 0; k < kPer; ++k)
             if (active(k)) v[k] = *reinterpret_cast<const u32x4*>(base + off[k]);
+    }
+    // anchor tile ta of KV head (b, c), formed from the last window queries:
+    // row r is query head c*Gh + 32 ta + r scaled (zero past Gh); hq0 is the
+    // index of query head (b, c*Gh)
+    __device__ __forceinline__ void load_anchor(const ScoreArgs& a, int64_t hq0, int ta) {
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            if (!active(k)) continue;
+            const int q = chunk_of(k), r = q / TileLds<D>::kChunks, ch = q - r * TileLds<D>::kChunks;
+            const int h = 32 * ta + r;
+            u32x4 x = {0u, 0u, 0u, 0u};
+            if (h < a.Gh) {
+                const u32x4 raw = *reinterpret_cast<const u32x4*>(a.q_last + (hq0 + h) * D + 8 * ch);
+#pragma unroll
+                for (int w = 0; w < 4; ++w)
+                    x[w] = scaled_anchor(raw[w] & 0xFFFFu, a.anchor_scale) |
+                           (scaled_anchor(raw[w] >> 16, a.anchor_scale) << 16);
+            }
+            v[k] = x;
+        }
     }
     __device__ __forceinline__ void store(u32x4* stage) const {
 #pragma unroll
@@ -247,17 +265,16 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
 
     const int n_tiles = a.rows_pad / 32;
     const int n_prox = a.rows / 32;
-    const uint16_t* pbase =
-        a.proxies + (static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh) * a.P * D;
+    const int64_t hq0 = static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh;
+    const uint16_t* pbase = a.proxies + hq0 * a.P * D;
     int off[St::kPer];
 #pragma unroll
     for (int k = 0; k < St::kPer; ++k) off[k] = St::src_off(k);
     St st;
     // tile t = rows [32t, 32t+32) of the padded row space
-    const uint16_t* abase = anchor_block<D>(a, head);
     auto load_tile = [&](int t) {
         if (t < n_prox) st.load_block(pbase + static_cast<int64_t>(32 * t) * D, off);
-        else st.load_block(abase + static_cast<int64_t>(32 * (t - n_prox)) * D, off);
+        else st.load_anchor(a, hq0, t - n_prox);
     };
 
     float2* part = a.part + (static_cast<int64_t>(head) * a.n_kb + kb) * a.rows_pad;
@@ -496,28 +513,6 @@ __global__ void __launch_bounds__(64 * WAVES) score_lse_kernel(ScoreArgs a) {
         lse_body<D, WAVES, NS, true>(a, head, kb, b, c, stage, mrg);
     else
         lse_body<D, WAVES, NS, false>(a, head, kb, b, c, stage, mrg);
-}
-
-// The anchor rows of every head (b, c): row h < Gh is query head c*Gh + h's
-// last window query (a bf16 value) times log2(e)/sqrt(d) in fp64, rounded
-// fp64 -> fp32 -> bf16 like the proxies; the padding rows are zero.  One
-// thread per pair of elements.
-__global__ void __launch_bounds__(256) anchor_rows_kernel(ScoreArgs a) {
-    const int head = static_cast<int>(blockIdx.y);
-    const int b = head / a.Hkv, c = head - b * a.Hkv;
-    const int n_rows = a.rows_pad - a.rows;
-    const int i = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x);   // element pair
-    if (i >= n_rows * a.d / 2) return;
-    const int r = (2 * i) / a.d, j = 2 * i - r * a.d;
-    uint32_t out = 0u;
-    if (r < a.Gh) {
-        const int64_t hq = static_cast<int64_t>(b) * a.Hq + static_cast<int64_t>(c) * a.Gh + r;
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(a.q_last + hq * a.d + j);
-        const double lo = static_cast<double>(__uint_as_float(v << 16)) * a.anchor_scale;
-        const double hi = static_cast<double>(__uint_as_float(v & 0xFFFF0000u)) * a.anchor_scale;
-        out = f32_to_bf16_bits(static_cast<float>(lo)) | (f32_to_bf16_bits(static_cast<float>(hi)) << 16);
-    }
-    reinterpret_cast<uint32_t*>(const_cast<uint16_t*>(a.anchors) + static_cast<int64_t>(head) * n_rows * a.d)[i] = out;
 }
 
 // L_row = M + log2(sum_kb S_kb * 2^(M_kb - M)), one thread per row; the
@@ -798,7 +793,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     float aacc[kSub] = {0.f, 0.f};
     for (int ta = 0; ta < n_anc; ++ta) {
         __syncthreads();
-        st[0].load_block(anchor_block<D>(a, head) + static_cast<int64_t>(32 * ta) * D, off);
+        st[0].load_anchor(a, hq0, ta);
         st[0].store(stage[0]);
         __syncthreads();
         read_frags<D>(stage[0], A, lane);
@@ -829,12 +824,8 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
 
 template <int D, int WAVES, int NS>
 hipError_t lse_impl(const ScoreArgs& a, hipStream_t s) {
-    const int pairs = (a.rows_pad - a.rows) * a.d / 2;
-    hipLaunchKernelGGL(anchor_rows_kernel, dim3((pairs + 255) / 256, a.B * a.Hkv), dim3(256), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((score_lse_kernel<D, WAVES, NS>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES), 0, s, a);
-    e = hipGetLastError();
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g2((a.rows_pad + 255) / 256, a.B * a.Hkv);
     hipLaunchKernelGGL(lse_combine_kernel, g2, dim3(256), 0, s, a);

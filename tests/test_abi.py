@@ -133,10 +133,10 @@ def test_workspace_queries(lib):
     s, p = _shape(B=4, Hq=28, Hkv=4, T=16384, W=64, d=128), _params()
     ws = lib.mmshiftkv_score_workspace(ctypes.byref(s), ctypes.byref(p))
     # partial (max, sum) per (head, key block of at most 1024 keys, row) +
-    # one lse per row + the scaled anchor rows; rows = Gh*P proxies + the
-    # anchor rows padded to 32
+    # one lse per row; rows = Gh*P proxies + the anchor rows padded to 32
+    # (the scaled anchor rows themselves are formed as the kernels stage them)
     rows_pad = 7 * 512 + 32
-    assert ws >= 16 * (16384 // 1024) * rows_pad * 8 + 16 * rows_pad * 4 + 16 * 32 * 128 * 2
+    assert ws >= 16 * (16384 // 1024) * rows_pad * 8 + 16 * rows_pad * 4
     assert ws % 256 == 0
     wsel = lib.mmshiftkv_select_workspace(ctypes.byref(s), ctypes.byref(p))
     assert wsel >= 16 * 16384 * 8

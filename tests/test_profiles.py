@@ -16,7 +16,7 @@ def test_traffic_summary_matches_score_source():
     with open(os.path.join(ROOT, "paper_2607_22586_amd", "csrc", "score.hip"), "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
     assert t["workload"] == "qwen7b_16k_b4"
-    for k in ("anchor_rows", "score_lse", "lse_combine", "score_mass"):
+    for k in ("score_lse", "lse_combine", "score_mass"):
         assert t["kernels"][k]["hbm_bytes_per_launch"] > 0, k
     assert 1.5 < t["fetch_factor"] < 2.5 and 0.5 < t["write_factor"] < 1.5
     import sys
@@ -24,7 +24,7 @@ def test_traffic_summary_matches_score_source():
     import bench
     got = bench.measured_traffic("qwen7b_16k_b4", "score_lse")
     if t["score_hip_sha256"] == sha:
-        want = sum(t["kernels"][k]["hbm_bytes_per_launch"] for k in ("anchor_rows", "score_lse", "lse_combine"))
+        want = sum(t["kernels"][k]["hbm_bytes_per_launch"] for k in ("score_lse", "lse_combine"))
         assert got == want
     else:
         assert got is None, "bench.py must not report counters taken on another score.hip"
