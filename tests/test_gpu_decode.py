@@ -85,6 +85,18 @@ def test_decode_check_keep_all_ragged():
     compare(x, g)
 
 
+def test_decode_check_fp32_cache():
+    """fp32 K/V (the compacted cache keeps fp32, so decode attention takes the
+    fp32 VALU kernel; coverage scores bf16-rounded keys as the prefill does):
+    T = 700, d = 64, budget 300 (two chunks of cached keys), 6 decode queries."""
+    x = wl.custom_layer(1, 4, 2, 700, 4, 64, dtype="fp32", seed=11)
+    x["q_dec"] = (2.0 * torch.randn((1, 4, 6, 64), generator=torch.Generator().manual_seed(13))).to(torch.bfloat16)
+    cfg = bd.SelectionConfig(P=64, G=4, seed=5)
+    g = gpu_check(x, cfg, budget=300)
+    assert g[4].dtype == np.float32
+    compare(x, g)
+
+
 def test_decode_check_full_size_sampled():
     """The benchmark's shape (B=4, T=16384, 28q/4kv, d=128, C=256) with 16
     decode queries per head: every row's coverage and output, checked against
