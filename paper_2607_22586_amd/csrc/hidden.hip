@@ -192,11 +192,14 @@ __device__ __forceinline__ floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
 }
 
 // Rows r of A (M x K) and of W (N x K) in 16-byte chunks; rows past the
-// matrix and k past D read as zero.
+// matrix and k past D read as zero.  FULL: every tile lies inside the
+// matrices, so the loads carry no condition (and the waits for them can be
+// counted exactly, leaving the next stage's loads in flight).
 struct GemmStage {
     u32x4 a[kLoads], w[kLoads];
 };
 
+template <bool FULL>
 __device__ __forceinline__ void gemm_fetch(const ProjectArgs& p, int m0, int n0, int k0, GemmStage& st) {
 #pragma unroll
     for (int q = 0; q < kLoads; ++q) {
@@ -204,10 +207,15 @@ __device__ __forceinline__ void gemm_fetch(const ProjectArgs& p, int m0, int n0,
         const int r = c / kRowChunks, kc = c % kRowChunks;
         const int k = k0 + 8 * kc;
         const u32x4 zero = {0u, 0u, 0u, 0u};
-        st.a[q] = (m0 + r < p.M && k < p.K)
-                      ? *reinterpret_cast<const u32x4*>(p.a + static_cast<int64_t>(m0 + r) * p.K + k) : zero;
-        st.w[q] = (n0 + r < p.N && k < p.K)
-                      ? *reinterpret_cast<const u32x4*>(p.w + static_cast<int64_t>(n0 + r) * p.K + k) : zero;
+        if (FULL) {
+            st.a[q] = *reinterpret_cast<const u32x4*>(p.a + static_cast<int64_t>(m0 + r) * p.K + k);
+            st.w[q] = *reinterpret_cast<const u32x4*>(p.w + static_cast<int64_t>(n0 + r) * p.K + k);
+        } else {
+            st.a[q] = (m0 + r < p.M && k < p.K)
+                          ? *reinterpret_cast<const u32x4*>(p.a + static_cast<int64_t>(m0 + r) * p.K + k) : zero;
+            st.w[q] = (n0 + r < p.N && k < p.K)
+                          ? *reinterpret_cast<const u32x4*>(p.w + static_cast<int64_t>(n0 + r) * p.K + k) : zero;
+        }
     }
 }
 
@@ -221,6 +229,7 @@ __device__ __forceinline__ void gemm_store(const GemmStage& st, u32x4* la, u32x4
     }
 }
 
+template <bool FULL>
 __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
     // two stages of (A tile, W tile); the fp32 output tile reuses the space
     __shared__ u32x4 lds[2 * 2 * kTileSlots];
@@ -241,10 +250,10 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
     // step ks); two register stages hold the global loads of steps ks+1 and
     // ks+2, so every load has two steps of MFMA work to arrive in
     GemmStage s0, s1;
-    gemm_fetch(p, m0, n0, 0, s0);
+    gemm_fetch<FULL>(p, m0, n0, 0, s0);
     gemm_store(s0, lds, lds + kTileSlots);
-    if (1 < n_k) gemm_fetch(p, m0, n0, kBK, s1);
-    if (2 < n_k) gemm_fetch(p, m0, n0, 2 * kBK, s0);
+    if (1 < n_k) gemm_fetch<FULL>(p, m0, n0, kBK, s1);
+    if (2 < n_k) gemm_fetch<FULL>(p, m0, n0, 2 * kBK, s0);
     __syncthreads();
     // step ks; `nx` holds the loads of step ks+1 and is refilled with ks+3
     auto step = [&](int ks, GemmStage& nx) {
@@ -268,7 +277,7 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
         if (ks + 1 < n_k) {
             u32x4* na = lds + (cur ^ 1) * 2 * kTileSlots;
             gemm_store(nx, na, na + kTileSlots);
-            if (ks + 3 < n_k) gemm_fetch(p, m0, n0, (ks + 3) * kBK, nx);
+            if (ks + 3 < n_k) gemm_fetch<FULL>(p, m0, n0, (ks + 3) * kBK, nx);
         }
         __syncthreads();
     };
@@ -361,7 +370,10 @@ hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s) {
 
 hipError_t launch_project(const ProjectArgs& p, hipStream_t s) {
     dim3 g((p.M + kBM - 1) / kBM, (p.N + kBN - 1) / kBN);
-    hipLaunchKernelGGL(project_kernel, g, dim3(kGemmThreads), 0, s, p);
+    if (p.M % kBM == 0 && p.N % kBN == 0 && p.K % kBK == 0)
+        hipLaunchKernelGGL(project_kernel<true>, g, dim3(kGemmThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(project_kernel<false>, g, dim3(kGemmThreads), 0, s, p);
     return hipGetLastError();
 }
 
