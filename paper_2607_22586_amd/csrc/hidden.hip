@@ -281,7 +281,40 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
         }
         __syncthreads();
     };
-    for (int ks = 0; ks < n_k; ks += 2) {
+    int ks = 0;
+    if (FULL) {
+        // steady state without conditions (so the waits for each stage's
+        // loads leave the younger stage in flight): steps ks, ks+1 with
+        // ks+4 < n_k, both refills inside the matrix
+        auto step_full = [&](int k, GemmStage& nx) {
+            const int cur = k & 1;
+            const u32x4* la = lds + cur * 2 * kTileSlots;
+            const u32x4* lw = la + kTileSlots;
+#pragma unroll
+            for (int kc = 0; kc < kBK / 16; ++kc) {
+                bf16x8 fa[2], fw[2];
+                const int chunk = 2 * kc + (lane >> 5);
+#pragma unroll
+                for (int x = 0; x < 2; ++x) {
+                    fa[x] = __builtin_bit_cast(bf16x8, la[(wm * 64 + 32 * x + (lane & 31)) * kRowSlots + chunk]);
+                    fw[x] = __builtin_bit_cast(bf16x8, lw[(wn * 64 + 32 * x + (lane & 31)) * kRowSlots + chunk]);
+                }
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(fa[x], fw[y], acc[x][y]);
+            }
+            u32x4* na = lds + (cur ^ 1) * 2 * kTileSlots;
+            gemm_store(nx, na, na + kTileSlots);
+            gemm_fetch<true>(p, m0, n0, (k + 3) * kBK, nx);
+            __syncthreads();
+        };
+        for (; ks + 4 < n_k; ks += 2) {
+            step_full(ks, s1);
+            step_full(ks + 1, s0);
+        }
+    }
+    for (; ks < n_k; ks += 2) {
         step(ks, s1);
         if (ks + 1 < n_k) step(ks + 1, s0);
     }
