@@ -206,7 +206,7 @@ def decode_check_bench(args):
         "config": {"workload": w.name, "layers": L, "batch": B, "T": T, "Hq": Hq, "Hkv": Hkv, "d": d,
                    "budget": w.budget, "n_dec": n, "decode_var_scale": wl.DECODE_VAR_SCALE},
         "coverage": {"mean": float(cov.mean()), "min": float(cov.min()), "max": float(cov.max())},
-        "roofline": {"kernel": "decode check call (decode_cover_kernel + combine + decode_attend_kernel)",
+        "roofline": {"kernel": "decode check call (decode_scale_kernel + decode_cover_kernel + decode_attend_mfma_kernel)",
                      "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": None,
                      "bytes_per_call": nbytes, "us_per_call": call_ms * 1e3},
