@@ -393,12 +393,6 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         constexpr bool PREV = decltype(prev)::value != 0, MF = decltype(mf)::value != 0,
                        FAST = decltype(fast)::value != 0;
         const u32x4* next = stage[(T4 + 1) % kRing];
-        // the two waves of a SIMD (w and w + WAVES/2) take turns at the
-        // higher issue priority, one tile each (see pass 2)
-        if ((((T4 & 1) ^ (wave / (WAVES / 2))) & 1) != 0)
-            __builtin_amdgcn_s_setprio(1);
-        else
-            __builtin_amdgcn_s_setprio(0);
         auto chain = [&](auto si) {
             constexpr int S = decltype(si)::value;
             constexpr int CUR = S & 1, PRV = CUR ^ 1, SP = (S + NS - 1) % NS;
@@ -569,7 +563,9 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     int head, kb;
     block_work(a.mass_n_kb, head, kb);
     const int b = head / a.Hkv, c = head - b * a.Hkv;
-    const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
+    // the wave index in a scalar register, so that the priority branch below
+    // is a scalar branch that each wave takes or skips
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave), lane = lane_id();
     const int key0 = kb * 64 * WAVES + wave * kWaveKeys;
     const float* L = a.lse + static_cast<int64_t>(head) * a.rows_pad;
 
@@ -700,11 +696,11 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
         constexpr int cur = T4 & 1, prev = cur ^ 1;
         const u32x4* next = stage[(T4 + 1) % kRing];
         const bool mfma_on = FAST || t < n_prox;
-        // The two waves of a SIMD (w and w + WAVES/2) take turns at the
-        // higher issue priority, one tile each, so that neither runs ahead
-        // and waits at the barrier (the older wave would otherwise win every
-        // arbitration).
-        if ((((T4 & 1) ^ (wave / (WAVES / 2))) & 1) != 0)
+        // Issue priority: on every other tile the younger wave of each SIMD
+        // (w >= WAVES/2) runs at the higher priority, so that the older one,
+        // which otherwise wins every arbitration, does not run ahead and wait
+        // at the barrier; on the other tiles both are equal.
+        if ((T4 & 1) != 0 || wave >= WAVES / 2)
             __builtin_amdgcn_s_setprio(1);
         else
             __builtin_amdgcn_s_setprio(0);
