@@ -229,6 +229,73 @@ __device__ __forceinline__ void gemm_store(const GemmStage& st, u32x4* la, u32x4
     }
 }
 
+// Epilogue of a 128 x 128 output tile: the fp32 accumulators (wave (wm, wn)
+// holds rows wm*64.., columns wn*64..) through LDS, then the rotary pairs,
+// the softmax scale and the bf16 rounding, to the proxies' layout.
+__device__ __forceinline__ void project_epilogue(const ProjectArgs& p, const floatx16 (&acc)[2][2], u32x4* lds,
+                                                 int m0, int n0, int wm, int wn, int lane) {
+    constexpr int kLd = kBN + 4;
+    float* tile = reinterpret_cast<float*>(lds);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int r = wm * 64 + 32 * x + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+                const int cc = wn * 64 + 32 * y + (lane & 31);
+                tile[r * kLd + cc] = acc[x][y][i];
+            }
+    __syncthreads();
+    const int d = p.d, half = d / 2;
+    const bool rope = p.cos != nullptr;
+    // each thread: one row, 8 consecutive output columns (one head's
+    // lower half when rotary pairs are formed)
+    const int groups = rope ? kBN / 16 : kBN / 8;     // 8-column groups per row
+    for (int g = static_cast<int>(threadIdx.x); g < kBM * groups; g += kGemmThreads) {
+        const int r = g / groups, cg = g % groups;
+        const int m = m0 + r;
+        if (m >= p.M) continue;
+        const int bb = m / p.P, i = m % p.P;
+        int col;
+        if (rope) {
+            const int c8 = cg * 8;                     // lower-half column index inside the tile's heads
+            col = (c8 / half) * d + (c8 % half);
+        } else {
+            col = cg * 8;
+        }
+        const int n = n0 + col;
+        if (n >= p.N) continue;
+        const int h = n / d, e = n % d;
+        uint16_t* out = p.out + ((static_cast<int64_t>(bb) * p.Hq + h) * p.P + i) * d;
+        u32x4 lo, hi;
+        if (!rope) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                lo[q] = f32_to_bf16_bits(scaled(tile[r * kLd + col + 2 * q], p.scale)) |
+                        (f32_to_bf16_bits(scaled(tile[r * kLd + col + 2 * q + 1], p.scale)) << 16);
+            *reinterpret_cast<u32x4*>(out + e) = lo;
+        } else {
+            uint32_t l16[8], h16[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const float x0 = tile[r * kLd + col + q], x1 = tile[r * kLd + col + half + q];
+                const float c = p.cos[e + q], s = p.sin[e + q];
+                const float a0 = x0 * c, a1 = x1 * s, b0 = x1 * c, b1 = x0 * s;
+                l16[q] = f32_to_bf16_bits(scaled(a0 - a1, p.scale));
+                h16[q] = f32_to_bf16_bits(scaled(b0 + b1, p.scale));
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                lo[q] = l16[2 * q] | (l16[2 * q + 1] << 16);
+                hi[q] = h16[2 * q] | (h16[2 * q + 1] << 16);
+            }
+            *reinterpret_cast<u32x4*>(out + e) = lo;
+            *reinterpret_cast<u32x4*>(out + e + half) = hi;
+        }
+    }
+}
+
 template <bool FULL>
 __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
     // two stages of (A tile, W tile); the fp32 output tile reuses the space
@@ -319,67 +386,118 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
         if (ks + 1 < n_k) step(ks + 1, s0);
     }
 
-    // epilogue: fp32 tile [kBM][kBN + 4] in LDS, then rotary pairs and bf16
-    constexpr int kLd = kBN + 4;
-    float* tile = reinterpret_cast<float*>(lds);
+    project_epilogue(p, acc, lds, m0, n0, wm, wn, lane);
+}
+
+// Full tiles with direct-to-LDS loads (global_load_lds_dwordx4): the tiles
+// of k step ks land in LDS stage ks % NS without passing through registers,
+// issued NS - 1 steps ahead; one barrier per step.  The waits are written out
+// (each wave waits for its own share of stage ks, the barrier then covers
+// every wave's share and every wave's reads of step ks - 1, whose stage the
+// step's new loads overwrite).  A row of a stage is DK / 8 chunks of 16
+// bytes, chunk c of row r at slot c ^ f(r), f chosen so that the 8 rows read
+// in one 128-byte LDS phase (one chunk each) fall in 8 different bank groups.
+template <int DK>
+struct DmaTile {
+    static constexpr int kChunks = DK / 8;                 // 16-byte chunks per row
+    static constexpr int kRow = DK * 2;                    // bytes per row
+    static constexpr int kTile = kBM * kRow;               // bytes per operand tile
+    static constexpr int kStage = 2 * kTile;               // A tile, then W tile
+    static constexpr int kRowsPerOp = 1024 / kRow;         // rows per 1 KB instruction
+    static constexpr int kOps = 32 / kRowsPerOp;           // instructions per operand per wave
+    static constexpr int kPerStage = 2 * kOps;             // loads per wave per stage
+    static __device__ __forceinline__ int slot(int r, int c) {
+        return kChunks == 4 ? c ^ ((r >> 1) & 3) : c ^ (r & 7);
+    }
+};
+
+// wave w issues rows 32 w .. 32 w + 31 of both tiles of one step
+template <int DK>
+__device__ __forceinline__ void dma_step(const ProjectArgs& p, int m0, int n0, int k0, char* stage, int wave, int lane) {
+    using T = DmaTile<DK>;
+#pragma unroll
+    for (int op = 0; op < 2; ++op) {
+        const uint16_t* src = op == 0 ? p.a + static_cast<int64_t>(m0) * p.K : p.w + static_cast<int64_t>(n0) * p.K;
+#pragma unroll
+        for (int j = 0; j < T::kOps; ++j) {
+            const int r0 = 32 * wave + T::kRowsPerOp * j, r = r0 + lane / T::kChunks;
+            const int c = T::slot(r, lane % T::kChunks);
+            __builtin_amdgcn_global_load_lds(src + static_cast<int64_t>(r) * p.K + k0 + 8 * c,
+                                             (__attribute__((address_space(3))) void*)(stage + op * T::kTile + r0 * T::kRow),
+                                             16, 0, 0);
+        }
+    }
+}
+
+// s_waitcnt with vmcnt = N and the other counters not waited on
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N < 64, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+
+template <int DK, int NS>
+__global__ void __launch_bounds__(kGemmThreads) project_dma_kernel(ProjectArgs p) {
+    using T = DmaTile<DK>;
+    static_assert(kBM == kBN && kBM == 128, "four waves of 32 rows per operand");
+    // the stages, or the epilogue's fp32 tile if that is larger
+    constexpr int kBytes = NS * T::kStage > kBM * (kBN + 4) * 4 ? NS * T::kStage : kBM * (kBN + 4) * 4;
+    __shared__ u32x4 lds[kBytes / 16];
+    char* base = reinterpret_cast<char*>(lds);
+    const int m0 = static_cast<int>(blockIdx.x) * kBM, n0 = static_cast<int>(blockIdx.y) * kBN;
+    const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
+    const int wm = wave >> 1, wn = wave & 1;
+    const int n_k = p.K / DK;
+    floatx16 acc[2][2];
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int r = wm * 64 + 32 * x + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-                const int cc = wn * 64 + 32 * y + (lane & 31);
-                tile[r * kLd + cc] = acc[x][y][i];
-            }
-    __syncthreads();
-    const int d = p.d, half = d / 2;
-    const bool rope = p.cos != nullptr;
-    // each thread: one row, 8 consecutive output columns (one head's
-    // lower half when rotary pairs are formed)
-    const int groups = rope ? kBN / 16 : kBN / 8;     // 8-column groups per row
-    for (int g = static_cast<int>(threadIdx.x); g < kBM * groups; g += kGemmThreads) {
-        const int r = g / groups, cg = g % groups;
-        const int m = m0 + r;
-        if (m >= p.M) continue;
-        const int bb = m / p.P, i = m % p.P;
-        int col;
-        if (rope) {
-            const int c8 = cg * 8;                     // lower-half column index inside the tile's heads
-            col = (c8 / half) * d + (c8 % half);
-        } else {
-            col = cg * 8;
-        }
-        const int n = n0 + col;
-        if (n >= p.N) continue;
-        const int h = n / d, e = n % d;
-        uint16_t* out = p.out + ((static_cast<int64_t>(bb) * p.Hq + h) * p.P + i) * d;
-        u32x4 lo, hi;
-        if (!rope) {
+            for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                lo[q] = f32_to_bf16_bits(scaled(tile[r * kLd + col + 2 * q], p.scale)) |
-                        (f32_to_bf16_bits(scaled(tile[r * kLd + col + 2 * q + 1], p.scale)) << 16);
-            *reinterpret_cast<u32x4*>(out + e) = lo;
-        } else {
-            uint32_t l16[8], h16[8];
+    for (int st = 0; st < NS - 1; ++st)
+        if (st < n_k) dma_step<DK>(p, m0, n0, st * DK, base + st * T::kStage, wave, lane);
+    for (int ks = 0; ks < n_k; ++ks) {
+        // this wave's loads of stage ks are the oldest outstanding; later
+        // stages in flight: min(NS - 2, n_k - 1 - ks)
+        const int later = min(NS - 2, n_k - 1 - ks);
+        if (later >= 3) wait_vm<3 * T::kPerStage>();
+        else if (later == 2) wait_vm<2 * T::kPerStage>();
+        else if (later == 1) wait_vm<T::kPerStage>();
+        else wait_vm<0>();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (ks + NS - 1 < n_k)
+            dma_step<DK>(p, m0, n0, (ks + NS - 1) * DK, base + ((ks + NS - 1) % NS) * T::kStage, wave, lane);
+        const char* sa = base + (ks % NS) * T::kStage;
+        const char* sw = sa + T::kTile;
+        // fragments of k chunk kc + 1 are read while the MFMAs of kc run
+        bf16x8 fa[2][2], fw[2][2];
+        auto read_frags = [&](int kc, int buf) {
+            const int c = 2 * kc + (lane >> 5);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const float x0 = tile[r * kLd + col + q], x1 = tile[r * kLd + col + half + q];
-                const float c = p.cos[e + q], s = p.sin[e + q];
-                const float a0 = x0 * c, a1 = x1 * s, b0 = x1 * c, b1 = x0 * s;
-                l16[q] = f32_to_bf16_bits(scaled(a0 - a1, p.scale));
-                h16[q] = f32_to_bf16_bits(scaled(b0 + b1, p.scale));
+            for (int x = 0; x < 2; ++x) {
+                const int ra = wm * 64 + 32 * x + (lane & 31), rw = wn * 64 + 32 * x + (lane & 31);
+                fa[buf][x] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sa + ra * T::kRow + 16 * T::slot(ra, c)));
+                fw[buf][x] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sw + rw * T::kRow + 16 * T::slot(rw, c)));
             }
+        };
+        read_frags(0, 0);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                lo[q] = l16[2 * q] | (l16[2 * q + 1] << 16);
-                hi[q] = h16[2 * q] | (h16[2 * q + 1] << 16);
-            }
-            *reinterpret_cast<u32x4*>(out + e) = lo;
-            *reinterpret_cast<u32x4*>(out + e + half) = hi;
+        for (int kc = 0; kc < DK / 16; ++kc) {
+            if (kc + 1 < DK / 16) read_frags(kc + 1, (kc + 1) & 1);
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(fa[kc & 1][x], fw[kc & 1][y], acc[x][y]);
         }
     }
+    // every wave's reads done before the tile reuses the stages
+    asm volatile("" ::: "memory");
+    __syncthreads();
+    project_epilogue(p, acc, lds, m0, n0, wm, wn, lane);
 }
 
 }  // namespace
@@ -403,7 +521,12 @@ hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s) {
 
 hipError_t launch_project(const ProjectArgs& p, hipStream_t s) {
     dim3 g((p.M + kBM - 1) / kBM, (p.N + kBN - 1) / kBN);
-    if (p.M % kBM == 0 && p.N % kBN == 0 && p.K % kBK == 0)
+    // full tiles: 64-wide k steps in two LDS stages loaded directly (two
+    // workgroups per CU; deeper rings of 32- or 64-wide steps leave one per
+    // CU, or more barriers per MFMA, and measured slower)
+    if (p.M % kBM == 0 && p.N % kBN == 0 && p.K % 64 == 0)
+        hipLaunchKernelGGL((project_dma_kernel<64, 2>), g, dim3(kGemmThreads), 0, s, p);
+    else if (p.M % kBM == 0 && p.N % kBN == 0 && p.K % kBK == 0)
         hipLaunchKernelGGL(project_kernel<true>, g, dim3(kGemmThreads), 0, s, p);
     else
         hipLaunchKernelGGL(project_kernel<false>, g, dim3(kGemmThreads), 0, s, p);
