@@ -192,14 +192,11 @@ __device__ __forceinline__ floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
 }
 
 // Rows r of A (M x K) and of W (N x K) in 16-byte chunks; rows past the
-// matrix and k past D read as zero.  FULL: every tile lies inside the
-// matrices, so the loads carry no condition (and the waits for them can be
-// counted exactly, leaving the next stage's loads in flight).
+// matrix and k past D read as zero.
 struct GemmStage {
     u32x4 a[kLoads], w[kLoads];
 };
 
-template <bool FULL>
 __device__ __forceinline__ void gemm_fetch(const ProjectArgs& p, int m0, int n0, int k0, GemmStage& st) {
 #pragma unroll
     for (int q = 0; q < kLoads; ++q) {
@@ -207,15 +204,10 @@ __device__ __forceinline__ void gemm_fetch(const ProjectArgs& p, int m0, int n0,
         const int r = c / kRowChunks, kc = c % kRowChunks;
         const int k = k0 + 8 * kc;
         const u32x4 zero = {0u, 0u, 0u, 0u};
-        if (FULL) {
-            st.a[q] = *reinterpret_cast<const u32x4*>(p.a + static_cast<int64_t>(m0 + r) * p.K + k);
-            st.w[q] = *reinterpret_cast<const u32x4*>(p.w + static_cast<int64_t>(n0 + r) * p.K + k);
-        } else {
-            st.a[q] = (m0 + r < p.M && k < p.K)
-                          ? *reinterpret_cast<const u32x4*>(p.a + static_cast<int64_t>(m0 + r) * p.K + k) : zero;
-            st.w[q] = (n0 + r < p.N && k < p.K)
-                          ? *reinterpret_cast<const u32x4*>(p.w + static_cast<int64_t>(n0 + r) * p.K + k) : zero;
-        }
+        st.a[q] = (m0 + r < p.M && k < p.K)
+                      ? *reinterpret_cast<const u32x4*>(p.a + static_cast<int64_t>(m0 + r) * p.K + k) : zero;
+        st.w[q] = (n0 + r < p.N && k < p.K)
+                      ? *reinterpret_cast<const u32x4*>(p.w + static_cast<int64_t>(n0 + r) * p.K + k) : zero;
     }
 }
 
@@ -296,7 +288,7 @@ __device__ __forceinline__ void project_epilogue(const ProjectArgs& p, const flo
     }
 }
 
-template <bool FULL>
+// Any shape (ragged tiles): register-staged loads, two LDS stages.
 __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
     // two stages of (A tile, W tile); the fp32 output tile reuses the space
     __shared__ u32x4 lds[2 * 2 * kTileSlots];
@@ -317,10 +309,10 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
     // step ks); two register stages hold the global loads of steps ks+1 and
     // ks+2, so every load has two steps of MFMA work to arrive in
     GemmStage s0, s1;
-    gemm_fetch<FULL>(p, m0, n0, 0, s0);
+    gemm_fetch(p, m0, n0, 0, s0);
     gemm_store(s0, lds, lds + kTileSlots);
-    if (1 < n_k) gemm_fetch<FULL>(p, m0, n0, kBK, s1);
-    if (2 < n_k) gemm_fetch<FULL>(p, m0, n0, 2 * kBK, s0);
+    if (1 < n_k) gemm_fetch(p, m0, n0, kBK, s1);
+    if (2 < n_k) gemm_fetch(p, m0, n0, 2 * kBK, s0);
     __syncthreads();
     // step ks; `nx` holds the loads of step ks+1 and is refilled with ks+3
     auto step = [&](int ks, GemmStage& nx) {
@@ -344,43 +336,11 @@ __global__ void __launch_bounds__(kGemmThreads) project_kernel(ProjectArgs p) {
         if (ks + 1 < n_k) {
             u32x4* na = lds + (cur ^ 1) * 2 * kTileSlots;
             gemm_store(nx, na, na + kTileSlots);
-            if (ks + 3 < n_k) gemm_fetch<FULL>(p, m0, n0, (ks + 3) * kBK, nx);
+            if (ks + 3 < n_k) gemm_fetch(p, m0, n0, (ks + 3) * kBK, nx);
         }
         __syncthreads();
     };
     int ks = 0;
-    if (FULL) {
-        // steady state without conditions (so the waits for each stage's
-        // loads leave the younger stage in flight): steps ks, ks+1 with
-        // ks+4 < n_k, both refills inside the matrix
-        auto step_full = [&](int k, GemmStage& nx) {
-            const int cur = k & 1;
-            const u32x4* la = lds + cur * 2 * kTileSlots;
-            const u32x4* lw = la + kTileSlots;
-#pragma unroll
-            for (int kc = 0; kc < kBK / 16; ++kc) {
-                bf16x8 fa[2], fw[2];
-                const int chunk = 2 * kc + (lane >> 5);
-#pragma unroll
-                for (int x = 0; x < 2; ++x) {
-                    fa[x] = __builtin_bit_cast(bf16x8, la[(wm * 64 + 32 * x + (lane & 31)) * kRowSlots + chunk]);
-                    fw[x] = __builtin_bit_cast(bf16x8, lw[(wn * 64 + 32 * x + (lane & 31)) * kRowSlots + chunk]);
-                }
-#pragma unroll
-                for (int x = 0; x < 2; ++x)
-#pragma unroll
-                    for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(fa[x], fw[y], acc[x][y]);
-            }
-            u32x4* na = lds + (cur ^ 1) * 2 * kTileSlots;
-            gemm_store(nx, na, na + kTileSlots);
-            gemm_fetch<true>(p, m0, n0, (k + 3) * kBK, nx);
-            __syncthreads();
-        };
-        for (; ks + 4 < n_k; ks += 2) {
-            step_full(ks, s1);
-            step_full(ks + 1, s0);
-        }
-    }
     for (; ks < n_k; ks += 2) {
         step(ks, s1);
         if (ks + 1 < n_k) step(ks + 1, s0);
@@ -526,10 +486,8 @@ hipError_t launch_project(const ProjectArgs& p, hipStream_t s) {
     // CU, or more barriers per MFMA, and measured slower)
     if (p.M % kBM == 0 && p.N % kBN == 0 && p.K % 64 == 0)
         hipLaunchKernelGGL((project_dma_kernel<64, 2>), g, dim3(kGemmThreads), 0, s, p);
-    else if (p.M % kBM == 0 && p.N % kBN == 0 && p.K % kBK == 0)
-        hipLaunchKernelGGL(project_kernel<true>, g, dim3(kGemmThreads), 0, s, p);
     else
-        hipLaunchKernelGGL(project_kernel<false>, g, dim3(kGemmThreads), 0, s, p);
+        hipLaunchKernelGGL(project_kernel, g, dim3(kGemmThreads), 0, s, p);
     return hipGetLastError();
 }
 
