@@ -205,12 +205,6 @@ __device__ __forceinline__ float pair_sum(float x0, float x1) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Both half-waves' maximum in every lane.
-__device__ __forceinline__ float pair_max(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-
 // Both half-waves' sum in every lane.
 __device__ __forceinline__ float pair_total(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
