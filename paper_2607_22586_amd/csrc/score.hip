@@ -37,6 +37,8 @@
 // one L2.
 #include <math.h>
 
+#include <utility>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -150,27 +152,34 @@ struct Stager {
 
 // Key fragments of the wave's 32*NS keys: kf[s][kc] holds key
 // key0 + 32*s + (lane % 32), dims [16*kc + 8*(lane/32), +8).
+// (BF16_FULL: the caller has checked that the keys are bf16 and that every
+// key of the sub-tile is < T, so the loads are unconditional and carry no
+// branch, which keeps the compiler's count of outstanding loads exact)
+template <int D, bool BF16_FULL = false>
+__device__ __forceinline__ void load_key_sub(const ScoreArgs& a, int b, int c, int key0, int s,
+                                             bf16x8 (&ks)[D / 16]) {
+    const int lane = lane_id();
+    const int col = 8 * (lane >> 5);
+    const int t = key0 + 32 * s + (lane & 31);
+    const bool ok = BF16_FULL || t < a.T;
+    const int64_t off = static_cast<int64_t>(b) * a.ksb + static_cast<int64_t>(c) * a.ksh +
+                        static_cast<int64_t>(ok ? t : 0) * a.kst;
+    if (BF16_FULL || a.k_dtype == 1) {
+        const uint16_t* p = static_cast<const uint16_t*>(a.k) + off + col;
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc) ks[kc] = ok ? load_bf16x8(p + 16 * kc) : zero_bf16x8();
+    } else {
+        const float* p = static_cast<const float*>(a.k) + off + col;
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc) ks[kc] = ok ? load_f32_as_bf16x8(p + 16 * kc) : zero_bf16x8();
+    }
+}
+
 template <int D, int NS = kSub>
 __device__ __forceinline__ void load_keys(const ScoreArgs& a, int b, int c, int key0,
                                           bf16x8 (&kf)[NS][D / 16]) {
-    const int lane = lane_id();
-    const int col = 8 * (lane >> 5);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        const int t = key0 + 32 * s + (lane & 31);
-        const bool ok = t < a.T;
-        const int64_t off = static_cast<int64_t>(b) * a.ksb + static_cast<int64_t>(c) * a.ksh +
-                            static_cast<int64_t>(ok ? t : 0) * a.kst;
-        if (a.k_dtype == 1) {
-            const uint16_t* p = static_cast<const uint16_t*>(a.k) + off + col;
-#pragma unroll
-            for (int kc = 0; kc < D / 16; ++kc) kf[s][kc] = ok ? load_bf16x8(p + 16 * kc) : zero_bf16x8();
-        } else {
-            const float* p = static_cast<const float*>(a.k) + off + col;
-#pragma unroll
-            for (int kc = 0; kc < D / 16; ++kc) kf[s][kc] = ok ? load_f32_as_bf16x8(p + 16 * kc) : zero_bf16x8();
-        }
-    }
+    for (int s = 0; s < NS; ++s) load_key_sub<D>(a, b, c, key0, s, kf[s]);
 }
 
 // Fragments of one 32-row tile for this lane: row (lane % 32), 16-byte
@@ -218,8 +227,20 @@ struct Tag {
     static constexpr int value = N;
 };
 
+// f(Tag<0>{}), ..., f(Tag<N-1>{}), unrolled at compile time.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(Tag<I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // ---------------------------------------------------------------- pass 1
 constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batched
+constexpr int kEarlyTiles = 8;    // pass-1 tiles taken sub-tile by sub-tile while the keys arrive
+constexpr int kEarlySubs = 4;     // sub-tiles per wave of that schedule
 
 // Pass 1 in the K * P^T layout.  Each wave holds NS sub-tiles of 32 keys; for
 // every 32-row tile of the row space it runs one chain of D/16 dependent
@@ -240,18 +261,20 @@ constexpr int kMergeTiles = 16;   // pass-1 tiles whose cross-wave merge is batc
 // (max, sum) pair is merged by the max-and-rescale rule.  Per tile, the two half-waves' sums of each
 // column are combined and the waves' pairs are merged every kMergeTiles tiles
 // into one partial per (row, key block).  FULL: every key of the block is < T.
-template <int D, int WAVES, int NS, bool FULL>
+template <int D, int WAVES, int NS, bool FULL, bool EARLY, int SLOTS>
 __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, int b, int c,
-                                         u32x4 (&stage)[kRing][TileLds<D>::kSlots],
+                                         u32x4 (&stage)[SLOTS][TileLds<D>::kSlots],
                                          float2 (&mrg)[2][kMergeTiles][WAVES][32]) {
     using St = Stager<D, WAVES>;
     constexpr int KC = D / 16;                 // MFMAs per chain
     static_assert(NS % 2 == 0, "chains alternate between two accumulator sets");
+    static_assert(!EARLY || (FULL && NS == kEarlySubs && SLOTS >= kEarlyTiles && kEarlyTiles >= kRing),
+                  "the early tiles are full blocks of four sub-tiles in their own LDS slots");
     const int wave = static_cast<int>(threadIdx.x) / kWave, lane = lane_id();
     const int key0 = kb * (32 * NS * WAVES) + wave * (32 * NS);
 
     bf16x8 kf[NS][KC];
-    load_keys<D, NS>(a, b, c, key0, kf);
+    if constexpr (!EARLY) load_keys<D, NS>(a, b, c, key0, kf);
     // keys of sub-tile s held by this lane that are < T: value i is key
     // key0 + 32 s + 8 (i / 4) + 4 (lane / 32) + i % 4, valid while
     // 8 (i / 4) + i % 4 < n_keys(s)
@@ -290,22 +313,23 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         }
     };
 
-    // Prologue: tiles 0-2 to LDS slots 0-2, tile 3 in the staging registers.
-    for (int k = 0; k < 3; ++k) {
-        if (k < n_tiles) {
-            load_tile(k);
-            st.store(stage[k]);
-        }
-    }
-    if (3 < n_tiles) load_tile(3);
-    __syncthreads();
     // fragments of tile t in set t % 2; the other set is refilled with tile
     // t+1 while tile t's chains run, one 16-byte read per NS/2 MFMAs
     bf16x8 A[2][KC];
-#pragma unroll
-    for (int kc = 0; kc < KC; ++kc) A[0][kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
-
     floatx16 acc[2];
+    if constexpr (!EARLY) {
+        // Prologue: tiles 0-2 to LDS slots 0-2, tile 3 in the staging registers.
+        for (int k = 0; k < 3; ++k) {
+            if (k < n_tiles) {
+                load_tile(k);
+                st.store(stage[k]);
+            }
+        }
+        if (3 < n_tiles) load_tile(3);
+        __syncthreads();
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) A[0][kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
+    }
     // per-lane pair of the tile being summed: fast part relative to zero
     // (the running sum over the tile's chains so far), exact part (max, sum)
     // from chains that left the fast range; me and se are back at -inf and 0
@@ -344,18 +368,20 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
             asm volatile("" : "+s"(exact_tile));
         }
     };
-    // column (max, sum) of tile tp from both half-waves, to LDS
-    auto finish_tile = [&](int tp, bool merge_now) {
+    // column (max, sum) of a tile from both half-waves: fast part sfv
+    // (relative to zero) and, when `exact` (wave-uniform), the exact part
+    // (mev, sev)
+    auto tile_pair = [&](float sfv, float mev, float sev, bool exact) {
         float mrow = 0.f, l;
-        if (!exact_tile) {
+        if (!exact) {
             // every chain was in range, so in a full block l >= 2^-60
-            l = pair_total(sf);
+            l = pair_total(sfv);
             if (!FULL && !(l > 0.f)) mrow = -INFINITY;
         } else {
             // lane pair: fast part (max 0) and exact part
-            float M = sf > 0.f ? fmaxf(0.f, me) : me;
+            float M = sfv > 0.f ? fmaxf(0.f, mev) : mev;
             float S = 0.f;
-            if (M != -INFINITY) S = (sf > 0.f ? sf * fast_exp2(-M) : 0.f) + (me == -INFINITY ? 0.f : se * fast_exp2(me - M));
+            if (M != -INFINITY) S = (sfv > 0.f ? sfv * fast_exp2(-M) : 0.f) + (mev == -INFINITY ? 0.f : sev * fast_exp2(mev - M));
             const auto rm = __builtin_amdgcn_permlane32_swap(__float_as_uint(M), __float_as_uint(M), false, false);
             const auto rs = __builtin_amdgcn_permlane32_swap(__float_as_uint(S), __float_as_uint(S), false, false);
             const float m0 = __uint_as_float(rm[0]), m1 = __uint_as_float(rm[1]);
@@ -367,11 +393,18 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
             // an empty sum (no valid key) carries no maximum, so it cannot
             // outweigh the pairs it is merged with
             if (!(l > 0.f)) mrow = -INFINITY;
+        }
+        return make_float2(mrow, l);
+    };
+    // column (max, sum) of tile tp from both half-waves, to LDS
+    auto finish_tile = [&](int tp, bool merge_now) {
+        const float2 pr = tile_pair(sf, me, se, exact_tile != 0);
+        if (exact_tile) {
             me = -INFINITY;
             se = 0.f;
             exact_tile = 0;
         }
-        if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = make_float2(mrow, l);
+        if (lane < 32) mrg[(tp / kMergeTiles) & 1][tp % kMergeTiles][wave][lane] = pr;
         if (merge_now) merge_chunk((tp - kMergeTiles) / kMergeTiles);
     };
 
@@ -460,10 +493,129 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
         }
         if ((T4 & 1) == 0) __syncthreads();
     };
+    int t0 = 0;
+    if constexpr (EARLY) {
+        // Early tiles: the first kEarlyTiles proxy tiles are staged in their
+        // own LDS slots before any key load is issued, and their chains run
+        // sub-tile by sub-tile (sub-tile 0 of every early tile, then
+        // sub-tile 1, ...).  Only sub-tile 0's keys are fetched up front;
+        // round s issues the loads of sub-tile s+1, so a quarter of the key
+        // block is in flight at a time and each round waits for its own
+        // quarter only (with every key load issued at once, the memory system
+        // serves them in its own order, and since a wave's loads complete in
+        // issue order the first quarter would be complete only near the end
+        // of the whole burst).  Per tile, the chains are summed in the same
+        // order as in the pipeline below, so the partials are the same
+        // numbers.
+        {
+            St pre[kEarlyTiles];
+#pragma unroll
+            for (int k = 0; k < kEarlyTiles; ++k) pre[k].load_block(pbase + static_cast<int64_t>(32 * k) * D, off);
+            load_key_sub<D, true>(a, b, c, key0, 0, kf[0]);
+#pragma unroll
+            for (int k = 0; k < kEarlyTiles; ++k) pre[k].store(stage[k]);
+        }
+        __syncthreads();
+        float sp[kEarlyTiles];                 // running fast sum of each early tile
+#pragma unroll
+        for (int k = 0; k < kEarlyTiles; ++k) sp[k] = 0.f;
+        int exact_mask = 0;                    // wave-uniform: early tiles with exact partials
+        // exact partials (max, sum) per (early tile, lane) of this wave, in
+        // the second merge buffer, which the pipeline first writes for tile
+        // kMergeTiles (after the barriers below)
+        float2* xs = &mrg[1][0][0][0] + wave * (kEarlyTiles * 64);
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) A[0][kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
+        // chain (sub-tile PS, tile PT) summed: running sum nsf, values in acc[PRV]
+        auto early_finish = [&](auto prv, auto ps, auto pt, float nsf) {
+            constexpr int PRV = decltype(prv)::value, PS = decltype(ps)::value, PT = decltype(pt)::value;
+            const bool in_range = nsf >= 0x1p-60f && nsf < a.lane_sum_hi;
+            if (__ballot(!in_range) == 0) {
+                sp[PT] = nsf;
+            } else {
+                if (PS == 0) sp[PT] = 0.f;
+                float mx = -INFINITY;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[PRV][i]);
+                float2 ex = ((exact_mask >> PT) & 1) ? xs[PT * 64 + lane] : make_float2(-INFINITY, 0.f);
+                if (mx != -INFINITY) {
+                    float ls = 0.f;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) ls += fast_exp2(acc[PRV][i] - mx);
+                    const float mm = fmaxf(ex.x, mx);
+                    ex.y = (ex.x == -INFINITY ? 0.f : ex.y * fast_exp2(ex.x - mm)) + ls * fast_exp2(mx - mm);
+                    ex.x = mm;
+                }
+                xs[PT * 64 + lane] = ex;
+                exact_mask |= 1 << PT;
+                asm volatile("" : "+s"(exact_mask));
+            }
+        };
+        static_for<kEarlySubs * kEarlyTiles>([&](auto ci) {
+            constexpr int C = decltype(ci)::value;
+            constexpr int S = C / kEarlyTiles, TT = C % kEarlyTiles;
+            constexpr int CUR = C & 1, PRV = CUR ^ 1;
+            constexpr int PC = C > 0 ? C - 1 : 0, PS = PC / kEarlyTiles, PT = PC % kEarlyTiles;
+            constexpr int NT = (TT + 1) % kEarlyTiles;     // the next chain's tile
+            if constexpr (TT == 0 && S + 1 < kEarlySubs) load_key_sub<D, true>(a, b, c, key0, S + 1, kf[S + 1]);
+            float l0 = (C > 0 && PS != 0) ? sp[PT] : -0.f, l1 = -0.f;
+#pragma unroll
+            for (int kc = 0; kc < KC; ++kc) {
+                acc[CUR] = mfma32(kf[S][kc], A[C & 1][kc], kc == 0 ? zero16() : acc[CUR]);
+                __builtin_amdgcn_sched_barrier(0);
+                if (C > 0 && kc > 0) {
+                    constexpr int kSlots = KC - 1;
+#pragma unroll
+                    for (int i = 16 * (kc - 1) / kSlots; i < 16 * kc / kSlots; ++i) {
+                        const float e = fast_exp2(acc[PRV][i]);
+                        if (i & 1) l1 += e; else l0 += e;
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                if (C + 1 < kEarlySubs * kEarlyTiles)
+                    A[(C + 1) & 1][kc] = lds_frag<D>(stage[NT], lane & 31, 2 * kc + (lane >> 5));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if constexpr (C > 0) early_finish(Tag<PRV>{}, Tag<PS>{}, Tag<PT>{}, l0 + l1);
+        });
+        // the pipeline's start: tiles kEarlyTiles .. +2 to ring slots 0-2,
+        // the next in the staging registers (fetched before the last chain
+        // is summed, stored once every wave is done with the early slots)
+        constexpr int kLast = kEarlySubs * kEarlyTiles - 1;
+        {
+            St pre[3];
+#pragma unroll
+            for (int k = 0; k < 3; ++k) pre[k].load_block(pbase + static_cast<int64_t>(32 * (kEarlyTiles + k)) * D, off);
+            load_tile(kEarlyTiles + 3);
+            {
+                float l0 = sp[kEarlyTiles - 1], l1 = -0.f;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float e = fast_exp2(acc[kLast & 1][i]);
+                    if (i & 1) l1 += e; else l0 += e;
+                }
+                early_finish(Tag<kLast & 1>{}, Tag<kEarlySubs - 1>{}, Tag<kEarlyTiles - 1>{}, l0 + l1);
+            }
+#pragma unroll
+            for (int k = 0; k < kEarlyTiles; ++k) {
+                const bool ex = ((exact_mask >> k) & 1) != 0;
+                const float2 xe = ex ? xs[k * 64 + lane] : make_float2(-INFINITY, 0.f);
+                const float2 pr = tile_pair(sp[k], xe.x, xe.y, ex);
+                if (lane < 32) mrg[0][k][wave][lane] = pr;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < 3; ++k) pre[k].store(stage[k]);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) A[0][kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
+        t0 = kEarlyTiles;
+    }
     using Off = Tag<0>;
     using On = Tag<1>;
-    iter(Tag<0>{}, Off{}, On{}, Off{}, 0);
-    int t = 1;
+    iter(Tag<0>{}, Off{}, On{}, Off{}, t0);
+    int t = t0 + 1;
     __builtin_amdgcn_s_waitcnt(0);
     for (; t + 3 + 4 < n_prox; t += 4) {
         iter(Tag<1>{}, On{}, On{}, On{}, t);
@@ -492,15 +644,26 @@ __device__ __forceinline__ void lse_body(const ScoreArgs& a, int head, int kb, i
 
 template <int D, int WAVES, int NS>
 __global__ void __launch_bounds__(64 * WAVES) score_lse_kernel(ScoreArgs a) {
-    __shared__ u32x4 stage[kRing][TileLds<D>::kSlots];
+    constexpr bool kEarly = NS == kEarlySubs;
+    constexpr int kSlotsAll = kEarly ? kEarlyTiles : kRing;
+    __shared__ u32x4 stage[kSlotsAll][TileLds<D>::kSlots];
     __shared__ float2 mrg[2][kMergeTiles][WAVES][32];
     int head, kb;
     block_work(a.n_kb, head, kb);
     const int b = head / a.Hkv, c = head - b * a.Hkv;
-    if ((kb + 1) * (32 * NS * WAVES) <= a.T)
-        lse_body<D, WAVES, NS, true>(a, head, kb, b, c, stage, mrg);
-    else
-        lse_body<D, WAVES, NS, false>(a, head, kb, b, c, stage, mrg);
+    if ((kb + 1) * (32 * NS * WAVES) <= a.T) {
+        // the early schedule needs every tile it stages ahead to be a proxy
+        // tile, and bf16 keys (loaded without conversion)
+        if constexpr (kEarly) {
+            if (a.rows / 32 >= 2 * kMergeTiles && a.k_dtype == 1) {
+                lse_body<D, WAVES, NS, true, true>(a, head, kb, b, c, stage, mrg);
+                return;
+            }
+        }
+        lse_body<D, WAVES, NS, true, false>(a, head, kb, b, c, stage, mrg);
+    } else {
+        lse_body<D, WAVES, NS, false, false>(a, head, kb, b, c, stage, mrg);
+    }
 }
 
 // L_row = M + log2(sum_kb S_kb * 2^(M_kb - M)), one thread per row; the
