@@ -22,6 +22,7 @@ double query_scale(int d) { return 1.4426950408889634074 / sqrt(static_cast<doub
 
 constexpr size_t kAlign = 256;
 constexpr size_t kMaxRowLds = 96 * 1024;   // Gh * P + 32 rows of fp32 in LDS
+constexpr size_t kMaxRowLds8 = 64 * 1024;  // the same with 8-wave mass blocks
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -100,6 +101,13 @@ ScoreLayout score_layout(const mmskv_shape* s, const mmskv_params* p) {
     l.mass_n_kb = (s->T + l.block_keys - 1) / l.block_keys;
     l.rows = Gh * p->P;
     l.rows_pad = l.rows + 32 * ((Gh + 31) / 32);
+    // 8-wave mass blocks hold 8 staged tiles (68 KiB at d = 128) next to the
+    // row normalisers; many rows take 4-wave blocks, which stage 4
+    if (l.plan.mass_waves == 8 && static_cast<size_t>(l.rows_pad) * sizeof(float) > kMaxRowLds8) {
+        l.plan.mass_waves = 4;
+        l.block_keys = 64 * l.plan.mass_waves;
+        l.mass_n_kb = (s->T + l.block_keys - 1) / l.block_keys;
+    }
     const size_t heads = static_cast<size_t>(s->B) * s->Hkv;
     l.part_bytes = heads * l.n_kb * l.rows_pad * sizeof(float2);
     l.lse_off = align_up(l.part_bytes);

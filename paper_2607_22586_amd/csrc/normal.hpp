@@ -92,12 +92,13 @@ __device__ void sincos_turn(uint32_t x, float& sn, float& cs) {
     }
     const float s0 = phi * ps;
     const float c0 = pc;
-    switch (q & 3) {
-        case 0: sn = s0; cs = c0; break;
-        case 1: sn = c0; cs = -s0; break;
-        case 2: sn = -s0; cs = -c0; break;
-        default: sn = -c0; cs = s0; break;
-    }
+    // quadrant q & 3 gives (s0, c0), (c0, -s0), (-s0, -c0), (-c0, s0): an
+    // odd q swaps the pair, q & 2 negates the sine and (q + 1) & 2 the
+    // cosine (selects and sign flips, no divergent branch)
+    const bool swap = (q & 1) != 0;
+    const float sv = swap ? c0 : s0, cv = swap ? s0 : c0;
+    sn = __uint_as_float(__float_as_uint(sv) ^ ((q & 2) ? 0x80000000u : 0u));
+    cs = __uint_as_float(__float_as_uint(cv) ^ (((q + 1) & 2) ? 0x80000000u : 0u));
 }
 
 // Four standard normals for dims 4*jq..4*jq+3 of proxy i, query head h,

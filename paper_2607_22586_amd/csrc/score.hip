@@ -710,15 +710,14 @@ struct TileCursor {
     }
 };
 
-template <int D, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
+// EARLY: a full block of bf16 keys, 16 proxies per group (each 16-row half
+// of a tile is one group) and 5 to 8 query heads per KV head (tiles 0-7 then
+// close exactly one proxy block); see the early phase below.
+template <int D, int WAVES, bool EARLY, int SLOTS>
+__device__ __forceinline__ void mass_body(const ScoreArgs& a, int head, int kb,
+                                          u32x4 (&stage)[SLOTS][TileLds<D>::kSlots], float* Llds) {
     using St = Stager<D, WAVES>;
-    __shared__ u32x4 stage[kRing][TileLds<D>::kSlots];
-    extern __shared__ float4 dyn_lds[];
-    float* Llds = reinterpret_cast<float*>(dyn_lds);     // [rows_pad]
-
-    int head, kb;
-    block_work(a.mass_n_kb, head, kb);
+    static_assert(!EARLY || SLOTS >= kEarlyTiles, "the early tiles have their own LDS slots");
     const int b = head / a.Hkv, c = head - b * a.Hkv;
     // the wave index in a scalar register, so that the priority branch below
     // is a scalar branch that each wave takes or skips
@@ -727,7 +726,7 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     const float* L = a.lse + static_cast<int64_t>(head) * a.rows_pad;
 
     bf16x8 kf[kSub][D / 16];
-    load_keys<D>(a, b, c, key0, kf);
+    if constexpr (!EARLY) load_keys<D>(a, b, c, key0, kf);
 
     const int g16 = a.P / a.G / 16;          // 16-row halves per proxy group
     const int n_prox = (a.P / 32) * a.Gh;
@@ -774,32 +773,34 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
             if (i < a.rows_pad) Llds[i] = -lv[j];
         }
     };
-    l_batch(static_cast<int>(threadIdx.x), [&]() {
-#pragma unroll
-        for (int k = 0; k < 3; ++k) {
-            if (ld.t < n_prox) load_tile(pre[k], ld);
-            ld.advance(a.Gh);
-        }
-#pragma unroll
-        for (int k = 3; k < 5; ++k) {
-            if (ld.t < n_prox) load_tile(st[k & 1], ld);
-            ld.advance(a.Gh);
-        }
-    });
-    for (int i0 = static_cast<int>(threadIdx.x) + kLBatch * 64 * WAVES; i0 < a.rows_pad; i0 += kLBatch * 64 * WAVES)
-        l_batch(i0, []() {});
-#pragma unroll
-    for (int k = 0; k < 3; ++k)
-        if (k < n_prox) pre[k].store(stage[k]);
-    __syncthreads();
-    bf16x8 A[D / 16];
-    read_frags<D>(stage[0], A, lane);
     TileCursor mm{0, 0, 0};                  // tile whose accumulator start is read next
     // accumulator starts of tiles t (set t % 2) and t + 1: read one tile ahead
     // into the other set, so none is copied
     floatx16 Cn[2];
-    Cn[0] = row_offsets(Llds + tile_row(mm), lane);
-    mm.advance(a.Gh);
+    bf16x8 A[D / 16];
+    if constexpr (!EARLY) {
+        l_batch(static_cast<int>(threadIdx.x), [&]() {
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                if (ld.t < n_prox) load_tile(pre[k], ld);
+                ld.advance(a.Gh);
+            }
+#pragma unroll
+            for (int k = 3; k < 5; ++k) {
+                if (ld.t < n_prox) load_tile(st[k & 1], ld);
+                ld.advance(a.Gh);
+            }
+        });
+        for (int i0 = static_cast<int>(threadIdx.x) + kLBatch * 64 * WAVES; i0 < a.rows_pad; i0 += kLBatch * 64 * WAVES)
+            l_batch(i0, []() {});
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            if (k < n_prox) pre[k].store(stage[k]);
+        __syncthreads();
+        read_frags<D>(stage[0], A, lane);
+        Cn[0] = row_offsets(Llds + tile_row(mm), lane);
+        mm.advance(a.Gh);
+    }
 
     const int64_t gm_base = static_cast<int64_t>(head) * a.G * a.T;
     const int my_key = key0 + lane;
@@ -919,10 +920,122 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
         if (PROBS) group_step();
         if ((T4 & 1) == 0) __syncthreads();
     };
+    int t0 = 0;
+    if constexpr (EARLY) {
+        // Early phase (as in the log-sum-exp pass): tiles 0-7 are staged in
+        // their own LDS slots before any key load, only sub-tile 0's keys are
+        // fetched up front, and the tiles' 16 chains (8 MFMAs each) run
+        // sub-tile by sub-tile, the first round fetching sub-tile 1's keys, so
+        // each round waits only for its own half of the keys.  Each sub-tile
+        // sums into its own runA / runB, in the same order as in the
+        // pipeline; the proxy block that tiles 0 .. Gh-1 close is folded per
+        // sub-tile when its last head passes and its two group masses are
+        // formed once both sub-tiles are in.
+        {
+            St pre8[kEarlyTiles];
+            l_batch(static_cast<int>(threadIdx.x), [&]() {
+#pragma unroll
+                for (int k = 0; k < kEarlyTiles; ++k) load_tile(pre8[k], TileCursor{k, k / a.Gh, k % a.Gh});
+                load_key_sub<D, true>(a, b, c, key0, 0, kf[0]);
+            });
+            for (int i0 = static_cast<int>(threadIdx.x) + kLBatch * 64 * WAVES; i0 < a.rows_pad;
+                 i0 += kLBatch * 64 * WAVES)
+                l_batch(i0, []() {});
+#pragma unroll
+            for (int k = 0; k < kEarlyTiles; ++k) pre8[k].store(stage[k]);
+        }
+        __syncthreads();
+        bf16x8 Ae[2][D / 16];
+        floatx16 ce[2];                      // accumulators of the current and the previous chain
+        float fold[2][kSub];                 // [half A / B][sub-tile]: the first proxy block's sums
+#pragma unroll
+        for (int kc = 0; kc < D / 16; ++kc) Ae[0][kc] = lds_frag<D>(stage[0], lane & 31, 2 * kc + (lane >> 5));
+        Cn[0] = row_offsets(Llds + tile_row(TileCursor{0, 0, 0}), lane);
+        // the sums of chain (sub-tile PS, tile PT), values in ce[PRV]; when
+        // tile PT is the last head of proxy block 0, that block's sums of
+        // sub-tile PS are set aside
+        auto early_sum = [&](auto prv, auto ps, int pt, int i0, int i1) {
+            constexpr int PRV = decltype(prv)::value, PS = decltype(ps)::value;
+            (void)pt;
+#pragma unroll
+            for (int i = i0; i < i1; ++i) {
+                const float e = fast_exp2(ce[PRV][i]);
+                if (i < 8) runA[PS][i & 1] += e; else runB[PS][i & 1] += e;
+            }
+        };
+        auto early_close = [&](auto ps, int pt) {
+            constexpr int PS = decltype(ps)::value;
+            if (pt == a.Gh - 1) {
+                fold[0][PS] = runA[PS][0] + runA[PS][1];
+                fold[1][PS] = runB[PS][0] + runB[PS][1];
+                runA[PS][0] = runA[PS][1] = runB[PS][0] = runB[PS][1] = 0.f;
+            }
+        };
+        static_for<kSub * kEarlyTiles>([&](auto ci) {
+            constexpr int C = decltype(ci)::value;
+            constexpr int S = C / kEarlyTiles, TT = C % kEarlyTiles;
+            constexpr int CUR = C & 1, PRV = CUR ^ 1;
+            constexpr int PC = C > 0 ? C - 1 : 0, PS = PC / kEarlyTiles, PT = PC % kEarlyTiles;
+            constexpr int NT = (TT + 1) % kEarlyTiles;
+            if constexpr (TT == 0 && S + 1 < kSub) load_key_sub<D, true>(a, b, c, key0, S + 1, kf[S + 1]);
+#pragma unroll
+            for (int kc = 0; kc < D / 16; ++kc) {
+                ce[CUR] = mfma32(Ae[C & 1][kc], kf[S][kc], kc == 0 ? Cn[C & 1] : ce[CUR]);
+                __builtin_amdgcn_sched_barrier(0);
+                // the previous chain's 16 values in slots 1-7 (none read
+                // before its last MFMA has had a slot to finish)
+                if (C > 0 && kc > 0) early_sum(Tag<PRV>{}, Tag<PS>{}, PT, 16 * (kc - 1) / 7, 16 * kc / 7);
+                __builtin_amdgcn_sched_barrier(0);
+                if (C + 1 < kSub * kEarlyTiles)
+                    Ae[(C + 1) & 1][kc] = lds_frag<D>(stage[NT], lane & 31, 2 * kc + (lane >> 5));
+                if (kc == D / 32 && C + 1 < kSub * kEarlyTiles)
+                    Cn[(C + 1) & 1] = row_offsets(Llds + tile_row(TileCursor{NT, NT / a.Gh, NT % a.Gh}), lane);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if constexpr (C > 0) early_close(Tag<PS>{}, PT);
+        });
+        // the pipeline's start: tiles 8-10 to ring slots 0-2, tiles 11 and 12
+        // in the staging registers (tile k in set k % 2), fetched before the
+        // last chain is summed and stored once every wave is done with the
+        // early slots
+        constexpr int kLast = kSub * kEarlyTiles - 1;
+        ld = TileCursor{kEarlyTiles, kEarlyTiles / a.Gh, kEarlyTiles % a.Gh};
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            load_tile(pre[k], ld);
+            ld.advance(a.Gh);
+        }
+#pragma unroll
+        for (int k = 3; k < 5; ++k) {
+            load_tile(st[(kEarlyTiles + k) & 1], ld);
+            ld.advance(a.Gh);
+        }
+        early_sum(Tag<kLast & 1>{}, Tag<kSub - 1>{}, kEarlyTiles - 1, 0, 16);
+        early_close(Tag<kSub - 1>{}, kEarlyTiles - 1);
+        // proxy block 0's two groups (halves A and B), as the pipeline forms
+        // them: the sub-tile sums, then the pair of sub-tiles per key
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+            const float tot = pair_sum(fold[h2][0], fold[h2][1]);
+            macc += tot;
+            if (a.group_mass != nullptr) a.group_mass[gm_base + static_cast<int64_t>(h2) * a.T + my_key] = tot;
+        }
+        g_idx = 2;
+        gs_h = kEarlyTiles % a.Gh;           // heads of proxy block 1 already summed
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 3; ++k) pre[k].store(stage[k]);
+        __syncthreads();
+        read_frags<D>(stage[0], A, lane);
+        mm = TileCursor{kEarlyTiles, kEarlyTiles / a.Gh, kEarlyTiles % a.Gh};
+        Cn[0] = row_offsets(Llds + tile_row(mm), lane);
+        mm.advance(a.Gh);
+        t0 = kEarlyTiles;
+    }
     using Off = Tag<0>;
     using On = Tag<1>;
-    iter(Tag<0>{}, Off{}, Off{}, 0);
-    int t = 1;
+    iter(Tag<0>{}, Off{}, Off{}, t0);
+    int t = t0 + 1;
     // drain the key and staging loads of the prologue here, once, so that no
     // wait for them lands inside the loop
     __builtin_amdgcn_s_waitcnt(0);
@@ -973,6 +1086,24 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
         a.mass[o] = macc;
         a.anchor[o] = anc;
     }
+}
+
+template <int D, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
+    constexpr bool kEarly = WAVES == 8 && D == 128;
+    __shared__ u32x4 stage[kEarly ? kEarlyTiles : kRing][TileLds<D>::kSlots];
+    extern __shared__ float4 dyn_lds[];
+    float* Llds = reinterpret_cast<float*>(dyn_lds);     // [rows_pad]
+    int head, kb;
+    block_work(a.mass_n_kb, head, kb);
+    if constexpr (kEarly) {
+        if ((kb + 1) * 64 * WAVES <= a.T && a.k_dtype == 1 && a.P == 16 * a.G && a.Gh >= 5 &&
+            a.Gh <= kEarlyTiles) {
+            mass_body<D, WAVES, true>(a, head, kb, stage, Llds);
+            return;
+        }
+    }
+    mass_body<D, WAVES, false>(a, head, kb, stage, Llds);
 }
 
 template <int D, int WAVES, int NS>
