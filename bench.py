@@ -49,10 +49,9 @@ def log(msg):
 
 
 def measured_traffic(workload, kernel):
-    """HBM bytes per launch of the pass `kernel` (the sum over the kernels its
-    C-ABI call launches) from the committed rocprofv3 counter summary, or None
-    when it is missing, for another workload or kernel, or older than the
-    current kernel source."""
+    """HBM bytes per launch of `kernel` (score_lse, score_mass, ...) from the
+    committed rocprofv3 counter summary, or None when it is missing, for
+    another workload or kernel, or older than the current kernel source."""
     import hashlib
     try:
         with open(TRAFFIC_FILE) as f:
@@ -63,12 +62,10 @@ def measured_traffic(workload, kernel):
         return None
     if t.get("workload") != workload or t.get("score_hip_sha256") != src:
         return None
-    # a pass is the kernels one C-ABI call launches
-    parts = {"score_lse": ("score_lse", "lse_combine")}.get(kernel, (kernel,))
-    ks = [t.get("kernels", {}).get(p) for p in parts]
-    if any(k is None or k.get("hbm_bytes_per_launch") is None for k in ks):
+    k = t.get("kernels", {}).get(kernel)
+    if k is None or k.get("hbm_bytes_per_launch") is None:
         return None
-    return sum(k["hbm_bytes_per_launch"] for k in ks)
+    return k["hbm_bytes_per_launch"]
 
 
 def measured_mfma_util(workload):
@@ -489,14 +486,19 @@ def main():
             bf = bufs[l % n]
             with torch.cuda.stream(s):
                 bd.build_proxies(x["q_win"], c, T, Hkv, out=(bf["prox"], bf["qlast"]))
-                if events is not None:
+                if events is None:
+                    bd.score_lse(bf["prox"], bf["qlast"], x["k"], c, bf["ws_score"], W)
+                else:
+                    # the log-sum-exp pass as its two calls, so that the events
+                    # bracket score_lse_kernel alone, then the merge kernel
                     events[l][0].record(s)
-                bd.score_lse(bf["prox"], bf["qlast"], x["k"], c, bf["ws_score"], W)
-                if events is not None:
+                    bd.score_lse(bf["prox"], bf["qlast"], x["k"], c, bf["ws_score"], W, stage="blocks")
                     events[l][1].record(s)
+                    bd.score_lse(bf["prox"], bf["qlast"], x["k"], c, bf["ws_score"], W, stage="merge")
+                    events[l][2].record(s)
                 bd.score_mass(bf["prox"], bf["qlast"], x["k"], c, bf["ws_score"], W, out=bf["sc"])
                 if events is not None:
-                    events[l][2].record(s)
+                    events[l][3].record(s)
                 bd.select_topk(bf["sc"], c, w.budget, w.budget, None, Hq, W, out=bf["sel"], workspace=bf["ws_sel"])
                 bd.gather_kv(x["k"], x["v"], bf["sel"], out=kv_out[l])
         for s in streams[1:n]:
@@ -521,16 +523,21 @@ def main():
     log("timed %d steps on %d stream(s): %.3f ms/step" % (args.steps, n_streams, ms_step))
 
     # kernel timing: one more warmup and K steps on one stream, with events
-    # around the two score passes of every layer (un-overlapped durations)
+    # around score_lse_kernel (mmshiftkv_score_lse_blocks), the merge of its
+    # partials (mmshiftkv_score_lse_merge) and score_mass_kernel
+    # (mmshiftkv_score_mass) of every layer (un-overlapped durations)
     step(n=1)
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(L)] for _ in range(args.steps)]
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(L)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     for s in range(args.steps):
         step(ev[s], n=1)
     torch.cuda.synchronize()
-    lse_ms = sum(ev[s][l][0].elapsed_time(ev[s][l][1]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
-    mass_ms = sum(ev[s][l][1].elapsed_time(ev[s][l][2]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
-    log("kernel timing on one stream: score_lse %.1f us, score_mass %.1f us per layer" % (lse_ms * 1e3, mass_ms * 1e3))
+
+    def ev_ms(i, j):
+        return sum(ev[s][l][i].elapsed_time(ev[s][l][j]) for s in range(args.steps) for l in range(L)) / (args.steps * L)
+    lse_ms, merge_ms, mass_ms = ev_ms(0, 1), ev_ms(1, 2), ev_ms(2, 3)
+    log("kernel timing on one stream: score_lse_kernel %.1f us, merge %.1f us, score_mass_kernel %.1f us per layer"
+        % (lse_ms * 1e3, merge_ms * 1e3, mass_ms * 1e3))
 
     # the other stages: each C-ABI call repeated back to back on one stream
     # (layer 0's inputs, the buffers of stream 0) behind a GPU-side spin long
@@ -574,15 +581,15 @@ def main():
         # leave layer 0's selection as a whole call made it
         bd.select_topk(*sel_args, out=bf["sel"], workspace=bf["ws_sel"])
         torch.cuda.synchronize()
-    stage_ms = {"build_proxies": stage_ms["build_proxies"], "score_lse": lse_ms, "score_mass": mass_ms,
-                **{k: v for k, v in stage_ms.items() if k != "build_proxies"}}
+    stage_ms = {"build_proxies": stage_ms["build_proxies"], "score_lse": lse_ms, "score_lse_merge": merge_ms,
+                "score_mass": mass_ms, **{k: v for k, v in stage_ms.items() if k != "build_proxies"}}
     log("per call (us): " + ", ".join("%s %.1f" % (k, v * 1e3) for k, v in stage_ms.items()))
 
     # algorithmic MFMA work of one scoring launch: 2*Gh*P*d flops per prompt
     # key per KV head (one proxy-by-key contraction), times B*Hkv*T keys
     flops = 2.0 * w.Gh * cfg.P * d * B * Hkv * T
-    # one launch = one C-ABI pass call: score_lse = score_lse_kernel + lse_combine_kernel,
-    # score_mass = score_mass_kernel
+    # one launch = one kernel: score_lse = score_lse_kernel (mmshiftkv_score_lse_blocks),
+    # score_mass = score_mass_kernel (mmshiftkv_score_mass)
     # algorithmic HBM bytes of the memory-bound stages, per layer (all heads)
     heads = B * Hkv
     eb = layers[0]["k"].element_size()
@@ -621,12 +628,14 @@ def main():
                    "budget": w.budget, "P": cfg.P, "G": cfg.G, "gamma": cfg.gamma, "tau": cfg.tau,
                    "lambda": cfg.lam, "mode": args.mode, "streams": n_streams},
         "stages_us_per_layer": {k: v * 1e3 for k, v in stage_ms.items()},
-        "stages_timing": "score passes: events around them in %d steps on one stream; the rest: %d back-to-back "
-                         "calls of one stage on one stream, queued behind a GPU spin (kernels + launch gaps)"
-                         % (args.steps, reps),
-        "non_score_us_per_layer": sum(v for k, v in stage_ms.items() if not k.startswith("score_")) * 1e3,
+        "stages_timing": "score_lse (score_lse_kernel), score_lse_merge (lse_combine_kernel) and score_mass "
+                         "(score_mass_kernel): events around each call in %d steps on one stream; the rest: %d "
+                         "back-to-back calls of one stage on one stream, queued behind a GPU spin (kernels + launch "
+                         "gaps)" % (args.steps, reps),
+        "non_score_us_per_layer": sum(v for k, v in stage_ms.items()
+                                      if k not in ("score_lse", "score_lse_merge", "score_mass")) * 1e3,
         "stage_hbm_frac": {k: stage_bytes[k] / (stage_ms[k] * 1e-3) / 1e9 / PEAK_HBM_GBS for k in stage_bytes},
-        "roofline": {"kernel": dom + " pass", "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+        "roofline": {"kernel": dom + "_kernel", "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(w.name, dom),
                      "timing": "%d steps on one stream after the throughput steps" % args.steps},

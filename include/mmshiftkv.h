@@ -180,6 +180,24 @@ int mmshiftkv_score_mass(const mmskv_shape *shape, const mmskv_params *params,
                          float *group_mass, float *mass, float *anchor,
                          void *workspace, size_t workspace_bytes, void *stream);
 
+/* The two halves of mmshiftkv_score_lse (the row normaliser of Sec. 3.2.2
+ * Eq. 7), same arguments and workspace, for callers that schedule or time
+ * them separately; in this order they are mmshiftkv_score_lse, and nothing
+ * else may write the workspace between them:
+ * mmshiftkv_score_lse_blocks: for every proxy and anchor row and every block
+ * of keys, the block's (max, sum of 2^(s - max)) pair (base 2), into the
+ * workspace; mmshiftkv_score_lse_merge: each row's log-sum-exp over all T
+ * keys from those pairs (the largest maximum as reference, every sum
+ * rescaled to it), into the workspace.  Errors as mmshiftkv_score_lse. */
+int mmshiftkv_score_lse_blocks(const mmskv_shape *shape, const mmskv_params *params,
+                               const uint16_t *proxies, const uint16_t *q_last,
+                               const void *k, int32_t k_dtype, const mmskv_strides *k_strides,
+                               void *workspace, size_t workspace_bytes, void *stream);
+int mmshiftkv_score_lse_merge(const mmskv_shape *shape, const mmskv_params *params,
+                              const uint16_t *proxies, const uint16_t *q_last,
+                              const void *k, int32_t k_dtype, const mmskv_strides *k_strides,
+                              void *workspace, size_t workspace_bytes, void *stream);
+
 /* Step 3 -- tau-sets, votes and budgeted selection (Sec. 3.2.2 Eqs. 9-10;
  * Sec. 3.2.3 Eq. 11; Algorithm 1).
  * VOTE: for each group, S_g = keys taken in (mass desc, index asc) order up to

@@ -22,7 +22,8 @@ MMSKV_F32, MMSKV_BF16 = 0, 1
 MMSKV_VOTE, MMSKV_MASS = 0, 1
 
 EXPORTED = ("mmshiftkv_build_proxies", "mmshiftkv_score_workspace", "mmshiftkv_score",
-            "mmshiftkv_score_lse", "mmshiftkv_score_mass", "mmshiftkv_select_workspace",
+            "mmshiftkv_score_lse", "mmshiftkv_score_lse_blocks", "mmshiftkv_score_lse_merge",
+            "mmshiftkv_score_mass", "mmshiftkv_select_workspace",
             "mmshiftkv_select_topk", "mmshiftkv_select_tau", "mmshiftkv_select_vote", "mmshiftkv_select_pick",
             "mmshiftkv_gather_kv", "mmshiftkv_status_string",
             "mmshiftkv_version", "mmshiftkv_hidden_stats_workspace", "mmshiftkv_hidden_stats",
@@ -77,6 +78,8 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_score_workspace.restype = SZ
     lib.mmshiftkv_score.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V, SZ, V]
     lib.mmshiftkv_score_lse.argtypes = [PS, PP, V, V, V, I32, PT, V, SZ, V]
+    lib.mmshiftkv_score_lse_blocks.argtypes = [PS, PP, V, V, V, I32, PT, V, SZ, V]
+    lib.mmshiftkv_score_lse_merge.argtypes = [PS, PP, V, V, V, I32, PT, V, SZ, V]
     lib.mmshiftkv_score_mass.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V, SZ, V]
     lib.mmshiftkv_score_noalloc.argtypes = [PS, PP, V, V, V, I32, PT, V, V, V, V]
     lib.mmshiftkv_select_workspace.argtypes = [PS, PP]
@@ -101,6 +104,7 @@ def load_library(path: str | None = None):
     lib.mmshiftkv_status_string.restype = ctypes.c_char_p
     lib.mmshiftkv_version.restype = ctypes.c_int
     for name in ("mmshiftkv_build_proxies", "mmshiftkv_score", "mmshiftkv_score_lse",
+                 "mmshiftkv_score_lse_blocks", "mmshiftkv_score_lse_merge",
                  "mmshiftkv_score_mass", "mmshiftkv_select_topk", "mmshiftkv_select_tau",
                  "mmshiftkv_select_vote", "mmshiftkv_select_pick", "mmshiftkv_gather_kv",
                  "mmshiftkv_hidden_stats", "mmshiftkv_hidden_proxies", "mmshiftkv_project_proxies",
@@ -316,11 +320,12 @@ def _score_call(which: str, proxies, q_last, k, cfg, W, out: ScoreOut | None, wo
     ws = workspace if workspace is not None else _ws(need, dev)
     strides = _strides4(k)
     with torch.cuda.device(dev):
-        if which == "lse":
-            rc = lib.mmshiftkv_score_lse(ctypes.byref(shape), ctypes.byref(prm), _p(proxies), _p(q_last),
-                                         _p(k), _dtype_code(k), ctypes.byref(strides), _p(ws),
-                                         ws.numel() * ws.element_size(), _stream(dev))
-            _check("mmshiftkv_score_lse", rc)
+        if which in ("lse", "lse_blocks", "lse_merge"):
+            name = "mmshiftkv_score_" + which
+            rc = getattr(lib, name)(ctypes.byref(shape), ctypes.byref(prm), _p(proxies), _p(q_last),
+                                    _p(k), _dtype_code(k), ctypes.byref(strides), _p(ws),
+                                    ws.numel() * ws.element_size(), _stream(dev))
+            _check(name, rc)
             return ws
         if out is None:
             gm = (torch.empty((B, Hkv, cfg.G, T), dtype=torch.float32, device=dev)
@@ -361,9 +366,14 @@ def score_noalloc(proxies, q_last, k, cfg: SelectionConfig, out: ScoreOut, W: in
     return out
 
 
-def score_lse(proxies, q_last, k, cfg: SelectionConfig, workspace: torch.Tensor, W: int = 1):
-    """mmshiftkv_score_lse: the row log-sum-exp pass (result kept in `workspace`)."""
-    return _score_call("lse", proxies, q_last, k, cfg, W, None, workspace)
+def score_lse(proxies, q_last, k, cfg: SelectionConfig, workspace: torch.Tensor, W: int = 1,
+              stage: str | None = None):
+    """mmshiftkv_score_lse: the row log-sum-exp pass (result kept in `workspace`);
+    with stage "blocks" or "merge" only that half (mmshiftkv_score_lse_blocks /
+    _merge), which must run in that order on one workspace."""
+    if stage not in (None, "blocks", "merge"):
+        raise ValueError("stage is None, 'blocks' or 'merge'")
+    return _score_call("lse" if stage is None else "lse_" + stage, proxies, q_last, k, cfg, W, None, workspace)
 
 
 def score_mass(proxies, q_last, k, cfg: SelectionConfig, workspace: torch.Tensor, W: int = 1,

@@ -267,15 +267,39 @@ size_t mmshiftkv_score_workspace(const mmskv_shape* shape, const mmskv_params* p
     return score_layout(shape, params).total;
 }
 
-int mmshiftkv_score_lse(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
-                        const uint16_t* q_last, const void* k, int32_t k_dtype,
-                        const mmskv_strides* k_strides, void* workspace, size_t workspace_bytes,
-                        void* stream) {
+static int score_lse_stages(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                            const uint16_t* q_last, const void* k, int32_t k_dtype,
+                            const mmskv_strides* k_strides, void* workspace, size_t workspace_bytes,
+                            void* stream, int stages) {
     ScoreArgs a;
     int rc = prepare_score(shape, params, proxies, q_last, k, k_dtype, k_strides, workspace,
                            workspace_bytes, &a);
     if (rc) return rc;
-    return status_of(launch_score_lse(a, static_cast<hipStream_t>(stream)));
+    return status_of(launch_score_lse(a, stages, static_cast<hipStream_t>(stream)));
+}
+
+int mmshiftkv_score_lse(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                        const uint16_t* q_last, const void* k, int32_t k_dtype,
+                        const mmskv_strides* k_strides, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+    return score_lse_stages(shape, params, proxies, q_last, k, k_dtype, k_strides, workspace, workspace_bytes,
+                            stream, kLseBlocks | kLseMerge);
+}
+
+int mmshiftkv_score_lse_blocks(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                               const uint16_t* q_last, const void* k, int32_t k_dtype,
+                               const mmskv_strides* k_strides, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+    return score_lse_stages(shape, params, proxies, q_last, k, k_dtype, k_strides, workspace, workspace_bytes,
+                            stream, kLseBlocks);
+}
+
+int mmshiftkv_score_lse_merge(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
+                              const uint16_t* q_last, const void* k, int32_t k_dtype,
+                              const mmskv_strides* k_strides, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+    return score_lse_stages(shape, params, proxies, q_last, k, k_dtype, k_strides, workspace, workspace_bytes,
+                            stream, kLseMerge);
 }
 
 int mmshiftkv_score_mass(const mmskv_shape* shape, const mmskv_params* params, const uint16_t* proxies,
@@ -308,7 +332,7 @@ int mmshiftkv_score(const mmskv_shape* shape, const mmskv_params* params, const 
     a.mass = mass;
     a.anchor = anchor;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = status_of(launch_score_lse(a, s));
+    rc = status_of(launch_score_lse(a, kLseBlocks | kLseMerge, s));
     if (rc) return rc;
     return status_of(launch_score_mass(a, s));
 }

@@ -152,7 +152,9 @@ int decode_max_rows();
 int decode_max_compact();
 
 hipError_t launch_build_proxies(const ProxyArgs& a, hipStream_t s);
-hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s);
+// Pass-1 stages: the per-(row, key block) partials, then their merge into L.
+constexpr int kLseBlocks = 1, kLseMerge = 2;
+hipError_t launch_score_lse(const ScoreArgs& a, int stages, hipStream_t s);
 hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s);
 // Selection stages: tau cuts and membership planes (VOTE) or clearing the
 // first-digit counts (MASS); votes, scores and first-digit counts; top-k.

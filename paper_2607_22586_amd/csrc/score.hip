@@ -1107,13 +1107,18 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
 }
 
 template <int D, int WAVES, int NS>
-hipError_t lse_impl(const ScoreArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((score_lse_kernel<D, WAVES, NS>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    dim3 g2((a.rows_pad + 255) / 256, a.B * a.Hkv);
-    hipLaunchKernelGGL(lse_combine_kernel, g2, dim3(256), 0, s, a);
-    return hipGetLastError();
+hipError_t lse_impl(const ScoreArgs& a, int stages, hipStream_t s) {
+    if (stages & kLseBlocks) {
+        hipLaunchKernelGGL((score_lse_kernel<D, WAVES, NS>), dim3(a.B * a.Hkv * a.n_kb), dim3(64 * WAVES), 0, s, a);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (stages & kLseMerge) {
+        dim3 g2((a.rows_pad + 255) / 256, a.B * a.Hkv);
+        hipLaunchKernelGGL(lse_combine_kernel, g2, dim3(256), 0, s, a);
+        return hipGetLastError();
+    }
+    return hipSuccess;
 }
 
 template <int D, int WAVES>
@@ -1154,14 +1159,14 @@ ScorePlan score_plan(int B, int Hkv, int T) {
     return p;
 }
 
-hipError_t launch_score_lse(const ScoreArgs& a, hipStream_t s) {
+hipError_t launch_score_lse(const ScoreArgs& a, int stages, hipStream_t s) {
     const int w = a.lse_waves, ns = a.lse_sub;
     if (a.d == 64) {
-        if (w == 8) return ns == 4 ? lse_impl<64, 8, 4>(a, s) : lse_impl<64, 8, 2>(a, s);
-        return lse_impl<64, 4, 2>(a, s);
+        if (w == 8) return ns == 4 ? lse_impl<64, 8, 4>(a, stages, s) : lse_impl<64, 8, 2>(a, stages, s);
+        return lse_impl<64, 4, 2>(a, stages, s);
     }
-    if (w == 8) return ns == 4 ? lse_impl<128, 8, 4>(a, s) : lse_impl<128, 8, 2>(a, s);
-    return lse_impl<128, 4, 2>(a, s);
+    if (w == 8) return ns == 4 ? lse_impl<128, 8, 4>(a, stages, s) : lse_impl<128, 8, 2>(a, stages, s);
+    return lse_impl<128, 4, 2>(a, stages, s);
 }
 
 hipError_t launch_score_mass(const ScoreArgs& a, hipStream_t s) {

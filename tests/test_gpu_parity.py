@@ -171,6 +171,8 @@ def test_per_head_budgets():
 
 
 def test_split_passes_equal_fused_and_deterministic():
+    """score = score_lse then score_mass = score_lse_blocks, score_lse_merge,
+    score_mass, bit for bit (and the same twice)."""
     x = wl.make_layer("qwen7b_4k", 0)
     cfg = bd.SelectionConfig(seed=2)
     q, k = x["q_win"].to(DEV), x["k"].to(DEV)
@@ -180,11 +182,17 @@ def test_split_passes_equal_fused_and_deterministic():
     bd.score_lse(prox, ql, k, cfg, ws, q.shape[2])
     b = bd.score_mass(prox, ql, k, cfg, ws, q.shape[2])
     c = bd.score(prox, ql, k, cfg, q.shape[2])
+    # the log-sum-exp pass as its two stage calls (blocks, then merge)
+    ws2 = torch.full_like(ws, 0x7F)
+    bd.score_lse(prox, ql, k, cfg, ws2, q.shape[2], stage="blocks")
+    bd.score_lse(prox, ql, k, cfg, ws2, q.shape[2], stage="merge")
+    e = bd.score_mass(prox, ql, k, cfg, ws2, q.shape[2])
     sa = bd.select_topk(a, cfg, 409, Hq=28, want_votes=True)
     sc = bd.select_topk(c, cfg, 409, Hq=28, want_votes=True)
     torch.cuda.synchronize()
     for u, w_ in ((a.group_mass, b.group_mass), (a.mass, b.mass), (a.anchor, b.anchor),
-                  (a.group_mass, c.group_mass), (a.anchor, c.anchor)):
+                  (a.group_mass, c.group_mass), (a.anchor, c.anchor),
+                  (a.group_mass, e.group_mass), (a.mass, e.mass), (a.anchor, e.anchor)):
         assert torch.equal(u, w_)
     assert torch.equal(sa.idx, sc.idx) and torch.equal(sa.votes, sc.votes)
 
