@@ -200,3 +200,30 @@ def test_select_stage_calls_equal_whole_call(T, mode):
     assert torch.equal(out.counts, whole.counts)
     if whole.votes is not None:
         assert torch.equal(out.votes, whole.votes)
+
+
+@pytest.mark.parametrize("Gh", [5, 6, 7, 8])
+def test_early_phases_equal_the_plain_pipeline(Gh):
+    """The early phases of both score passes (the first 8 proxy tiles taken
+    sub-tile by sub-tile while the keys arrive; bf16 keys, full key blocks)
+    sum in the pipeline's order, so they must give the same bits as the
+    plain pipeline.  fp32 keys that hold bf16 values are scored exactly like
+    the bf16 keys but always take the plain pipeline, so the two calls are
+    compared bit for bit, at a shape where both passes use their early
+    phase (batch 4, 4 KV heads, T = 16384: 1024-key pass-1 blocks and
+    8-wave pass-2 blocks)."""
+    B, Hkv, T, d, W = 4, 4, 16384, 128, 16
+    Hq = Gh * Hkv
+    g = torch.Generator(device="cpu").manual_seed(100 + Gh)
+    q = torch.randn((B, Hq, W, d), generator=g).to(torch.bfloat16).to(DEV)
+    k = torch.randn((B, Hkv, T, d), generator=g).to(torch.bfloat16).to(DEV)
+    cfg = bd.SelectionConfig(seed=7, layer=Gh)
+    prox, ql = bd.build_proxies(q, cfg, T, Hkv)
+    a = bd.score(prox, ql, k, cfg, W)
+    b = bd.score(prox, ql, k.float(), cfg, W)
+    torch.cuda.synchronize()
+    for u, v in ((a.group_mass, b.group_mass), (a.mass, b.mass), (a.anchor, b.anchor)):
+        assert torch.equal(u, v)
+    # and the masses are a softmax's: P * Gh in total per (b, c)
+    tot = a.mass.double().sum(dim=2)
+    assert torch.allclose(tot, torch.full_like(tot, cfg.P * Gh), rtol=1e-4)
