@@ -202,8 +202,8 @@ def test_select_stage_calls_equal_whole_call(T, mode):
         assert torch.equal(out.votes, whole.votes)
 
 
-@pytest.mark.parametrize("Gh", [5, 6, 7, 8])
-def test_early_phases_equal_the_plain_pipeline(Gh):
+@pytest.mark.parametrize("Gh,T", [(5, 16384), (6, 16384), (7, 16384), (8, 16384), (7, 16000)])
+def test_early_phases_equal_the_plain_pipeline(Gh, T):
     """The early phases of both score passes (the first 8 proxy tiles taken
     sub-tile by sub-tile while the keys arrive; bf16 keys, full key blocks)
     sum in the pipeline's order, so they must give the same bits as the
@@ -211,10 +211,11 @@ def test_early_phases_equal_the_plain_pipeline(Gh):
     the bf16 keys but always take the plain pipeline, so the two calls are
     compared bit for bit, at a shape where both passes use their early
     phase (batch 4, 4 KV heads, T = 16384: 1024-key pass-1 blocks and
-    8-wave pass-2 blocks)."""
-    B, Hkv, T, d, W = 4, 4, 16384, 128, 16
+    8-wave pass-2 blocks); at T = 16000 the last key block of each head is
+    ragged and takes the plain pipeline within the same launch."""
+    B, Hkv, d, W = 4, 4, 128, 16
     Hq = Gh * Hkv
-    g = torch.Generator(device="cpu").manual_seed(100 + Gh)
+    g = torch.Generator(device="cpu").manual_seed(100 + Gh + T)
     q = torch.randn((B, Hq, W, d), generator=g).to(torch.bfloat16).to(DEV)
     k = torch.randn((B, Hkv, T, d), generator=g).to(torch.bfloat16).to(DEV)
     cfg = bd.SelectionConfig(seed=7, layer=Gh)
