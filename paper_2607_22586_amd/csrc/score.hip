@@ -1022,9 +1022,15 @@ __device__ __forceinline__ void mass_body(const ScoreArgs& a, int head, int kb,
         }
         g_idx = 2;
         gs_h = kEarlyTiles % a.Gh;           // heads of proxy block 1 already summed
+        // the anchor tile (Gh <= 8 rows: one tile) goes to early slot 4,
+        // which nothing writes again, so the pipeline's end reads it there
+        // without a barrier of its own
+        St anc;
+        anc.load_anchor(a, hq0, 0);
         __syncthreads();
 #pragma unroll
         for (int k = 0; k < 3; ++k) pre[k].store(stage[k]);
+        anc.store(stage[kRing]);
         __syncthreads();
         read_frags<D>(stage[0], A, lane);
         mm = TileCursor{kEarlyTiles, kEarlyTiles / a.Gh, kEarlyTiles % a.Gh};
@@ -1058,11 +1064,16 @@ __device__ __forceinline__ void mass_body(const ScoreArgs& a, int head, int kb,
     // the pipeline: query head 32*ta + row of anchor tile ta
     float aacc[kSub] = {0.f, 0.f};
     for (int ta = 0; ta < n_anc; ++ta) {
-        __syncthreads();
-        st[0].load_anchor(a, hq0, ta);
-        st[0].store(stage[0]);
-        __syncthreads();
-        read_frags<D>(stage[0], A, lane);
+        if constexpr (EARLY) {
+            // staged after the early phase (n_anc == 1)
+            read_frags<D>(stage[kRing], A, lane);
+        } else {
+            __syncthreads();
+            st[0].load_anchor(a, hq0, ta);
+            st[0].store(stage[0]);
+            __syncthreads();
+            read_frags<D>(stage[0], A, lane);
+        }
         floatx16 ac[kSub];
         const floatx16 c0 = row_offsets(Llds + a.rows + 32 * ta, lane);
 #pragma unroll
