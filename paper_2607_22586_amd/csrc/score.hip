@@ -35,6 +35,16 @@
 // Workgroups are numbered so that all key blocks of one (b, c) land on the
 // same XCD (workgroup i runs on XCD i mod 8), keeping that head's proxies in
 // one L2.
+//
+// Early phase.  Every workgroup needs its whole key block before the
+// pipeline can start, and all of them fetch their keys at once at the start
+// of a pass.  Where the blocks allow it (full blocks of bf16 keys; pass 1
+// with four sub-tiles per wave, pass 2 with 8-wave blocks at d = 128 and
+// the paper's 16 proxies per group), the first 8 proxy tiles are staged in
+// LDS slots of their own before any key load is issued, and their chains run
+// sub-tile by sub-tile while the rest of the keys arrive, each round
+// fetching the next sub-tile's keys.  Per tile the sums are formed in the
+// pipeline's order, so the results are the same bits either way.
 #include <math.h>
 
 #include <utility>
