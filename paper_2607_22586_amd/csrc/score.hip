@@ -1118,8 +1118,10 @@ __global__ void __launch_bounds__(64 * WAVES) score_mass_kernel(ScoreArgs a) {
     int head, kb;
     block_work(a.mass_n_kb, head, kb);
     if constexpr (kEarly) {
+        // (the early phase and the pipeline's start load tiles 0 .. 12 as
+        // proxy tiles, so a head must have at least 16 of them)
         if ((kb + 1) * 64 * WAVES <= a.T && a.k_dtype == 1 && a.P == 16 * a.G && a.Gh >= 5 &&
-            a.Gh <= kEarlyTiles) {
+            a.Gh <= kEarlyTiles && (a.P / 32) * a.Gh >= 2 * kEarlyTiles) {
             mass_body<D, WAVES, true>(a, head, kb, stage, Llds);
             return;
         }

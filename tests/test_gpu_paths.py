@@ -202,8 +202,9 @@ def test_select_stage_calls_equal_whole_call(T, mode):
         assert torch.equal(out.votes, whole.votes)
 
 
-@pytest.mark.parametrize("Gh,T", [(5, 16384), (6, 16384), (7, 16384), (8, 16384), (7, 16000)])
-def test_early_phases_equal_the_plain_pipeline(Gh, T):
+@pytest.mark.parametrize("Gh,T,P", [(5, 16384, 512), (6, 16384, 512), (7, 16384, 512), (8, 16384, 512),
+                                    (7, 16000, 512), (7, 16384, 32)])
+def test_early_phases_equal_the_plain_pipeline(Gh, T, P):
     """The early phases of both score passes (the first 8 proxy tiles taken
     sub-tile by sub-tile while the keys arrive; bf16 keys, full key blocks)
     sum in the pipeline's order, so they must give the same bits as the
@@ -212,13 +213,15 @@ def test_early_phases_equal_the_plain_pipeline(Gh, T):
     compared bit for bit, at a shape where both passes use their early
     phase (batch 4, 4 KV heads, T = 16384: 1024-key pass-1 blocks and
     8-wave pass-2 blocks); at T = 16000 the last key block of each head is
-    ragged and takes the plain pipeline within the same launch."""
+    ragged and takes the plain pipeline within the same launch; with P = 32
+    (one 32-row tile per head) neither pass has tiles enough for its early
+    phase and both take the plain pipeline."""
     B, Hkv, d, W = 4, 4, 128, 16
     Hq = Gh * Hkv
-    g = torch.Generator(device="cpu").manual_seed(100 + Gh + T)
+    g = torch.Generator(device="cpu").manual_seed(100 + Gh + T + P)
     q = torch.randn((B, Hq, W, d), generator=g).to(torch.bfloat16).to(DEV)
     k = torch.randn((B, Hkv, T, d), generator=g).to(torch.bfloat16).to(DEV)
-    cfg = bd.SelectionConfig(seed=7, layer=Gh)
+    cfg = bd.SelectionConfig(seed=7, layer=Gh, P=P, G=P // 16)
     prox, ql = bd.build_proxies(q, cfg, T, Hkv)
     a = bd.score(prox, ql, k, cfg, W)
     b = bd.score(prox, ql, k.float(), cfg, W)
