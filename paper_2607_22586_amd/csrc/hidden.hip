@@ -13,16 +13,18 @@
 //                heads), fp64 -> fp32 -> bf16.
 // project        q[b, h, i, :] = W_Q^(h) H~[b, i, :]: a bf16 GEMM of the
 //                (B*P) x D samples against the (Hq*d) x D weights (both with
-//                the reduction dimension contiguous) on
-//                v_mfma_f32_32x32x16_bf16 with fp32 accumulation: 128x128
-//                output tiles, 64-wide k steps double buffered in LDS through
-//                registers, four waves of 64x64; the epilogue goes through
-//                LDS so that the rotary pairs (e, e + d/2) of a head meet in
-//                one thread, then multiplies by the query scale
-//                log2(e)/sqrt(d) in fp64 and rounds to bf16.
+//                the reduction dimension contiguous) with fp32 accumulation.
+//                Without rotary tables, on full 128 x 224 tiles: four waves
+//                of 64 x 112 on v_mfma_f32_16x16x32_bf16.  Otherwise 128x128
+//                tiles of four 64x64 waves on v_mfma_f32_32x32x16_bf16, the
+//                epilogue through LDS so that the rotary pairs (e, e + d/2)
+//                of a head meet in one thread.  Both multiply by the query
+//                scale log2(e)/sqrt(d) in fp64 and round to bf16.
 #pragma clang fp contract(off)
 
 #include <math.h>
+
+#include <type_traits>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -460,6 +462,157 @@ __global__ void __launch_bounds__(kGemmThreads) project_dma_kernel(ProjectArgs p
     project_epilogue(p, acc, lds, m0, n0, wm, wn, lane);
 }
 
+// Full tiles without rotary tables: 128 x 224 output tiles (the benchmark
+// shape has 16 x 16 of them, one per CU), four waves of 64 x 112 on
+// v_mfma_f32_16x16x32_bf16 (4 x 7 accumulator blocks per wave).  A k step is
+// 64 wide and lands in one of two LDS stages by direct loads: each wave issues
+// 11 of the step's 44 loads of 8 rows x 128 bytes, from a uniform base
+// advanced per step plus loop-invariant 32-bit lane offsets (chunk c of row r
+// at slot c ^ (r & 7)).  A step runs its two 32-wide halves back to back: the
+// A fragments of the next half are read before a half's 28 MFMAs, and each W
+// fragment is refilled right after the four MFMAs that last read it.  The
+// barrier sits between the halves: by then every wave has its own loads of
+// the next stage and its reads of the current one complete, so after it the
+// next stage can be read and the loads two steps ahead overwrite the current
+// stage.
+constexpr int kWM = 128, kWN = 224, kWK = 64;
+constexpr int kWRow = kWK * 2;                      // bytes per staged row
+constexpr int kWTileA = kWM * kWRow;                // the A rows of a stage
+constexpr int kWStage = (kWM + kWN) * kWRow;        // 45,056 bytes
+constexpr int kWLoads = (kWM + kWN) / 8 / 4;        // loads per wave and stage
+constexpr int kWLd = kWN + 4;                       // epilogue row pitch (floats)
+constexpr int kWLds = 2 * kWStage > kWM * kWLd * 4 ? 2 * kWStage : kWM * kWLd * 4;
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// s_waitcnt vmcnt(0) lgkmcnt(0)
+__device__ __forceinline__ void wait_vm_lgkm0() { __builtin_amdgcn_s_waitcnt(0x0070); }
+
+__global__ void __launch_bounds__(kGemmThreads) project_wide_kernel(ProjectArgs p) {
+    __shared__ u32x4 lds[kWLds / 16];
+    char* base = reinterpret_cast<char*>(lds);
+    const int nN = p.N / kWN;
+    const int m0 = static_cast<int>(blockIdx.x) / nN * kWM, n0 = static_cast<int>(blockIdx.x) % nN * kWN;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave), lane = lane_id();
+    const int wm = wave >> 1, wn = wave & 1;
+    const int n_k = p.K / kWK;                      // at least 2 (checked by the host)
+    floatx4 acc[4][7];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 7; ++y) acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // load j of a stage: rows 8 (wave + 4 j) .. + 7 of the A tile (j < 4) or
+    // of the W tile (j >= 4, less 16 groups); lane -> row + (lane >> 3), slot lane & 7
+    uint32_t voff[kWLoads];
+#pragma unroll
+    for (int j = 0; j < kWLoads; ++j) {
+        const int g = wave + 4 * j - (j < 4 ? 0 : kWM / 8);
+        const int r = 8 * g + (lane >> 3);
+        voff[j] = static_cast<uint32_t>(((j < 4 ? m0 : n0) + r) * p.K * 2 + 16 * ((lane & 7) ^ (r & 7)));
+    }
+    auto loads = [&](int k0, char* stage) {
+        const char* ab = reinterpret_cast<const char*>(p.a) + 2 * k0;
+        const char* wb = reinterpret_cast<const char*>(p.w) + 2 * k0;
+#pragma unroll
+        for (int j = 0; j < kWLoads; ++j) {
+            const int g = wave + 4 * j - (j < 4 ? 0 : kWM / 8);
+            char* dst = stage + (j < 4 ? 0 : kWTileA) + 8 * g * kWRow;
+            __builtin_amdgcn_global_load_lds((j < 4 ? ab : wb) + voff[j],
+                                             (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+        }
+    };
+    // fragment rows wm*64 + 16x + (lane & 15) and wn*112 + 16y + (lane & 15)
+    // (both = lane & 7 mod 8), 16-byte chunk 4 h + (lane >> 4) of half h
+    const int rA = wm * 64 + (lane & 15), rW = wn * 112 + (lane & 15);
+    const int oA0 = rA * kWRow + 16 * ((lane >> 4) ^ (lane & 7));
+    const int oA1 = rA * kWRow + 16 * ((4 + (lane >> 4)) ^ (lane & 7));
+    const int oW0 = kWTileA + rW * kWRow + 16 * ((lane >> 4) ^ (lane & 7));
+    const int oW1 = kWTileA + rW * kWRow + 16 * ((4 + (lane >> 4)) ^ (lane & 7));
+    auto rd = [&](const char* q) { return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(q)); };
+    bf16x8 fa0[4], fa1[4], fw[7];
+
+    loads(0, base);
+    loads(kWK, base + kWStage);
+    wait_vm<kWLoads>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int x = 0; x < 4; ++x) fa0[x] = rd(base + oA0 + x * 16 * kWRow);
+#pragma unroll
+    for (int y = 0; y < 7; ++y) fw[y] = rd(base + oW0 + y * 16 * kWRow);
+
+    // step ks on stage st (half 0's fragments already in fa0 / fw); nst is
+    // the next stage; the loads of step ks + 2 go to st
+    auto step = [&](int ks, char* st, const char* nst, auto last_tag) {
+        constexpr bool kLast = decltype(last_tag)::value;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) fa1[x] = rd(st + oA1 + x * 16 * kWRow);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int y = 0; y < 7; ++y) {
+#pragma unroll
+            for (int x = 0; x < 4; ++x) acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa0[x], fw[y], acc[x][y], 0, 0, 0);
+            fw[y] = rd(st + oW1 + y * 16 * kWRow);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if constexpr (!kLast) {
+            wait_vm_lgkm0();
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (ks + 2 < n_k) loads((ks + 2) * kWK, st);
+#pragma unroll
+            for (int x = 0; x < 4; ++x) fa0[x] = rd(nst + oA0 + x * 16 * kWRow);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int y = 0; y < 7; ++y) {
+#pragma unroll
+            for (int x = 0; x < 4; ++x) acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa1[x], fw[y], acc[x][y], 0, 0, 0);
+            if constexpr (!kLast) fw[y] = rd(nst + oW0 + y * 16 * kWRow);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    int ks = 0;
+    for (; ks + 2 < n_k; ks += 2) {
+        step(ks, base, base + kWStage, std::false_type{});
+        step(ks + 1, base + kWStage, base, std::false_type{});
+    }
+    if (ks + 1 < n_k) {
+        step(ks, base, base + kWStage, std::false_type{});
+        ++ks;
+    }
+    step(ks, base + (ks & 1) * kWStage, nullptr, std::true_type{});
+
+    // epilogue: the fp32 tile through LDS (every wave's stage reads are done),
+    // then 8 consecutive columns of one row per thread and group: the query
+    // scale in fp64, bf16, one 16-byte store into the proxies' layout
+    asm volatile("" ::: "memory");
+    __syncthreads();
+    float* tile = reinterpret_cast<float*>(lds);
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 7; ++y)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                tile[(wm * 64 + 16 * x + 4 * (lane >> 4) + i) * kWLd + wn * 112 + 16 * y + (lane & 15)] = acc[x][y][i];
+    __syncthreads();
+    constexpr int kGroups = kWN / 8;
+    for (int g = static_cast<int>(threadIdx.x); g < kWM * kGroups; g += kGemmThreads) {
+        const int r = g / kGroups, c = 8 * (g % kGroups);
+        const int m = m0 + r, n = n0 + c;
+        const int bb = m / p.P, i = m % p.P, h = n / p.d, e = n % p.d;
+        const float* src = tile + r * kWLd + c;
+        u32x4 v;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            v[q] = f32_to_bf16_bits(scaled(src[2 * q], p.scale)) | (f32_to_bf16_bits(scaled(src[2 * q + 1], p.scale)) << 16);
+        *reinterpret_cast<u32x4*>(p.out + ((static_cast<int64_t>(bb) * p.Hq + h) * p.P + i) * p.d + e) = v;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_hidden_stats(const HiddenArgs& a, hipStream_t s) {
@@ -480,6 +633,13 @@ hipError_t launch_hidden_proxies(const HiddenArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_project(const ProjectArgs& p, hipStream_t s) {
+    // without rotary tables, on full 128 x 224 tiles whose lane offsets fit
+    // in 31 bits: one 128 x 224 tile per workgroup
+    if (p.cos == nullptr && p.M % kWM == 0 && p.N % kWN == 0 && p.K % kWK == 0 && p.K >= 2 * kWK &&
+        static_cast<int64_t>(p.M > p.N ? p.M : p.N) * p.K * 2 < (static_cast<int64_t>(1) << 31)) {
+        hipLaunchKernelGGL(project_wide_kernel, dim3((p.M / kWM) * (p.N / kWN)), dim3(kGemmThreads), 0, s, p);
+        return hipGetLastError();
+    }
     dim3 g((p.M + kBM - 1) / kBM, (p.N + kBN - 1) / kBN);
     // full tiles: 64-wide k steps in two LDS stages loaded directly (two
     // workgroups per CU; deeper rings of 32- or 64-wide steps leave one per

@@ -122,7 +122,9 @@ def test_hidden_proxies_bit_exact(B, P, D, gamma, layer):
 # ---------------------------------------------------------------- Eq. 6
 @pytest.mark.parametrize("B,P,D,Hq,d,rope", [
     (2, 64, 3584, 28, 128, False), (3, 40, 200, 3, 64, False), (1, 50, 136, 2, 128, True),
-    (2, 33, 3584, 4, 64, True), (1, 1, 8, 1, 64, False)])
+    (2, 33, 3584, 4, 64, True), (1, 1, 8, 1, 64, False),
+    # full 128 x 224 tiles without rotation, 2, 3 and 5 k steps of 64
+    (2, 128, 128, 7, 64, False), (1, 128, 192, 14, 64, False), (1, 256, 320, 7, 64, False)])
 def test_projection_within_bound(B, P, D, Hq, d, rope):
     rng_in = wl.custom_hidden(B, P, D, Hq, d, seed=B * 1000 + P)
     hp = rng_in["hidden"]                        # any bf16 [B, P, D] serves as samples
