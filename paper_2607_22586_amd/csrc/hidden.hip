@@ -482,6 +482,10 @@ constexpr int kWStage = (kWM + kWN) * kWRow;        // 45,056 bytes
 constexpr int kWLoads = (kWM + kWN) / 8 / 4;        // loads per wave and stage
 constexpr int kWLd = kWN + 4;                       // epilogue row pitch (floats)
 constexpr int kWLds = 2 * kWStage > kWM * kWLd * 4 ? 2 * kWStage : kWM * kWLd * 4;
+// the four waves issue the 8-row groups of a stage in turn: the A tile's 16
+// groups are loads j < 4 of every wave, the W tile's 28 the rest
+static_assert((kWM + kWN) % 32 == 0 && kWM / 8 == 4 * 4 && kGemmThreads == 4 * kWave, "load split");
+static_assert(kWN == 2 * 112 && kWM == 2 * 64, "four waves of 64 x 112");
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 // s_waitcnt vmcnt(0) lgkmcnt(0)
