@@ -115,15 +115,35 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
             st[d + j] = sg;
         }
     }
+    // Draws of this thread's first kPreItems items, made before the
+    // statistics are published (they do not depend on them): every wave
+    // draws while the statistics lanes run their serial sums.  The draws are
+    // fp32 values, so keeping them as fp32 and widening later is exact.
+    constexpr int kPreItems = 4;
+    const int n_items = a.P * qpb;
+    float zp[kPreItems][4], zp2[kPreItems][4];
+    if (one_chunk) {
+#pragma unroll
+        for (int k = 0; k < kPreItems; ++k) {
+            const int item = tid + k * kProxyThreads;
+            if (item < n_items) {
+                const int i = item / qpb, jq = q0 + item % qpb;
+                double z[4];
+                normal_quad(a.key0, a.key1, b, a.layer, h, i, jq, z);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) zp[k][e] = static_cast<float>(z[e]);
+                if (rope) normal_quad(a.key0, a.key1, b, a.layer, h, i, jq + d / 8, z);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) zp2[k][e] = rope ? static_cast<float>(z[e]) : 0.f;
+            }
+        }
+    }
     __syncthreads();
 
     uint16_t* out_head = a.proxies + (static_cast<int64_t>(b) * a.Hq + h) * a.P * d;
-    for (int item = tid; item < a.P * qpb; item += kProxyThreads) {
-        const int i = item / qpb;
-        const int jq = q0 + item % qpb;
+    // proxy i, quad jq from its draws z (and z2, the partner quad's, with rotary placement)
+    auto emit = [&](int i, int jq, const double (&z)[4], const double (&z2)[4]) {
         uint16_t* row = out_head + static_cast<int64_t>(i) * d;
-        double z[4];
-        normal_quad(a.key0, a.key1, b, a.layer, h, i, jq, z);
         double x[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -142,8 +162,7 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
         } else {
             // partner dims j + d/2 come from quad jq + d/8
             const int jq2 = jq + d / 8;
-            double z2[4], y[4];
-            normal_quad(a.key0, a.key1, b, a.layer, h, i, jq2, z2);
+            double y[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int j = 4 * jq2 + e;
@@ -169,6 +188,28 @@ __global__ void __launch_bounds__(kProxyThreads) build_proxies_kernel(ProxyArgs 
             *reinterpret_cast<uint2*>(row + 4 * jq) = pl;
             *reinterpret_cast<uint2*>(row + half + 4 * jq) = ph;
         }
+    };
+    int item = tid;
+    if (one_chunk) {
+#pragma unroll
+        for (int k = 0; k < kPreItems; ++k, item += kProxyThreads) {
+            if (item < n_items) {
+                double z[4], z2[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    z[e] = static_cast<double>(zp[k][e]);
+                    z2[e] = static_cast<double>(zp2[k][e]);
+                }
+                emit(item / qpb, q0 + item % qpb, z, z2);
+            }
+        }
+    }
+    for (; item < n_items; item += kProxyThreads) {
+        const int i = item / qpb, jq = q0 + item % qpb;
+        double z[4], z2[4] = {0.0, 0.0, 0.0, 0.0};
+        normal_quad(a.key0, a.key1, b, a.layer, h, i, jq, z);
+        if (rope) normal_quad(a.key0, a.key1, b, a.layer, h, i, jq + d / 8, z2);
+        emit(i, jq, z, z2);
     }
 
     // anchor query: window row W-1, all dims, by workgroup 0
